@@ -1,0 +1,448 @@
+"""Plain fp64 CPU oracle of TrimMoE's per-layer adaptive-depth MoE step.
+
+TEST INFRASTRUCTURE ONLY: imported by the tests, ``__graft_entry__.smoke()``
+and the CPU-baseline leg of ``bench.py``; never by the product path.
+
+It computes, token by token and layer by layer, what the online algorithm of
+TrimMoE (arXiv 2608.00573, Sec. V, Algorithm 2 in Table II) decides and
+what the MoE layer then outputs, restricted to one device and to the myopic
+horizon H = 1 (Sec. V-E: with H = 1 the look-ahead term vanishes):
+
+* routing, gating weights and layer importance   -- Sec. III-B, Eq. (4)
+* skip degradation Lambda = rho(I)                -- Sec. III-B, Eq. (5)
+* substitution loss Q                             -- Sec. III-A, Eq. (3)
+* per-step execute / skip costs                   -- Sec. V-A, Eq. (31), (32)
+* per-token budget and feasible action set        -- Sec. V-B, Eq. (33), (34)
+* transmission necessity and importance admission -- Sec. V-C, Eq. (35)
+* action choice and state update                  -- Sec. V-E, Eq. (40)-(42)
+* exit head confidence and exit gate              -- Sec. III-C, Eq. (7)-(9)
+* residual bypass of a skipped layer              -- Sec. III-B
+
+Readings taken where the paper is silent or ambiguous (each is also listed,
+with its reason, in the design notes of the repository):
+
+A1  exit head: xi = max softmax(W_exit h + b) (a vocabulary head); the
+    paper's own linear+sigmoid head (Sec. IV-A) is the "sigmoid" mode.
+A2  exit takes effect right after an executed layer l with xi_l >= p_J;
+    the token then runs no later layer.  xi is not evaluated after the last
+    layer, nor after a skipped layer (Eq. (9)).
+A3  at H = 1 an admissible exit is always taken (its cost is 0, every
+    remaining layer costs > 0; Sec. V-A).
+A4  comparisons are non-strict exactly as printed: xi >= p_J (Eq. (8)),
+    I <= theta (Sec. V-C), D + Q <= budget (Eq. (34)).
+A5  I = sum of the full-softmax router probabilities of the top-k experts
+    (router bias included), before any renormalisation.
+A6  slot weight w = p_e, or p_e / I when top-k renormalisation is on; a
+    substitute inherits its target's weight.
+A7  phi(x) = min(1, phi_scale * x) in Eq. (3).
+A8  rho(I) = min(1, s_l * I) with a per-layer slope s_l (an input).
+A9  the budget is per token (Eq. (33) already divides by the token count).
+A10 one device: the token never moves; "local" experts are the ones this
+    device holds, a remote expert is a round trip.
+A11 with top-k > 1 every routed slot is resolved on its own under the one
+    token budget; Gamma > 0 iff no feasible all-local assignment exists; a
+    skip bypasses all slots of the layer.
+A12 normalised per-slot delays t_local, t_remote; the execute cost is
+    omega_T * sum of slot delays + omega_D * sum Q / budget.
+A13 a remote slot's only useful substitute is its minimum-Q local expert
+    with Sim >= sim_min (ties to the lower id): any other local substitute
+    has the same delay and spends more budget.
+A14 ties: lower expert id in top-k; among execute options fewer
+    substitutions, then the lower slot bitmask; execute before skip.
+A15 slots that end on the same expert are merged into one row whose weight
+    is the sum, added in rank order.
+A16 the shared expert (if any) is always local, takes no part in I or in
+    substitution, and is bypassed together with the routed ones by a skip.
+A17 budget = 0: only zero-loss options are feasible and the quality terms
+    of the costs are taken as 0.
+A18 a skip charges only Lambda; an exit charges nothing (Eq. (17)).
+A19 h_{l+1} = h_l + MoE(h_l): no normalisation inside the step.
+
+Precision (bf16 storage): inputs are the stored bf16 values widened to
+fp64; products and sums are fp64; the expert activation is rounded to bf16
+(round-to-nearest-even) before the down projection; h is rounded to bf16
+once per executed layer after the weighted sum.  In fp32 storage mode only
+h is rounded, to fp32.
+
+Every deciding margin is recorded so a caller can tell which decisions are
+too close to call at fp32 accuracy (the "band").
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+ACT_INACTIVE, ACT_EXEC, ACT_SKIP = 0, 1, 2
+KIND_NONE, KIND_LOCAL, KIND_SUB, KIND_REMOTE = -1, 0, 1, 2
+
+_INF = float("inf")
+
+
+# ----------------------------------------------------------------------------
+# rounding
+# ----------------------------------------------------------------------------
+def round_bf16(x):
+    """Round fp64 values to the nearest bf16 (ties to even), returned as fp64.
+
+    Operates on the fp64 bit pattern directly (52 -> 7 mantissa bits), so
+    there is no intermediate fp32 rounding.  Valid for finite values whose
+    magnitude is 0 or at least 2^-126 (bf16 normal range), which covers all
+    values of this step; smaller nonzero magnitudes raise.
+    """
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+    tiny = (a != 0) & (np.abs(a) < 2.0 ** -126)
+    if np.any(tiny) or not np.all(np.isfinite(a)):
+        raise ValueError("round_bf16: value outside the supported range")
+    b = a.view(np.uint64)
+    lsb = (b >> np.uint64(45)) & np.uint64(1)
+    b = (b + np.uint64((1 << 44) - 1) + lsb) & ~np.uint64((1 << 45) - 1)
+    return b.view(np.float64)
+
+
+def round_f32(x):
+    return np.asarray(x, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+# ----------------------------------------------------------------------------
+# Eq. (3): substitution loss, and the per-layer substitute table (A13)
+# ----------------------------------------------------------------------------
+def q_loss(sim: float, phi_scale: float) -> float:
+    """Q_l(r, k) for k != r, Eq. (3) with phi(x) = min(1, phi_scale * x)."""
+    return min(1.0, phi_scale * (1.0 - sim) / 2.0)
+
+
+def substitutes(sim, local, phi_scale: float, sim_min: float):
+    """Best local substitute c(e) for every expert e of one layer.
+
+    Returns (c, q, margins): c[e] = argmin over local j != e with
+    Sim[e][j] >= sim_min of Q(e, j) (ties to the lower j), -1 if none;
+    q[e] = Q(e, c[e]); margins[e] = the smallest deciding margin of that
+    choice (gap to the second-best candidate, distance of any candidate's
+    Sim to sim_min).
+    """
+    E = len(local)
+    c = [-1] * E
+    q = [math.nan] * E
+    margins = [_INF] * E
+    for e in range(E):
+        cands = []
+        m = _INF
+        for j in range(E):
+            if j == e or not local[j]:
+                continue
+            s = float(sim[e][j])
+            m = min(m, abs(s - sim_min))
+            if s >= sim_min:
+                cands.append((q_loss(s, phi_scale), j))
+        cands.sort()
+        if cands:
+            c[e] = cands[0][1]
+            q[e] = cands[0][0]
+            if len(cands) > 1:
+                m = min(m, cands[1][0] - cands[0][0])
+        margins[e] = m
+    return c, q, margins
+
+
+# ----------------------------------------------------------------------------
+# Eq. (4): routing, gating weights, importance
+# ----------------------------------------------------------------------------
+def route(z, k: int, normalize: bool):
+    """Top-k of the router logits z (ties to the lower id).
+
+    Returns (S, w, I, p, margin): S in rank order, slot weights w, the
+    importance I (Eq. (4), reading A5), the full softmax p and the smallest
+    gap between consecutive logits among the first k+1 ranks.
+    """
+    z = np.asarray(z, dtype=np.float64)
+    order = np.argsort(-z, kind="stable")
+    S = [int(e) for e in order[:k]]
+    ex = np.exp(z - z.max())
+    p = ex / ex.sum()
+    I = float(sum(p[e] for e in S))
+    w = [float(p[e] / I) if normalize else float(p[e]) for e in S]
+    ranked = z[order[: min(k + 1, len(z))]]
+    margin = float(np.min(ranked[:-1] - ranked[1:])) if len(ranked) > 1 else _INF
+    return S, w, I, p, margin
+
+
+# ----------------------------------------------------------------------------
+# Algorithm 2 at H = 1 for one token at one layer
+# ----------------------------------------------------------------------------
+def decide(S, w, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol):
+    """Execute/skip decision and server-expert selection for one token.
+
+    Implements Eq. (31), (32), (34), (35), the importance admission of
+    Sec. V-C and the argmin of Eq. (40) at H = 1 (readings A8-A18).
+    Returns a dict with the action, per-slot (target, exec, kind, weight),
+    the merged execute rows, the degradation charged, and the margins.
+    """
+    k = len(S)
+    wt = pol["omega_t"]
+    wd = 1.0 - wt
+    t_loc, t_rem = pol["t_local"], pol["t_remote"]
+    margins = []
+
+    kinds0 = []
+    qs = []
+    n_local = n_remote = 0
+    rsub = []  # ranks of remote slots that have a local substitute
+    for r, e in enumerate(S):
+        if local[e]:
+            kinds0.append(KIND_LOCAL)
+            n_local += 1
+            qs.append(0.0)
+        else:
+            kinds0.append(KIND_REMOTE)
+            n_remote += 1
+            qs.append(sub_q[e] if sub_c[e] >= 0 else math.nan)
+            if sub_c[e] >= 0:
+                rsub.append(r)
+
+    def quality(sq):
+        return wd * sq / budget if budget > 0 else 0.0
+
+    # enumerate execute assignments A (bitmask over slot ranks, bits only on
+    # substitutable remote slots); Eq. (34) budget filter, Eq. (31) cost
+    options = []
+    for sel in range(1 << len(rsub)):
+        mask = 0
+        sq = 0.0
+        for i, r in enumerate(rsub):
+            if sel >> i & 1:
+                mask |= 1 << r
+                sq += qs[r]
+        n_sub = bin(mask).count("1")
+        if mask:
+            margins.append(abs(budget - d_hat - sq))
+        if d_hat + sq <= budget:
+            f = wt * ((n_local + n_sub) * t_loc + (n_remote - n_sub) * t_rem) \
+                + quality(sq)
+            options.append((f, n_sub, mask, sq))
+    options.sort()
+    best_f, best_nsub, best_mask, best_sq = options[0]
+    if len(options) > 1:
+        margins.append(options[1][0] - options[0][0])
+
+    # Eq. (35): Gamma > 0 iff no feasible assignment leaves no remote slot
+    all_local_feasible = any(n_sub == n_remote for (_, n_sub, _, _) in options)
+    gamma_pos = not all_local_feasible
+
+    lam = min(1.0, slope * I)  # Eq. (5), reading A8
+    skip = False
+    if gamma_pos:
+        margins.append(abs(I - theta))
+        margins.append(abs(budget - d_hat - lam))
+        if I <= theta and d_hat + lam <= budget:
+            f_skip = quality(lam)  # Eq. (32)
+            margins.append(abs(best_f - f_skip))
+            skip = f_skip < best_f  # tie goes to execute (A14)
+
+    out = dict(target=list(S), weight=list(w), importance=I, lam=lam,
+               gamma_pos=gamma_pos, margins=margins)
+    if skip:
+        out.update(action=ACT_SKIP, exec=[-1] * k, kind=[KIND_NONE] * k,
+                   d_inc=lam, rows=[])
+        return out
+    exec_ids, kinds = [], []
+    for r, e in enumerate(S):
+        if best_mask >> r & 1:
+            exec_ids.append(sub_c[e])
+            kinds.append(KIND_SUB)
+        else:
+            exec_ids.append(e)
+            kinds.append(kinds0[r])
+    rows = []  # merged (expert, weight), first-occurrence rank order (A15)
+    for x, wx in zip(exec_ids, w):
+        for i, (y, wy) in enumerate(rows):
+            if y == x:
+                rows[i] = (y, wy + wx)
+                break
+        else:
+            rows.append((x, wx))
+    out.update(action=ACT_EXEC, exec=exec_ids, kind=kinds, d_inc=best_sq,
+               rows=rows)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# expert FFN and exit head
+# ----------------------------------------------------------------------------
+def _silu(g):
+    return g / (1.0 + np.exp(-g))
+
+
+def expert_ffn(X, w_up, w_gate, w_down, act: str, bf16: bool):
+    """E(x) = W_down act(W_up x) for the rows of X (fp64).
+
+    ReLU: act = relu(W_up x).  SwiGLU: act = silu(W_gate x) * (W_up x).
+    With bf16 storage the activation is rounded to bf16 before W_down.
+    """
+    u = X @ w_up.T
+    if act == "relu":
+        a = np.maximum(u, 0.0)
+    else:
+        a = _silu(X @ w_gate.T) * u
+    if bf16:
+        a = round_bf16(a)
+    return a @ w_down.T
+
+
+def exit_confidence(H, w_exit, b_exit, mode: str):
+    """xi for the rows of H, Eq. (7).
+
+    softmax mode (A1): xi = max_v softmax(z)_v = 1 / sum_v exp(z_v - max z)
+    with z = W_exit h + b; sigmoid mode: xi = 1 / (1 + exp(-(w . h + b))).
+    """
+    z = H @ w_exit.T
+    if b_exit is not None:
+        z = z + b_exit
+    if mode == "sigmoid":
+        return 1.0 / (1.0 + np.exp(-z[:, 0]))
+    m = z.max(axis=1, keepdims=True)
+    return 1.0 / np.exp(z - m).sum(axis=1)
+
+
+# ----------------------------------------------------------------------------
+# state, layer, stack
+# ----------------------------------------------------------------------------
+def init_state(h0, n_layers: int):
+    """Algorithm 2 initialisation: D = 0, every token active (Eq. (6))."""
+    T = h0.shape[0]
+    return dict(h=np.array(h0, dtype=np.float64, copy=True),
+                d_acc=np.zeros(T), active=list(range(T)),
+                exit_layer=np.full(T, n_layers, dtype=np.int64),
+                xi=np.full(T, math.nan))
+
+
+def layer_step(model, l: int, pol, state, token_budget=None, token_p_exit=None):
+    """One MoE layer l (0-based) for every active token; returns the trace.
+
+    ``state`` is updated in place: h, d_acc, the active list (in token
+    order), exit_layer and xi.  ``token_budget`` / ``token_p_exit``
+    optionally give a per-token budget / confidence requirement.
+    """
+    L = model["layers"][l]
+    N, E, k = model["n_layers"], model["n_experts"], model["top_k"]
+    T = state["h"].shape[0]
+    bf16 = model["dtype"] == "bf16"
+    local = [bool(v) for v in L["local_mask"]]
+    sub_c, sub_q, sub_m = substitutes(L["sim"], local, pol["phi_scale"],
+                                      pol["sim_min"])
+
+    tr = dict(action=np.zeros(T, np.int8),
+              target=np.full((T, k), -1, np.int16),
+              exec=np.full((T, k), -1, np.int16),
+              kind=np.full((T, k), KIND_NONE, np.int8),
+              gate=np.full((T, k), math.nan),
+              importance=np.full(T, math.nan),
+              xi=np.full(T, math.nan), d_acc=np.full(T, math.nan),
+              margin=np.full(T, _INF), rows={})
+
+    act_list = list(state["active"])
+    h = state["h"]
+    if act_list:
+        Z = h[act_list] @ L["w_router"].T
+        if L["b_router"] is not None:
+            Z = Z + L["b_router"]
+
+    execd = []
+    for i, q in enumerate(act_list):
+        S, w, I, _, m_route = route(Z[i], k, bool(model["normalize_topk"]))
+        budget = pol["budget"] if token_budget is None else float(token_budget[q])
+        dec = decide(S, w, I, local, sub_c, sub_q, state["d_acc"][q], budget,
+                     L["theta"], L["skip_slope"], pol)
+        m = min([m_route] + dec["margins"]
+                + [sub_m[e] for e in S if not local[e]])
+        tr["margin"][q] = m
+        tr["action"][q] = dec["action"]
+        tr["target"][q] = S
+        tr["gate"][q] = w
+        tr["importance"][q] = I
+        tr["exec"][q] = dec["exec"]
+        tr["kind"][q] = dec["kind"]
+        state["d_acc"][q] += dec["d_inc"]  # Eq. (41) / (42)
+        if dec["action"] == ACT_EXEC:
+            execd.append(q)
+            tr["rows"][q] = dec["rows"]
+
+    # grouped expert FFN over the executed rows, then the residual update
+    if execd:
+        upd = np.zeros((len(execd), h.shape[1]))
+        pos = {q: i for i, q in enumerate(execd)}
+        by_expert = {}
+        for q in execd:
+            for x, wx in tr["rows"][q]:
+                by_expert.setdefault(x, []).append((q, wx))
+        X_all = h[execd]
+        for x, lst in by_expert.items():
+            idx = [pos[q] for q, _ in lst]
+            Y = expert_ffn(X_all[idx], L["w_up"][x],
+                           None if L["w_gate"] is None else L["w_gate"][x],
+                           L["w_down"][x], model["act"], bf16)
+            for j, (q, wx) in enumerate(lst):
+                upd[pos[q]] += wx * Y[j]
+        if L.get("ws_up") is not None:
+            upd += expert_ffn(X_all, L["ws_up"], L["ws_gate"], L["ws_down"],
+                              "swiglu", bf16)
+        new = X_all + upd
+        h[execd] = round_bf16(new) if bf16 else round_f32(new)
+
+        # exit gate after an executed layer, never after the last (A2, A3)
+        if l < N - 1:
+            xi = exit_confidence(h[execd], L["w_exit"], L["b_exit"],
+                                 model.get("conf_mode", "softmax"))
+            for i, q in enumerate(execd):
+                pj = pol["p_exit"] if token_p_exit is None else float(token_p_exit[q])
+                tr["xi"][q] = xi[i]
+                state["xi"][q] = xi[i]
+                tr["margin"][q] = min(tr["margin"][q], abs(xi[i] - pj))
+                if xi[i] >= pj:  # Eq. (8)
+                    state["exit_layer"][q] = l
+
+    for q in act_list:
+        tr["d_acc"][q] = state["d_acc"][q]
+    state["active"] = [q for q in act_list if state["exit_layer"][q] == N]
+    return tr
+
+
+def stack_forward(model, pol, h0, token_budget=None, token_p_exit=None):
+    """Algorithm 2 over all N layers; returns (final state, per-layer traces)."""
+    state = init_state(h0, model["n_layers"])
+    traces = []
+    for l in range(model["n_layers"]):
+        traces.append(layer_step(model, l, pol, state, token_budget, token_p_exit))
+    return state, traces
+
+
+# ----------------------------------------------------------------------------
+# conversion of generated inputs (torch tensors) to the oracle's fp64 model
+# ----------------------------------------------------------------------------
+def _f64(t):
+    if t is None:
+        return None
+    import torch
+    return t.detach().to("cpu").to(torch.float64).numpy()
+
+
+def model_from_inputs(inputs, layers=None):
+    """fp64 numpy copy of generated inputs (exact widening of stored values)."""
+    cfg = inputs["cfg"]
+    sel = range(cfg["n_layers"]) if layers is None else layers
+    out = dict(n_layers=cfg["n_layers"], n_experts=cfg["n_experts"],
+               top_k=cfg["top_k"], dtype=cfg["dtype"], act=cfg["act"],
+               normalize_topk=cfg["normalize_topk"],
+               conf_mode=cfg.get("conf_mode", "softmax"), layers={})
+    for l in sel:
+        L = inputs["layers"][l]
+        out["layers"][l] = dict(
+            w_router=_f64(L["w_router"]), b_router=_f64(L["b_router"]),
+            w_up=_f64(L["w_up"]), w_gate=_f64(L["w_gate"]), w_down=_f64(L["w_down"]),
+            ws_up=_f64(L["ws_up"]), ws_gate=_f64(L["ws_gate"]),
+            ws_down=_f64(L["ws_down"]), w_exit=_f64(L["w_exit"]),
+            b_exit=_f64(L["b_exit"]),
+            local_mask=[int(v) for v in L["local_mask"].cpu()],
+            sim=_f64(L["sim"]), theta=float(L["theta"]),
+            skip_slope=float(L["skip_slope"]))
+    return out
