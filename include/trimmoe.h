@@ -1,0 +1,225 @@
+/*
+ * trimmoe.h -- C ABI of the adaptive-depth MoE step (TrimMoE, arXiv
+ * 2608.00573) on one AMD Instinct MI355X (gfx950).
+ *
+ * One call of trimmoe_layer_step runs, for every still-active token, the
+ * online decision of the paper's Algorithm 2 (Table II) at look-ahead
+ * horizon H = 1 and the MoE layer it selects:
+ *
+ *   route   router logits, top-k, layer importance I (Sec. III-B, Eq. (4))
+ *   decide  substitution of remote experts by local ones (Eq. (3)), skip
+ *           admission and costs (Eq. (5), (31), (32), (34), (35), the
+ *           importance threshold of Sec. V-C), budget update (Eq. (41),
+ *           (42))
+ *   FFN     grouped expert FFN over the executed (token, expert) rows, the
+ *           weighted combine and the residual update (a skipped layer is the
+ *           identity path, Sec. III-B)
+ *   exit    exit-head confidence xi (Eq. (7)) after an executed layer and
+ *           the exit gate xi >= p_J (Eq. (8), (9)); exited tokens are
+ *           removed from the active list.
+ *
+ * Conventions
+ *  - Every pointer inside trimmoe_layer, trimmoe_state and trimmoe_trace is a
+ *    DEVICE pointer on the current HIP device; trimmoe_model,
+ *    trimmoe_policy and the layer array are HOST structs read during the
+ *    call only.  Matrices are row-major and contiguous, 16-byte aligned.
+ *  - dtype TRIMMOE_BF16: weights and h are bf16 (2-byte words); routed and
+ *    shared activations are rounded to bf16 before the down projection and
+ *    h is rounded to bf16 once per executed layer.  TRIMMOE_F32: all fp32.
+ *  - All arguments are validated before anything is enqueued; on any error
+ *    nothing is launched and no output is modified.
+ *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL
+ *    is the null stream).  TRIMMOE_OK means "enqueued"; kernel faults
+ *    surface at the caller's next synchronisation.
+ *  - The library never allocates, frees or synchronises; it keeps no
+ *    global state.  The caller owns the workspace (size from
+ *    trimmoe_workspace_size).  Calls that share a workspace or a state must
+ *    be ordered on one stream.
+ */
+#ifndef TRIMMOE_H
+#define TRIMMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TRIMMOE_ABI_VERSION 1
+
+/* status codes */
+#define TRIMMOE_OK 0
+#define TRIMMOE_ERR_NULL (-1)      /* a required pointer is NULL             */
+#define TRIMMOE_ERR_SHAPE (-2)     /* unsupported or inconsistent dimensions */
+#define TRIMMOE_ERR_DTYPE (-3)     /* unknown dtype / activation / mode      */
+#define TRIMMOE_ERR_POLICY (-4)    /* NaN or out-of-range policy scalar      */
+#define TRIMMOE_ERR_LAYER (-5)     /* layer index out of range               */
+#define TRIMMOE_ERR_WORKSPACE (-6) /* workspace NULL, misaligned or too small */
+#define TRIMMOE_ERR_HIP (-7)       /* a kernel launch was rejected by HIP    */
+
+#define TRIMMOE_F32 0
+#define TRIMMOE_BF16 1
+
+#define TRIMMOE_ACT_RELU 0   /* E(x) = W_down relu(W_up x)                    */
+#define TRIMMOE_ACT_SWIGLU 1 /* E(x) = W_down (silu(W_gate x) * (W_up x))     */
+
+#define TRIMMOE_CONF_SOFTMAX 0 /* xi = max softmax(W_exit h + b), V >= 2     */
+#define TRIMMOE_CONF_SIGMOID 1 /* xi = sigmoid(w . h + b), W_exit is [1, d]  */
+
+/* limits checked by validation */
+#define TRIMMOE_MAX_EXPERTS 256
+#define TRIMMOE_MAX_TOPK 8
+
+/* actions recorded in the trace */
+#define TRIMMOE_ACT_INACTIVE 0
+#define TRIMMOE_ACT_EXEC 1
+#define TRIMMOE_ACT_SKIP 2
+
+/* per-slot kinds recorded in the trace */
+#define TRIMMOE_KIND_NONE (-1)   /* token inactive or layer skipped          */
+#define TRIMMOE_KIND_LOCAL 0     /* target expert, resident on this GPU      */
+#define TRIMMOE_KIND_SUBST 1     /* local substitute of a remote target      */
+#define TRIMMOE_KIND_REMOTE 2    /* remote target executed exactly           */
+
+/*
+ * One MoE layer.  E = n_experts, d = d_model, F = d_ff, Fs = d_ff_shared,
+ * V = vocab_exit (1 in sigmoid mode).  Weight element type = model dtype.
+ */
+typedef struct trimmoe_layer {
+  const void* w_router;   /* [E, d]   router (Sec. III-B)                       */
+  const float* b_router;  /* [E] fp32 or NULL                                   */
+  const void* w_up;       /* [E, F, d]                                          */
+  const void* w_gate;     /* [E, F, d] (SwiGLU) or NULL (ReLU)                  */
+  const void* w_down;     /* [E, d, F]                                          */
+  const void* ws_up;      /* [Fs, d] shared expert (SwiGLU) or NULL if Fs == 0  */
+  const void* ws_gate;    /* [Fs, d]                                            */
+  const void* ws_down;    /* [d, Fs]                                            */
+  const void* w_exit;     /* [V, d]   exit head h_l (Eq. (7))                   */
+  const float* b_exit;    /* [V] fp32 or NULL                                   */
+  const uint8_t* local_mask; /* [E]  1 = expert resident on this GPU (Eq. (1)) */
+  const float* sim;       /* [E, E] fp32 expert similarity Sim_l (Eq. (3))      */
+  float theta;            /* importance threshold theta_l (Eq. (24), Sec. V-C)  */
+  float skip_slope;       /* s_l of the skip degradation rho(I)=min(1,s_l I)    */
+} trimmoe_layer;
+
+typedef struct trimmoe_model {
+  int32_t n_layers;       /* N                                                  */
+  int32_t d_model;        /* d; bf16: multiple of 64, f32: multiple of 4        */
+  int32_t n_experts;      /* E, 1..256                                          */
+  int32_t top_k;          /* k, 1..min(8, E)                                    */
+  int32_t d_ff;           /* F; bf16: multiple of 64                            */
+  int32_t d_ff_shared;    /* Fs, 0 = no shared expert; bf16: multiple of 64     */
+  int32_t vocab_exit;     /* V                                                  */
+  int32_t dtype;          /* TRIMMOE_F32 | TRIMMOE_BF16                         */
+  int32_t act;            /* TRIMMOE_ACT_RELU | TRIMMOE_ACT_SWIGLU              */
+  int32_t conf_mode;      /* TRIMMOE_CONF_SOFTMAX | TRIMMOE_CONF_SIGMOID        */
+  int32_t normalize_topk; /* 1: slot weight p_e / I, 0: p_e                     */
+  const trimmoe_layer* layers; /* host array of N layers                        */
+} trimmoe_model;
+
+/*
+ * Online policy (Sec. V).  Costs: execute = omega_t * sum of per-slot
+ * delays (t_local or t_remote) + (1 - omega_t) * sum Q / budget (Eq. (31));
+ * skip = (1 - omega_t) * Lambda / budget (Eq. (32)).  Q(e, j) =
+ * min(1, phi_scale * (1 - Sim[e][j]) / 2) (Eq. (3)); a local expert j is a
+ * feasible substitute of e when Sim[e][j] >= sim_min.
+ */
+typedef struct trimmoe_policy {
+  float p_exit;      /* confidence requirement p_J (Eq. (8))               */
+  float budget;      /* per-token degradation budget D_i (Eq. (33)), >= 0   */
+  float omega_t;     /* delay weight in [0, 1]; omega_D = 1 - omega_t       */
+  float t_local;     /* normalised delay of a local slot, >= 0              */
+  float t_remote;    /* normalised delay of a remote slot, >= 0             */
+  float phi_scale;   /* phi(x) = min(1, phi_scale * x), >= 0                */
+  float sim_min;     /* similarity floor of feasible substitutes            */
+  const float* p_exit_tok; /* [T] device, per-token p_J, or NULL            */
+  const float* budget_tok; /* [T] device, per-token budget, or NULL         */
+} trimmoe_policy;
+
+/*
+ * Per-token state, all device memory owned by the caller.  T = n_tokens.
+ *   h          [T, d]  hidden states; updated in place; an exited token
+ *                      keeps its state at exit time (Eq. (8)).
+ *   d_acc      [T] f32 accumulated degradation D-hat (Eq. (41), (42)).
+ *   active_idx [T] i32 tokens still active, ascending; first *n_active used.
+ *   n_active   [1] i32 number of active tokens (device).
+ *   exit_layer [T] i32 0-based layer after which the token exited, or N.
+ *   xi         [T] f32 last evaluated confidence, NaN if none yet.
+ */
+typedef struct trimmoe_state {
+  int32_t n_tokens;
+  void* h;
+  float* d_acc;
+  int32_t* active_idx;
+  int32_t* n_active;
+  int32_t* exit_layer;
+  float* xi;
+} trimmoe_state;
+
+/*
+ * Optional per-layer decision record (device memory, NULL = not written).
+ * Row l of each array covers layer l; entries of tokens inactive at layer l
+ * are written as: action 0, target/exec -1, kind -1, gate/importance/xi/
+ * d_acc NaN.  exec[t][s] is the expert slot s runs (target, substitute, or
+ * -1 if skipped); kind per the TRIMMOE_KIND_* codes; gate is the slot
+ * weight; xi is NaN where no confidence was evaluated; d_acc is D-hat
+ * after the layer.  counters[l][0..7] = active, executed, skipped, exited,
+ * substituted slots, remote slots, merged rows, distinct experts.
+ */
+typedef struct trimmoe_trace {
+  int8_t* action;      /* [N, T]    */
+  int16_t* target;     /* [N, T, k] */
+  int16_t* exec;       /* [N, T, k] */
+  int8_t* kind;        /* [N, T, k] */
+  float* gate;         /* [N, T, k] */
+  float* importance;   /* [N, T]    */
+  float* xi;           /* [N, T]    */
+  float* d_acc;        /* [N, T]    */
+  int32_t* counters;   /* [N, 8]    */
+} trimmoe_trace;
+
+/* TRIMMOE_ABI_VERSION of the built library. */
+int trimmoe_abi_version(void);
+
+/* Static text for a status code (never NULL). */
+const char* trimmoe_status_str(int status);
+
+/*
+ * Bytes of workspace that trimmoe_layer_step / trimmoe_stack_forward need
+ * for up to max_tokens tokens (written to *bytes_out).  The workspace must
+ * be 256-byte aligned.  Host-only; validates the model like the steps do.
+ */
+int trimmoe_workspace_size(const trimmoe_model* m, int32_t max_tokens,
+                           size_t* bytes_out);
+
+/*
+ * Algorithm 2 initialisation (Table II, first loop): d_acc = 0, every token
+ * active in index order, n_active = T, exit_layer = N, xi = NaN.  h is not
+ * touched.
+ */
+int trimmoe_state_reset(const trimmoe_model* m, trimmoe_state* s, void* stream);
+
+/*
+ * One MoE layer `layer` (0-based) for the active tokens of `s` (Algorithm 2
+ * at H = 1, Eq. (3)-(9), (31)-(35), (40)-(42)).  Reads the active list and
+ * n_active on the device (no host round trip); updates h, d_acc,
+ * active_idx, n_active, exit_layer and xi.  The confidence of layer N-1 is
+ * not evaluated.  trace may be NULL.
+ */
+int trimmoe_layer_step(const trimmoe_model* m, int32_t layer,
+                       const trimmoe_policy* p, trimmoe_state* s,
+                       trimmoe_trace* trace, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/* trimmoe_state_reset followed by trimmoe_layer_step for l = 0 .. N-1. */
+int trimmoe_stack_forward(const trimmoe_model* m, const trimmoe_policy* p,
+                          trimmoe_state* s, trimmoe_trace* trace,
+                          void* workspace, size_t workspace_bytes,
+                          void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TRIMMOE_H */

@@ -65,7 +65,10 @@ once per executed layer after the weighted sum.  In fp32 storage mode only
 h is rounded, to fp32.
 
 Every deciding margin is recorded so a caller can tell which decisions are
-too close to call at fp32 accuracy (the "band").
+too close to call at fp32 accuracy (the "band"): ``margin_pre`` covers the
+decisions taken before the expert FFN (routing, substitution, skip),
+``margin_exit`` the exit gate (which reads the layer's rounded output), and
+``margin`` is the smaller of the two.
 """
 from __future__ import annotations
 
@@ -338,7 +341,8 @@ def layer_step(model, l: int, pol, state, token_budget=None, token_p_exit=None):
               gate=np.full((T, k), math.nan),
               importance=np.full(T, math.nan),
               xi=np.full(T, math.nan), d_acc=np.full(T, math.nan),
-              margin=np.full(T, _INF), rows={})
+              margin=np.full(T, _INF), margin_pre=np.full(T, _INF),
+              margin_exit=np.full(T, _INF), rows={})
 
     act_list = list(state["active"])
     h = state["h"]
@@ -356,6 +360,7 @@ def layer_step(model, l: int, pol, state, token_budget=None, token_p_exit=None):
         m = min([m_route] + dec["margins"]
                 + [sub_m[e] for e in S if not local[e]])
         tr["margin"][q] = m
+        tr["margin_pre"][q] = m
         tr["action"][q] = dec["action"]
         tr["target"][q] = S
         tr["gate"][q] = w
@@ -397,6 +402,7 @@ def layer_step(model, l: int, pol, state, token_budget=None, token_p_exit=None):
                 pj = pol["p_exit"] if token_p_exit is None else float(token_p_exit[q])
                 tr["xi"][q] = xi[i]
                 state["xi"][q] = xi[i]
+                tr["margin_exit"][q] = abs(xi[i] - pj)
                 tr["margin"][q] = min(tr["margin"][q], abs(xi[i] - pj))
                 if xi[i] >= pj:  # Eq. (8)
                     state["exit_layer"][q] = l

@@ -1,0 +1,248 @@
+"""ctypes binding of libtrimmoe (include/trimmoe.h): marshalling only.
+
+Every step of the adaptive-depth MoE layer runs inside the HIP library;
+this module only mirrors the C structs, passes device pointers taken from
+torch tensors (torch provides device memory and streams) and turns status
+codes into exceptions.  There is no fallback: if the library is missing
+the import of ``lib()`` raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libtrimmoe.so")
+
+TRIMMOE_OK = 0
+STATUS = {0: "OK", -1: "ERR_NULL", -2: "ERR_SHAPE", -3: "ERR_DTYPE", -4: "ERR_POLICY",
+          -5: "ERR_LAYER", -6: "ERR_WORKSPACE", -7: "ERR_HIP"}
+F32, BF16 = 0, 1
+ACT_RELU, ACT_SWIGLU = 0, 1
+CONF_SOFTMAX, CONF_SIGMOID = 0, 1
+MAX_EXPERTS, MAX_TOPK = 256, 8
+
+
+class Layer(C.Structure):
+    _fields_ = [("w_router", C.c_void_p), ("b_router", C.c_void_p),
+                ("w_up", C.c_void_p), ("w_gate", C.c_void_p), ("w_down", C.c_void_p),
+                ("ws_up", C.c_void_p), ("ws_gate", C.c_void_p), ("ws_down", C.c_void_p),
+                ("w_exit", C.c_void_p), ("b_exit", C.c_void_p),
+                ("local_mask", C.c_void_p), ("sim", C.c_void_p),
+                ("theta", C.c_float), ("skip_slope", C.c_float)]
+
+
+class Model(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("d_model", C.c_int32), ("n_experts", C.c_int32),
+                ("top_k", C.c_int32), ("d_ff", C.c_int32), ("d_ff_shared", C.c_int32),
+                ("vocab_exit", C.c_int32), ("dtype", C.c_int32), ("act", C.c_int32),
+                ("conf_mode", C.c_int32), ("normalize_topk", C.c_int32),
+                ("layers", C.POINTER(Layer))]
+
+
+class Policy(C.Structure):
+    _fields_ = [("p_exit", C.c_float), ("budget", C.c_float), ("omega_t", C.c_float),
+                ("t_local", C.c_float), ("t_remote", C.c_float), ("phi_scale", C.c_float),
+                ("sim_min", C.c_float), ("p_exit_tok", C.c_void_p),
+                ("budget_tok", C.c_void_p)]
+
+
+class State(C.Structure):
+    _fields_ = [("n_tokens", C.c_int32), ("h", C.c_void_p), ("d_acc", C.c_void_p),
+                ("active_idx", C.c_void_p), ("n_active", C.c_void_p),
+                ("exit_layer", C.c_void_p), ("xi", C.c_void_p)]
+
+
+class Trace(C.Structure):
+    _fields_ = [("action", C.c_void_p), ("target", C.c_void_p), ("exec", C.c_void_p),
+                ("kind", C.c_void_p), ("gate", C.c_void_p), ("importance", C.c_void_p),
+                ("xi", C.c_void_p), ("d_acc", C.c_void_p), ("counters", C.c_void_p)]
+
+
+EXPORTS = ["trimmoe_abi_version", "trimmoe_status_str", "trimmoe_workspace_size",
+           "trimmoe_state_reset", "trimmoe_layer_step", "trimmoe_stack_forward"]
+
+_lib = None
+
+
+def lib():
+    """The loaded libtrimmoe.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "paper_2608_00573_amd.build.build() (there is no fallback)")
+        L = C.CDLL(LIB_PATH)
+        L.trimmoe_abi_version.restype = C.c_int
+        L.trimmoe_status_str.restype = C.c_char_p
+        L.trimmoe_status_str.argtypes = [C.c_int]
+        L.trimmoe_workspace_size.restype = C.c_int
+        L.trimmoe_workspace_size.argtypes = [C.POINTER(Model), C.c_int32, C.POINTER(C.c_size_t)]
+        L.trimmoe_state_reset.restype = C.c_int
+        L.trimmoe_state_reset.argtypes = [C.POINTER(Model), C.POINTER(State), C.c_void_p]
+        L.trimmoe_layer_step.restype = C.c_int
+        L.trimmoe_layer_step.argtypes = [C.POINTER(Model), C.c_int32, C.POINTER(Policy),
+                                         C.POINTER(State), C.POINTER(Trace), C.c_void_p,
+                                         C.c_size_t, C.c_void_p]
+        L.trimmoe_stack_forward.restype = C.c_int
+        L.trimmoe_stack_forward.argtypes = [C.POINTER(Model), C.POINTER(Policy),
+                                            C.POINTER(State), C.POINTER(Trace), C.c_void_p,
+                                            C.c_size_t, C.c_void_p]
+        _lib = L
+    return _lib
+
+
+class TrimmoeError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} returned {status} ({STATUS.get(status, '?')})")
+        self.status = status
+
+
+def _check(fn: str, rc: int):
+    if rc != TRIMMOE_OK:
+        raise TrimmoeError(fn, rc)
+
+
+def _ptr(t):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream_handle(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return C.c_void_p(stream.cuda_stream)
+
+
+# ------------------------------------------------------------- wrappers ----
+def trimmoe_abi_version() -> int:
+    return lib().trimmoe_abi_version()
+
+
+def trimmoe_status_str(status: int) -> str:
+    return lib().trimmoe_status_str(status).decode()
+
+
+def trimmoe_workspace_size(model: Model, max_tokens: int) -> int:
+    out = C.c_size_t(0)
+    _check("trimmoe_workspace_size",
+           lib().trimmoe_workspace_size(C.byref(model), max_tokens, C.byref(out)))
+    return out.value
+
+
+def trimmoe_state_reset(model: Model, state: State, stream=None):
+    _check("trimmoe_state_reset",
+           lib().trimmoe_state_reset(C.byref(model), C.byref(state), _stream_handle(stream)))
+
+
+def trimmoe_layer_step(model: Model, layer: int, policy: Policy, state: State, trace,
+                       workspace: torch.Tensor, stream=None):
+    tr = C.byref(trace) if trace is not None else None
+    _check("trimmoe_layer_step",
+           lib().trimmoe_layer_step(C.byref(model), layer, C.byref(policy), C.byref(state), tr,
+                                    _ptr(workspace), workspace.numel(), _stream_handle(stream)))
+
+
+def trimmoe_stack_forward(model: Model, policy: Policy, state: State, trace,
+                          workspace: torch.Tensor, stream=None):
+    tr = C.byref(trace) if trace is not None else None
+    _check("trimmoe_stack_forward",
+           lib().trimmoe_stack_forward(C.byref(model), C.byref(policy), C.byref(state), tr,
+                                       _ptr(workspace), workspace.numel(),
+                                       _stream_handle(stream)))
+
+
+# ------------------------------------------------ struct construction ------
+class ModelHandle:
+    """A Model struct over device tensors; keeps the tensors alive.
+
+    ``layers`` is a list of dicts with the keys of trimmoe_layer (torch
+    tensors on one GPU, or None) plus the floats ``theta`` and
+    ``skip_slope``.
+    """
+
+    def __init__(self, *, n_layers, d_model, n_experts, top_k, d_ff, d_ff_shared, vocab_exit,
+                 dtype, act, conf_mode, normalize_topk, layers):
+        self._keep = []
+        arr = (Layer * n_layers)()
+        for i, L in enumerate(layers):
+            for key in ("w_router", "b_router", "w_up", "w_gate", "w_down", "ws_up", "ws_gate",
+                        "ws_down", "w_exit", "b_exit", "local_mask", "sim"):
+                t = L.get(key)
+                if t is not None:
+                    if not t.is_contiguous():
+                        t = t.contiguous()
+                    self._keep.append(t)
+                setattr(arr[i], key, None if t is None else t.data_ptr())
+            arr[i].theta = float(L["theta"])
+            arr[i].skip_slope = float(L["skip_slope"])
+        self.layers = arr
+        self.model = Model(n_layers, d_model, n_experts, top_k, d_ff, d_ff_shared, vocab_exit,
+                           dtype, act, conf_mode, normalize_topk,
+                           C.cast(arr, C.POINTER(Layer)))
+
+
+def make_policy(*, p_exit, budget, omega_t, t_local, t_remote, phi_scale, sim_min,
+                p_exit_tok=None, budget_tok=None) -> Policy:
+    return Policy(p_exit, budget, omega_t, t_local, t_remote, phi_scale, sim_min,
+                  None if p_exit_tok is None else p_exit_tok.data_ptr(),
+                  None if budget_tok is None else budget_tok.data_ptr())
+
+
+class StateBuffers:
+    """Caller-owned per-token state on one GPU (h is used in place)."""
+
+    def __init__(self, h: torch.Tensor):
+        T = h.shape[0]
+        dev = h.device
+        self.h = h
+        self.d_acc = torch.zeros(T, dtype=torch.float32, device=dev)
+        self.active_idx = torch.zeros(max(T, 1), dtype=torch.int32, device=dev)
+        self.n_active = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.exit_layer = torch.zeros(max(T, 1), dtype=torch.int32, device=dev)
+        self.xi = torch.zeros(max(T, 1), dtype=torch.float32, device=dev)
+        self.state = State(T, h.data_ptr(), self.d_acc.data_ptr(), self.active_idx.data_ptr(),
+                           self.n_active.data_ptr(), self.exit_layer.data_ptr(),
+                           self.xi.data_ptr())
+
+
+class TraceBuffers:
+    """Per-layer decision record on one GPU."""
+
+    def __init__(self, n_layers: int, T: int, k: int, device):
+        z = dict(device=device)
+        self.action = torch.zeros(n_layers, T, dtype=torch.int8, **z)
+        self.target = torch.zeros(n_layers, T, k, dtype=torch.int16, **z)
+        self.exec = torch.zeros(n_layers, T, k, dtype=torch.int16, **z)
+        self.kind = torch.zeros(n_layers, T, k, dtype=torch.int8, **z)
+        self.gate = torch.zeros(n_layers, T, k, dtype=torch.float32, **z)
+        self.importance = torch.zeros(n_layers, T, dtype=torch.float32, **z)
+        self.xi = torch.zeros(n_layers, T, dtype=torch.float32, **z)
+        self.d_acc = torch.zeros(n_layers, T, dtype=torch.float32, **z)
+        self.counters = torch.zeros(n_layers, 8, dtype=torch.int32, **z)
+        self.trace = Trace(*(getattr(self, n).data_ptr() for n in
+                             ("action", "target", "exec", "kind", "gate", "importance", "xi",
+                              "d_acc", "counters")))
+
+
+def alloc_workspace(model: Model, max_tokens: int, device) -> torch.Tensor:
+    """A 256-byte aligned uint8 workspace of the size the library asks for."""
+    n = trimmoe_workspace_size(model, max_tokens)
+    ws = torch.empty(n + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + n]
+
+
+def model_handle(dims: dict, layers: list) -> ModelHandle:
+    """ModelHandle from a dims dict (n_layers, d_model, n_experts, top_k, d_ff,
+    d_ff_shared, vocab_exit, dtype 'bf16'|'f32', act 'relu'|'swiglu',
+    normalize_topk, optional conf_mode 'softmax'|'sigmoid') and per-layer
+    tensor dicts keyed like trimmoe_layer."""
+    return ModelHandle(
+        n_layers=dims["n_layers"], d_model=dims["d_model"], n_experts=dims["n_experts"],
+        top_k=dims["top_k"], d_ff=dims["d_ff"], d_ff_shared=dims["d_ff_shared"],
+        vocab_exit=dims["vocab_exit"], dtype={"f32": F32, "bf16": BF16}[dims["dtype"]],
+        act={"relu": ACT_RELU, "swiglu": ACT_SWIGLU}[dims["act"]],
+        conf_mode={"softmax": CONF_SOFTMAX, "sigmoid": CONF_SIGMOID}[dims.get("conf_mode", "softmax")],
+        normalize_topk=int(dims["normalize_topk"]), layers=layers)

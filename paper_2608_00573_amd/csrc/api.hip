@@ -1,0 +1,286 @@
+// C ABI of libtrimmoe: argument validation, workspace carving and the
+// per-layer launch sequence of the adaptive-depth MoE step.  The declared
+// interface and its conventions are in include/trimmoe.h.
+//
+// Launch sequence of one layer, all on the caller's stream and sized for
+// the worst case (every kernel reads the live counts from device memory
+// and retires early, so the host never waits on the device):
+//   [trace fill] -> substitution table -> route+decide -> offsets/tiles ->
+//   permute -> up/gate GEMM -> down GEMM (-> shared expert) -> combine ->
+//   (not the last layer) exit GEMM -> exit gate -> compaction.
+#include <math.h>
+#include <string.h>
+
+#include "common.h"
+
+using namespace trimmoe;
+
+namespace {
+
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+int validate_model(const trimmoe_model* m) {
+  if (!m || !m->layers) return TRIMMOE_ERR_NULL;
+  if (m->dtype != TRIMMOE_F32 && m->dtype != TRIMMOE_BF16) return TRIMMOE_ERR_DTYPE;
+  if (m->act != TRIMMOE_ACT_RELU && m->act != TRIMMOE_ACT_SWIGLU) return TRIMMOE_ERR_DTYPE;
+  if (m->conf_mode != TRIMMOE_CONF_SOFTMAX && m->conf_mode != TRIMMOE_CONF_SIGMOID)
+    return TRIMMOE_ERR_DTYPE;
+  if (m->normalize_topk != 0 && m->normalize_topk != 1) return TRIMMOE_ERR_SHAPE;
+  if (m->n_layers < 1 || m->d_model < 1 || m->n_experts < 1 ||
+      m->n_experts > TRIMMOE_MAX_EXPERTS || m->top_k < 1 || m->top_k > TRIMMOE_MAX_TOPK ||
+      m->top_k > m->n_experts || m->d_ff < 1 || m->d_ff_shared < 0 || m->vocab_exit < 1)
+    return TRIMMOE_ERR_SHAPE;
+  if (m->conf_mode == TRIMMOE_CONF_SIGMOID && m->vocab_exit != 1) return TRIMMOE_ERR_SHAPE;
+  if (m->dtype == TRIMMOE_BF16) {
+    if (m->d_model % 64 || m->d_ff % 64 || m->d_ff_shared % 64) return TRIMMOE_ERR_SHAPE;
+  } else {
+    if (m->d_model % 4) return TRIMMOE_ERR_SHAPE;
+  }
+  const bool swiglu = m->act == TRIMMOE_ACT_SWIGLU;
+  for (int l = 0; l < m->n_layers; ++l) {
+    const trimmoe_layer& L = m->layers[l];
+    if (!L.w_router || !L.w_up || !L.w_down || !L.w_exit || !L.local_mask || !L.sim)
+      return TRIMMOE_ERR_NULL;
+    if (swiglu && !L.w_gate) return TRIMMOE_ERR_NULL;
+    if (m->d_ff_shared > 0 && (!L.ws_up || !L.ws_gate || !L.ws_down)) return TRIMMOE_ERR_NULL;
+    const void* mats[] = {L.w_router, L.w_up, L.w_down, L.w_exit,
+                          swiglu ? L.w_gate : L.w_up,
+                          m->d_ff_shared ? L.ws_up : L.w_up,
+                          m->d_ff_shared ? L.ws_gate : L.w_up,
+                          m->d_ff_shared ? L.ws_down : L.w_up};
+    for (const void* q : mats)
+      if (!aligned16(q)) return TRIMMOE_ERR_SHAPE;
+    if (isnan(L.theta) || !(L.skip_slope >= 0.f) || isinf(L.skip_slope)) return TRIMMOE_ERR_POLICY;
+  }
+  return TRIMMOE_OK;
+}
+
+int validate_policy(const trimmoe_policy* p) {
+  if (!p) return TRIMMOE_ERR_NULL;
+  if (isnan(p->p_exit) || isnan(p->sim_min)) return TRIMMOE_ERR_POLICY;
+  if (!(p->budget >= 0.f) || isinf(p->budget)) return TRIMMOE_ERR_POLICY;
+  if (!(p->omega_t >= 0.f && p->omega_t <= 1.f)) return TRIMMOE_ERR_POLICY;
+  if (!(p->t_local >= 0.f) || !(p->t_remote >= 0.f) || isinf(p->t_local) || isinf(p->t_remote))
+    return TRIMMOE_ERR_POLICY;
+  if (!(p->phi_scale >= 0.f) || isinf(p->phi_scale)) return TRIMMOE_ERR_POLICY;
+  return TRIMMOE_OK;
+}
+
+int validate_state(const trimmoe_model* m, const trimmoe_state* s) {
+  if (!s) return TRIMMOE_ERR_NULL;
+  if (s->n_tokens < 0) return TRIMMOE_ERR_SHAPE;
+  if (!s->h || !s->d_acc || !s->active_idx || !s->n_active || !s->exit_layer || !s->xi)
+    return TRIMMOE_ERR_NULL;
+  if (!aligned16(s->h)) return TRIMMOE_ERR_SHAPE;
+  (void)m;
+  return TRIMMOE_OK;
+}
+
+// Carve the workspace (base == NULL: only measure).  Returns total bytes.
+size_t carve(const trimmoe_model* m, int T, char* base, LayerParams* p) {
+  const bool bf16 = m->dtype == TRIMMOE_BF16;
+  const int E = m->n_experts, k = m->top_k, d = m->d_model, F = m->d_ff, Fs = m->d_ff_shared;
+  const size_t es = bf16 ? 2 : 4;
+  const int Tm = T > 0 ? T : 1;
+  const size_t R = (size_t)Tm * k;
+  const int nblk = cdiv(Tm, kRouteTokens);
+  const int max_tiles = (int)cdiv((int)R, kGemmBM) + E;
+  const int n_vtiles = bf16 ? cdiv(m->vocab_exit, kExitTileBF16) : cdiv(m->vocab_exit, kExitTileF32);
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> void* {
+    void* q = base ? base + off : nullptr;
+    off = align256(off + bytes);
+    return q;
+  };
+  LayerParams tmp;
+  LayerParams& P = p ? *p : tmp;
+  P.sub_c = (int32_t*)take(E * 4);
+  P.sub_q = (float*)take(E * 4);
+  P.tok_exec = (int32_t*)take(R * 4);
+  P.tok_w = (float*)take(R * 4);
+  P.tok_row = (int32_t*)take(R * 4);
+  P.tok_action = (int32_t*)take((size_t)Tm * 4);
+  P.tok_keep = (int32_t*)take((size_t)Tm * 4);
+  P.exec_list = (int32_t*)take((size_t)Tm * 4);
+  P.exec_pos = (int32_t*)take((size_t)Tm * 4);
+  P.blk_cnt = (int32_t*)take((size_t)nblk * E * 4);
+  P.blk_off = (int32_t*)take((size_t)nblk * E * 4);
+  P.blk_xcnt = (int32_t*)take((size_t)nblk * 4);
+  P.blk_xoff = (int32_t*)take((size_t)nblk * 4);
+  P.exp_off = (int32_t*)take((size_t)(E + 1) * 4);
+  P.counts = (int32_t*)take(kCntSlots * 4);
+  P.tiles = (int4*)take((size_t)max_tiles * 16);
+  P.x_perm = take(R * d * es);
+  P.act_buf = take(R * F * es);
+  P.y_buf = (float*)take(R * d * 4);
+  P.xs = Fs ? take((size_t)Tm * d * es) : nullptr;
+  P.act_s = Fs ? take((size_t)Tm * Fs * es) : nullptr;
+  P.y_s = Fs ? (float*)take((size_t)Tm * d * 4) : nullptr;
+  P.hx = take((size_t)Tm * d * es);
+  P.partials = (float2*)take((size_t)Tm * n_vtiles * 8);
+  P.n_vtiles = n_vtiles;
+  P.max_tiles = max_tiles;
+  return off;
+}
+
+void fill_params(LayerParams& P, const trimmoe_model* m, int l, const trimmoe_policy* pol,
+                 const trimmoe_state* s, const trimmoe_trace* tr) {
+  const trimmoe_layer& L = m->layers[l];
+  const int T = s->n_tokens, k = m->top_k;
+  P.N = m->n_layers;
+  P.d = m->d_model;
+  P.E = m->n_experts;
+  P.k = k;
+  P.F = m->d_ff;
+  P.Fs = m->d_ff_shared;
+  P.V = m->vocab_exit;
+  P.act = m->act;
+  P.conf_mode = m->conf_mode;
+  P.normalize = m->normalize_topk;
+  P.layer = l;
+  P.w_router = L.w_router;
+  P.b_router = L.b_router;
+  P.w_up = L.w_up;
+  P.w_gate = m->act == TRIMMOE_ACT_SWIGLU ? L.w_gate : nullptr;
+  P.w_down = L.w_down;
+  P.ws_up = L.ws_up;
+  P.ws_gate = L.ws_gate;
+  P.ws_down = L.ws_down;
+  P.w_exit = L.w_exit;
+  P.b_exit = L.b_exit;
+  P.local_mask = L.local_mask;
+  P.sim = L.sim;
+  P.theta = L.theta;
+  P.skip_slope = L.skip_slope;
+  P.p_exit = pol->p_exit;
+  P.budget = pol->budget;
+  P.omega_t = pol->omega_t;
+  P.t_local = pol->t_local;
+  P.t_remote = pol->t_remote;
+  P.phi_scale = pol->phi_scale;
+  P.sim_min = pol->sim_min;
+  P.p_exit_tok = pol->p_exit_tok;
+  P.budget_tok = pol->budget_tok;
+  P.T = T;
+  P.h = s->h;
+  P.d_acc = s->d_acc;
+  P.active_idx = s->active_idx;
+  P.n_active = s->n_active;
+  P.exit_layer = s->exit_layer;
+  P.xi = s->xi;
+  const size_t rowT = (size_t)l * T, rowTk = (size_t)l * T * k;
+  P.tr_action = tr && tr->action ? tr->action + rowT : nullptr;
+  P.tr_target = tr && tr->target ? tr->target + rowTk : nullptr;
+  P.tr_exec = tr && tr->exec ? tr->exec + rowTk : nullptr;
+  P.tr_kind = tr && tr->kind ? tr->kind + rowTk : nullptr;
+  P.tr_gate = tr && tr->gate ? tr->gate + rowTk : nullptr;
+  P.tr_importance = tr && tr->importance ? tr->importance + rowT : nullptr;
+  P.tr_xi = tr && tr->xi ? tr->xi + rowT : nullptr;
+  P.tr_d_acc = tr && tr->d_acc ? tr->d_acc + rowT : nullptr;
+  P.tr_counters = tr && tr->counters ? tr->counters + (size_t)l * 8 : nullptr;
+}
+
+bool any_trace(const trimmoe_trace* tr) {
+  return tr && (tr->action || tr->target || tr->exec || tr->kind || tr->gate || tr->importance ||
+                tr->xi || tr->d_acc || tr->counters);
+}
+
+int check_workspace(const trimmoe_model* m, const trimmoe_state* s, void* ws, size_t bytes) {
+  if (!ws) return TRIMMOE_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) & 255) return TRIMMOE_ERR_WORKSPACE;
+  if (bytes < carve(m, s->n_tokens, nullptr, nullptr)) return TRIMMOE_ERR_WORKSPACE;
+  return TRIMMOE_OK;
+}
+
+int run_layer(const trimmoe_model* m, int l, const trimmoe_policy* pol, const trimmoe_state* s,
+              const trimmoe_trace* tr, void* ws, hipStream_t st) {
+  if (s->n_tokens == 0) return TRIMMOE_OK;
+  LayerParams P;
+  memset(&P, 0, sizeof(P));
+  carve(m, s->n_tokens, static_cast<char*>(ws), &P);
+  fill_params(P, m, l, pol, s, tr);
+  const bool bf16 = m->dtype == TRIMMOE_BF16;
+  if (any_trace(tr) && launch_trace_fill(P, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  if (launch_subst(P, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  if (launch_route(P, bf16, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  if (launch_scan(P, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  if (launch_permute(P, bf16, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  if (launch_expert_ffn(P, bf16, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  if (launch_combine(P, bf16, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  if (l < m->n_layers - 1) {
+    if (launch_exit_head(P, bf16, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+    if (launch_exit_reduce(P, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+    if (launch_compact(P, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  }
+  return TRIMMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int trimmoe_abi_version(void) { return TRIMMOE_ABI_VERSION; }
+
+const char* trimmoe_status_str(int status) {
+  switch (status) {
+    case TRIMMOE_OK: return "ok";
+    case TRIMMOE_ERR_NULL: return "required pointer is NULL";
+    case TRIMMOE_ERR_SHAPE: return "unsupported or inconsistent shape or alignment";
+    case TRIMMOE_ERR_DTYPE: return "unknown dtype, activation or confidence mode";
+    case TRIMMOE_ERR_POLICY: return "policy scalar out of range or NaN";
+    case TRIMMOE_ERR_LAYER: return "layer index out of range";
+    case TRIMMOE_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case TRIMMOE_ERR_HIP: return "HIP kernel launch failed";
+    default: return "unknown status";
+  }
+}
+
+int trimmoe_workspace_size(const trimmoe_model* m, int32_t max_tokens, size_t* bytes_out) {
+  if (!bytes_out) return TRIMMOE_ERR_NULL;
+  int rc = validate_model(m);
+  if (rc) return rc;
+  if (max_tokens < 0) return TRIMMOE_ERR_SHAPE;
+  *bytes_out = carve(m, max_tokens, nullptr, nullptr);
+  return TRIMMOE_OK;
+}
+
+int trimmoe_state_reset(const trimmoe_model* m, trimmoe_state* s, void* stream) {
+  int rc = validate_model(m);
+  if (rc) return rc;
+  if ((rc = validate_state(m, s))) return rc;
+  if (s->n_tokens == 0) return TRIMMOE_OK;
+  if (launch_state_reset(m, s, static_cast<hipStream_t>(stream)) != hipSuccess) return TRIMMOE_ERR_HIP;
+  return TRIMMOE_OK;
+}
+
+int trimmoe_layer_step(const trimmoe_model* m, int32_t layer, const trimmoe_policy* p,
+                       trimmoe_state* s, trimmoe_trace* trace, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  int rc = validate_model(m);
+  if (rc) return rc;
+  if ((rc = validate_policy(p))) return rc;
+  if ((rc = validate_state(m, s))) return rc;
+  if (layer < 0 || layer >= m->n_layers) return TRIMMOE_ERR_LAYER;
+  if ((rc = check_workspace(m, s, workspace, workspace_bytes))) return rc;
+  return run_layer(m, layer, p, s, trace, workspace, static_cast<hipStream_t>(stream));
+}
+
+int trimmoe_stack_forward(const trimmoe_model* m, const trimmoe_policy* p, trimmoe_state* s,
+                          trimmoe_trace* trace, void* workspace, size_t workspace_bytes,
+                          void* stream) {
+  int rc = validate_model(m);
+  if (rc) return rc;
+  if ((rc = validate_policy(p))) return rc;
+  if ((rc = validate_state(m, s))) return rc;
+  if ((rc = check_workspace(m, s, workspace, workspace_bytes))) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (s->n_tokens == 0) return TRIMMOE_OK;
+  if (launch_state_reset(m, s, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  for (int l = 0; l < m->n_layers; ++l)
+    if ((rc = run_layer(m, l, p, s, trace, workspace, st))) return rc;
+  return TRIMMOE_OK;
+}
+
+}  // extern "C"

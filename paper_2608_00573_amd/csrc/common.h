@@ -1,0 +1,142 @@
+// Internal definitions shared by the HIP kernels and the host launcher of
+// libtrimmoe (adaptive-depth MoE step, gfx950).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "trimmoe.h"
+
+namespace trimmoe {
+
+typedef uint16_t bf16_t;
+
+// ---------------------------------------------------------------- tiling --
+// tokens handled by one block of the route and permute kernels
+constexpr int kRouteTokens = 32;
+// rows of an expert group covered by one grouped-GEMM tile
+constexpr int kGemmBM = 128;
+constexpr int kGemmBN = 128;
+constexpr int kGemmBK = 64;
+// vocabulary rows of one exit-head tile (bf16 MFMA path / fp32 path)
+constexpr int kExitTileBF16 = 128;
+constexpr int kExitTileF32 = 16;
+// fp32 GEMM tile
+constexpr int kF32Tile = 16;
+
+// slots of the small device counter block in the workspace
+enum CountSlot {
+  kCntRows = 0,   // merged (token, expert) rows of this layer
+  kCntTiles = 1,  // grouped-GEMM row tiles
+  kCntExec = 2,   // executed tokens
+  kCntSlots = 8
+};
+
+// --------------------------------------------------------------- numbers --
+__device__ __forceinline__ float bf2f(bf16_t v) {
+  return __uint_as_float(static_cast<uint32_t>(v) << 16);
+}
+
+// fp32 -> bf16, round to nearest, ties to even (NaN stays NaN)
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<bf16_t>(bf16_t v) { return bf2f(v); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f2bf(v); }
+
+// --------------------------------------------------- per-layer arguments --
+// Everything one layer's kernels need, passed by value.
+struct LayerParams {
+  // model
+  int N, d, E, k, F, Fs, V, act, conf_mode, normalize, layer;
+  // layer tensors
+  const void* w_router;
+  const float* b_router;
+  const void* w_up;
+  const void* w_gate;
+  const void* w_down;
+  const void* ws_up;
+  const void* ws_gate;
+  const void* ws_down;
+  const void* w_exit;
+  const float* b_exit;
+  const uint8_t* local_mask;
+  const float* sim;
+  float theta, skip_slope;
+  // policy
+  float p_exit, budget, omega_t, t_local, t_remote, phi_scale, sim_min;
+  const float* p_exit_tok;
+  const float* budget_tok;
+  // state
+  int T;
+  void* h;
+  float* d_acc;
+  int32_t* active_idx;
+  int32_t* n_active;
+  int32_t* exit_layer;
+  float* xi;
+  // trace (already offset to this layer's rows; all NULL when no trace)
+  int8_t* tr_action;
+  int16_t* tr_target;
+  int16_t* tr_exec;
+  int8_t* tr_kind;
+  float* tr_gate;
+  float* tr_importance;
+  float* tr_xi;
+  float* tr_d_acc;
+  int32_t* tr_counters;
+  // workspace
+  int32_t* sub_c;      // [E]
+  float* sub_q;        // [E]
+  int32_t* tok_exec;   // [T*k] merged rows per active position, -1 padded
+  float* tok_w;        // [T*k]
+  int32_t* tok_row;    // [T*k] permuted row of each merged row
+  int32_t* tok_action; // [T]   ACT_EXEC / ACT_SKIP per active position
+  int32_t* tok_keep;   // [T]   1 = still active after this layer
+  int32_t* exec_list;  // [T]   token id of each executed token (active order)
+  int32_t* exec_pos;   // [T]   active position of each executed token
+  int32_t* blk_cnt;    // [nblk*E]
+  int32_t* blk_off;    // [nblk*E]
+  int32_t* blk_xcnt;   // [nblk]
+  int32_t* blk_xoff;   // [nblk]
+  int32_t* exp_off;    // [E+1]
+  int32_t* counts;     // [kCntSlots]
+  int4* tiles;         // [max_tiles] (expert, row begin, row end, 0)
+  void* x_perm;        // [T*k, d]
+  void* act_buf;       // [T*k, F]
+  float* y_buf;        // [T*k, d]
+  void* xs;            // [T, d]    shared-expert input rows
+  void* act_s;         // [T, Fs]
+  float* y_s;          // [T, d]
+  void* hx;            // [T, d]    updated rows of executed tokens
+  float2* partials;    // [T, n_vtiles] (max, sum exp) per vocabulary tile
+  int n_vtiles;
+  int max_tiles;
+};
+
+// launchers (decide.hip)
+hipError_t launch_state_reset(const trimmoe_model* m, const trimmoe_state* s,
+                              hipStream_t st);
+hipError_t launch_trace_fill(const LayerParams& p, hipStream_t st);
+hipError_t launch_subst(const LayerParams& p, hipStream_t st);
+hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st);
+hipError_t launch_scan(const LayerParams& p, hipStream_t st);
+hipError_t launch_permute(const LayerParams& p, bool bf16, hipStream_t st);
+hipError_t launch_combine(const LayerParams& p, bool bf16, hipStream_t st);
+hipError_t launch_exit_reduce(const LayerParams& p, hipStream_t st);
+hipError_t launch_compact(const LayerParams& p, hipStream_t st);
+
+// launchers (gemm.hip)
+hipError_t launch_expert_ffn(const LayerParams& p, bool bf16, hipStream_t st);
+hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st);
+
+}  // namespace trimmoe

@@ -1,0 +1,607 @@
+// Decision-side kernels of the adaptive-depth MoE step (gfx950):
+//   substitution table, routing + online decision, bucketing of the executed
+//   (token, expert) rows, row permutation, weighted combine, exit gate and
+//   the stable compaction of the active-token list.
+//
+// The decision rule is TrimMoE's online algorithm (arXiv 2608.00573,
+// Sec. V, Algorithm 2 in Table II) at look-ahead horizon H = 1:
+//   * routing / importance:        Sec. III-B, Eq. (4)
+//   * substitution loss:           Sec. III-A, Eq. (3)
+//   * skip degradation:            Sec. III-B, Eq. (5), rho(I) = min(1, s_l I)
+//   * execute / skip cost:         Sec. V-A, Eq. (31), (32)
+//   * feasible action set:         Sec. V-B, Eq. (34)
+//   * transmission necessity:      Sec. V-C, Eq. (35) + importance threshold
+//   * argmin and state update:     Sec. V-E, Eq. (40)-(42)
+//   * exit gate:                   Sec. III-C, Eq. (8), (9)
+// With top-k > 1 every routed slot is resolved on its own under the one
+// per-token budget; the only useful substitute of a remote slot is its
+// minimum-Q local expert (same delay, least budget); ties: lower expert id
+// in top-k, then fewer substitutions, then the lower slot bitmask, and
+// execute before skip.  Comparisons are non-strict as printed (Eq. (8),
+// (34), Sec. V-C).
+#include <math.h>
+
+#include "common.h"
+
+namespace trimmoe {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int RB = kRouteTokens;
+constexpr int KMAX = TRIMMOE_MAX_TOPK;
+
+// ----------------------------------------------------------- state reset --
+__global__ void k_state_reset(int T, int N, float* d_acc, int32_t* active_idx,
+                              int32_t* n_active, int32_t* exit_layer, float* xi) {
+  int t = blockIdx.x * blockDim.x + threadIdx.x;
+  if (t == 0) *n_active = T;
+  if (t < T) {
+    d_acc[t] = 0.f;
+    active_idx[t] = t;
+    exit_layer[t] = N;
+    xi[t] = __int_as_float(0x7fc00000);
+  }
+}
+
+// ------------------------------------------------ trace: inactive default --
+__global__ void k_trace_fill(LayerParams p) {
+  int t = blockIdx.x * blockDim.x + threadIdx.x;
+  const float qnan = __int_as_float(0x7fc00000);
+  if (blockIdx.x == 0 && threadIdx.x < 8 && p.tr_counters) p.tr_counters[threadIdx.x] = 0;
+  if (t >= p.T) return;
+  if (p.tr_action) p.tr_action[t] = TRIMMOE_ACT_INACTIVE;
+  for (int s = 0; s < p.k; ++s) {
+    size_t o = (size_t)t * p.k + s;
+    if (p.tr_target) p.tr_target[o] = -1;
+    if (p.tr_exec) p.tr_exec[o] = -1;
+    if (p.tr_kind) p.tr_kind[o] = TRIMMOE_KIND_NONE;
+    if (p.tr_gate) p.tr_gate[o] = qnan;
+  }
+  if (p.tr_importance) p.tr_importance[t] = qnan;
+  if (p.tr_xi) p.tr_xi[t] = qnan;
+  if (p.tr_d_acc) p.tr_d_acc[t] = qnan;
+}
+
+// ------------------------------------- Eq. (3): best local substitute c(e) --
+// c(e) = argmin over local j != e with Sim[e][j] >= sim_min of
+// Q(e, j) = min(1, phi_scale * (1 - Sim[e][j]) / 2), ties to the lower j.
+__global__ void k_subst(LayerParams p) {
+  int e = threadIdx.x;
+  if (e >= p.E) return;
+  int best = -1;
+  float bq = 0.f;
+  for (int j = 0; j < p.E; ++j) {
+    if (j == e || !p.local_mask[j]) continue;
+    float s = p.sim[(size_t)e * p.E + j];
+    if (!(s >= p.sim_min)) continue;
+    float q = fminf(1.f, p.phi_scale * (1.f - s) * 0.5f);
+    if (best < 0 || q < bq) {
+      best = j;
+      bq = q;
+    }
+  }
+  p.sub_c[e] = best;
+  p.sub_q[e] = bq;
+}
+
+// ------------------------------------------- route + decide (one layer) --
+// One block = RB active tokens.  Phase 1: router logits into LDS (MFMA
+// 16x16x32 bf16 tiles, or fp32 FMA).  Phase 2: one thread per token runs
+// the decision.  Phase 3: per-block expert histogram for the bucketing.
+template <bool BF16>
+__global__ __launch_bounds__(256) void k_route(LayerParams p) {
+  extern __shared__ float zs[];  // [RB][E]
+  __shared__ int s_cnt[TRIMMOE_MAX_EXPERTS];
+  __shared__ int s_xcnt;
+  __shared__ int sS[RB][KMAX];
+  __shared__ float sQ[RB][KMAX];
+  __shared__ float sW[RB][KMAX];    // slot weights in rank order
+  __shared__ int sRsub[RB][KMAX];   // ranks of substitutable remote slots
+  __shared__ int sRx[RB][KMAX];     // merged rows: expert
+  __shared__ float sRw[RB][KMAX];   // merged rows: summed weight
+
+  const int n_a = *p.n_active;
+  const int base = blockIdx.x * RB;
+  if (base >= n_a) return;
+  const int nt = min(RB, n_a - base);
+  const int E = p.E, d = p.d, k = p.k;
+  for (int e = threadIdx.x; e < E; e += blockDim.x) s_cnt[e] = 0;
+  if (threadIdx.x == 0) s_xcnt = 0;
+
+  if constexpr (BF16) {
+    const bf16_t* h = static_cast<const bf16_t*>(p.h);
+    const bf16_t* W = static_cast<const bf16_t*>(p.w_router);
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int nct = (E + 15) >> 4;
+    for (int tile = wave; tile < 2 * nct; tile += 4) {
+      const int rt = tile & 1, ct = tile >> 1;
+      const int tl = rt * 16 + (lane & 15);
+      const bool tv = tl < nt;
+      const int t = tv ? p.active_idx[base + tl] : 0;
+      const int e = ct * 16 + (lane & 15);
+      const bool ev = e < E;
+      const bf16_t* hr = h + (size_t)t * d + 8 * (lane >> 4);
+      const bf16_t* wr = W + (size_t)(ev ? e : 0) * d + 8 * (lane >> 4);
+      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+      for (int k0 = 0; k0 < d; k0 += 32) {
+        uint4 av = tv ? *reinterpret_cast<const uint4*>(hr + k0) : make_uint4(0, 0, 0, 0);
+        uint4 bv = ev ? *reinterpret_cast<const uint4*>(wr + k0) : make_uint4(0, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
+                                                      __builtin_bit_cast(bf16x8_t, bv),
+                                                      acc, 0, 0, 0);
+      }
+      // accumulator: column = lane % 16 (expert), row = 4 * (lane / 16) + r (token)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = rt * 16 + 4 * (lane >> 4) + r;
+        if (row < nt && ev) zs[row * E + e] = acc[r];
+      }
+    }
+  } else {
+    const float* h = static_cast<const float*>(p.h);
+    const float* W = static_cast<const float*>(p.w_router);
+    for (int idx = threadIdx.x; idx < nt * E; idx += blockDim.x) {
+      const int i = idx / E, e = idx % E;
+      const int t = p.active_idx[base + i];
+      const float* hr = h + (size_t)t * d;
+      const float* wr = W + (size_t)e * d;
+      float acc = 0.f;
+      for (int j = 0; j < d; ++j) acc = fmaf(hr[j], wr[j], acc);
+      zs[i * E + e] = acc;
+    }
+  }
+  __syncthreads();
+
+  const int i = threadIdx.x;
+  if (i < nt) {
+    const int pos = base + i;
+    const int t = p.active_idx[pos];
+    float* z = zs + i * E;
+    const float ninf = -__builtin_inff();
+    for (int e = 0; e < E; ++e) {
+      float v = z[e] + (p.b_router ? p.b_router[e] : 0.f);
+      z[e] = (v == v) ? v : ninf;  // NaN ranks last
+    }
+    // top-k in rank order (ties to the lower id), selection without flags:
+    // the next pick is the largest logit ranked strictly after the last one
+    float vprev = 0.f;
+    int iprev = -1;
+    for (int r = 0; r < k; ++r) {
+      int be = -1;
+      float bv = 0.f;
+      for (int e = 0; e < E; ++e) {
+        const float v = z[e];
+        const bool after = (r == 0) || (v < vprev) || (v == vprev && e > iprev);
+        if (after && (be < 0 || v > bv)) {
+          be = e;
+          bv = v;
+        }
+      }
+      sS[i][r] = be;
+      vprev = bv;
+      iprev = be;
+    }
+    // softmax over all E (Eq. (4)): p_e = exp(z_e - max) / sum
+    const float zmax = z[sS[i][0]];
+    float sum = 0.f;
+    for (int e = 0; e < E; ++e) sum += expf(z[e] - zmax);
+    float I = 0.f;
+    for (int r = 0; r < k; ++r) {
+      const float pr = expf(z[sS[i][r]] - zmax) / sum;
+      sW[i][r] = pr;
+      I += pr;
+    }
+    if (p.normalize)
+      for (int r = 0; r < k; ++r) sW[i][r] = sW[i][r] / I;
+
+    // resolve slots: local exact, or remote with/without a local substitute
+    int n_loc = 0, n_rem = 0, nsub = 0;
+    for (int r = 0; r < k; ++r) {
+      const int e = sS[i][r];
+      if (p.local_mask[e]) {
+        ++n_loc;
+        sQ[i][r] = 0.f;
+      } else {
+        ++n_rem;
+        const int c = p.sub_c[e];
+        sQ[i][r] = c >= 0 ? p.sub_q[e] : 0.f;
+        if (c >= 0) sRsub[i][nsub++] = r;
+      }
+    }
+    const float budget = p.budget_tok ? p.budget_tok[t] : p.budget;
+    const float D = p.d_acc[t];
+    const float wt = p.omega_t, wd = 1.f - p.omega_t;
+    // Eq. (34) + Eq. (31): enumerate substitution subsets of remote slots
+    bool have = false, all_local = false;
+    float bf = 0.f, bsq = 0.f;
+    int bns = 0, bmask = 0;
+    for (int sel = 0; sel < (1 << nsub); ++sel) {
+      float sq = 0.f;
+      int mask = 0;
+      for (int u = 0; u < nsub; ++u) {
+        if ((sel >> u) & 1) {
+          mask |= 1 << sRsub[i][u];
+          sq += sQ[i][sRsub[i][u]];
+        }
+      }
+      if (!(D + sq <= budget)) continue;
+      const int ns = __popc(sel);
+      if (ns == n_rem) all_local = true;
+      const float f = wt * ((float)(n_loc + ns) * p.t_local + (float)(n_rem - ns) * p.t_remote) +
+                      (budget > 0.f ? wd * sq / budget : 0.f);
+      const bool better = !have || f < bf || (f == bf && (ns < bns || (ns == bns && mask < bmask)));
+      if (better) {
+        have = true;
+        bf = f;
+        bns = ns;
+        bmask = mask;
+        bsq = sq;
+      }
+    }
+    // Eq. (35) + importance threshold + Eq. (32): skip admission and choice
+    const float lam = fminf(1.f, p.skip_slope * I);
+    bool skip = false;
+    if (!all_local && I <= p.theta && D + lam <= budget) {
+      const float fs = budget > 0.f ? wd * lam / budget : 0.f;
+      skip = fs < bf;
+    }
+    if (!have) skip = false;  // unreachable: the empty assignment is feasible
+
+    // per-slot execution and merged rows (a substitute keeps its target's weight)
+    int nrows = 0, nsubst = 0, nremote = 0;
+    for (int r = 0; r < k; ++r) {
+      const int e = sS[i][r];
+      int x = -1, kind = TRIMMOE_KIND_NONE;
+      if (!skip) {
+        if ((bmask >> r) & 1) {
+          x = p.sub_c[e];
+          kind = TRIMMOE_KIND_SUBST;
+          ++nsubst;
+        } else {
+          x = e;
+          kind = p.local_mask[e] ? TRIMMOE_KIND_LOCAL : TRIMMOE_KIND_REMOTE;
+          if (kind == TRIMMOE_KIND_REMOTE) ++nremote;
+        }
+        int j = 0;
+        for (; j < nrows; ++j)
+          if (sRx[i][j] == x) break;
+        if (j < nrows) {
+          sRw[i][j] += sW[i][r];  // merge duplicates in rank order
+        } else {
+          sRx[i][nrows] = x;
+          sRw[i][nrows] = sW[i][r];
+          ++nrows;
+        }
+      }
+      if (p.tr_target) p.tr_target[(size_t)t * k + r] = (int16_t)e;
+      if (p.tr_exec) p.tr_exec[(size_t)t * k + r] = (int16_t)x;
+      if (p.tr_kind) p.tr_kind[(size_t)t * k + r] = (int8_t)kind;
+      if (p.tr_gate) p.tr_gate[(size_t)t * k + r] = sW[i][r];
+    }
+    for (int j = 0; j < k; ++j) {
+      p.tok_exec[(size_t)pos * k + j] = j < nrows ? sRx[i][j] : -1;
+      p.tok_w[(size_t)pos * k + j] = j < nrows ? sRw[i][j] : 0.f;
+    }
+    const float dnew = D + (skip ? lam : bsq);  // Eq. (41) / (42)
+    p.d_acc[t] = dnew;
+    p.tok_action[pos] = skip ? TRIMMOE_ACT_SKIP : TRIMMOE_ACT_EXEC;
+    p.tok_keep[pos] = 1;
+    for (int j = 0; j < nrows; ++j) atomicAdd(&s_cnt[sRx[i][j]], 1);
+    if (!skip) atomicAdd(&s_xcnt, 1);
+    if (p.tr_action) p.tr_action[t] = skip ? TRIMMOE_ACT_SKIP : TRIMMOE_ACT_EXEC;
+    if (p.tr_importance) p.tr_importance[t] = I;
+    if (p.tr_d_acc) p.tr_d_acc[t] = dnew;
+    if (p.tr_counters) {
+      atomicAdd(&p.tr_counters[0], 1);
+      atomicAdd(&p.tr_counters[skip ? 2 : 1], 1);
+      if (nsubst) atomicAdd(&p.tr_counters[4], nsubst);
+      if (nremote) atomicAdd(&p.tr_counters[5], nremote);
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < E; e += blockDim.x) p.blk_cnt[(size_t)blockIdx.x * E + e] = s_cnt[e];
+  if (threadIdx.x == 0) p.blk_xcnt[blockIdx.x] = s_xcnt;
+}
+
+// ------------------------------------------- expert offsets and tile list --
+__global__ __launch_bounds__(256) void k_scan(LayerParams p) {
+  __shared__ int s_tot[TRIMMOE_MAX_EXPERTS];
+  __shared__ int s_off[TRIMMOE_MAX_EXPERTS + 1];
+  __shared__ int s_toff[TRIMMOE_MAX_EXPERTS + 1];
+  const int n_a = *p.n_active;
+  const int nb = (n_a + RB - 1) / RB;
+  const int E = p.E;
+  const int e = threadIdx.x;
+  if (e < E) {
+    int run = 0;
+    for (int b = 0; b < nb; ++b) {
+      const int c = p.blk_cnt[(size_t)b * E + e];
+      p.blk_off[(size_t)b * E + e] = run;
+      run += c;
+    }
+    s_tot[e] = run;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int off = 0, toff = 0, distinct = 0;
+    for (int x = 0; x < E; ++x) {
+      s_off[x] = off;
+      s_toff[x] = toff;
+      off += s_tot[x];
+      toff += (s_tot[x] + kGemmBM - 1) / kGemmBM;
+      distinct += s_tot[x] > 0;
+    }
+    s_off[E] = off;
+    s_toff[E] = toff;
+    int xo = 0;
+    for (int b = 0; b < nb; ++b) {
+      p.blk_xoff[b] = xo;
+      xo += p.blk_xcnt[b];
+    }
+    p.counts[kCntRows] = off;
+    p.counts[kCntTiles] = toff;
+    p.counts[kCntExec] = xo;
+    p.exp_off[E] = off;
+    if (p.tr_counters) {
+      p.tr_counters[6] = off;
+      p.tr_counters[7] = distinct;
+    }
+  }
+  __syncthreads();
+  if (e < E) {
+    p.exp_off[e] = s_off[e];
+    const int n = s_toff[e + 1] - s_toff[e];
+    for (int u = 0; u < n; ++u)
+      p.tiles[s_toff[e] + u] = make_int4(e, s_off[e] + u * kGemmBM, s_off[e] + s_tot[e], 0);
+  }
+}
+
+// ------------------------------------------------- stable row permutation --
+// Row of (active position pos, merged row j with expert e) =
+//   exp_off[e] + (rows of e in earlier blocks) + (rows of e earlier in block),
+// i.e. rows of one expert stay in token order.  Copies h rows into x_perm
+// (and into xs for the shared expert) with 16-byte vectors.
+template <typename ST>
+__global__ __launch_bounds__(256) void k_permute(LayerParams p) {
+  __shared__ int s_exec[RB * KMAX];
+  __shared__ int s_row[RB * KMAX];
+  __shared__ int s_tok[RB];
+  __shared__ int s_act[RB];
+  __shared__ int s_xidx[RB];
+  const int n_a = *p.n_active;
+  const int base = blockIdx.x * RB;
+  if (base >= n_a) return;
+  const int nt = min(RB, n_a - base);
+  const int k = p.k, E = p.E;
+  const int i = threadIdx.x;
+  if (i < nt) {
+    const int pos = base + i;
+    s_tok[i] = p.active_idx[pos];
+    s_act[i] = p.tok_action[pos];
+    for (int j = 0; j < k; ++j) s_exec[i * k + j] = p.tok_exec[(size_t)pos * k + j];
+  }
+  __syncthreads();
+  if (i < nt) {
+    const int pos = base + i;
+    for (int j = 0; j < k; ++j) {
+      const int e = s_exec[i * k + j];
+      if (e < 0) {
+        s_row[i * k + j] = -1;
+        continue;
+      }
+      int rank = 0;
+      for (int i2 = 0; i2 < i; ++i2)
+        for (int j2 = 0; j2 < k; ++j2) rank += (s_exec[i2 * k + j2] == e);
+      const int row = p.exp_off[e] + p.blk_off[(size_t)blockIdx.x * E + e] + rank;
+      s_row[i * k + j] = row;
+      p.tok_row[(size_t)pos * k + j] = row;
+    }
+    if (s_act[i] == TRIMMOE_ACT_EXEC) {
+      int xr = 0;
+      for (int i2 = 0; i2 < i; ++i2) xr += (s_act[i2] == TRIMMOE_ACT_EXEC);
+      const int xidx = p.blk_xoff[blockIdx.x] + xr;
+      p.exec_list[xidx] = s_tok[i];
+      p.exec_pos[xidx] = pos;
+      s_xidx[i] = xidx;
+    } else {
+      s_xidx[i] = -1;
+    }
+  }
+  __syncthreads();
+  const ST* h = static_cast<const ST*>(p.h);
+  ST* xp = static_cast<ST*>(p.x_perm);
+  const int vec = 16 / sizeof(ST);
+  const int nchunk = p.d / vec;
+  for (int idx = threadIdx.x; idx < nt * k * nchunk; idx += blockDim.x) {
+    const int q = idx / nchunk, c = idx % nchunk;
+    const int row = s_row[q];
+    if (row < 0) continue;
+    const int t = s_tok[q / k];
+    reinterpret_cast<uint4*>(xp + (size_t)row * p.d)[c] =
+        reinterpret_cast<const uint4*>(h + (size_t)t * p.d)[c];
+  }
+  if (p.Fs > 0) {
+    ST* xs = static_cast<ST*>(p.xs);
+    for (int idx = threadIdx.x; idx < nt * nchunk; idx += blockDim.x) {
+      const int q = idx / nchunk, c = idx % nchunk;
+      const int xidx = s_xidx[q];
+      if (xidx < 0) continue;
+      reinterpret_cast<uint4*>(xs + (size_t)xidx * p.d)[c] =
+          reinterpret_cast<const uint4*>(h + (size_t)s_tok[q] * p.d)[c];
+    }
+  }
+}
+
+// ------------------------------------------------ weighted combine (R4) --
+// h[t] <- round(h[t] + sum_rows w * Y[row] (+ shared Y)), summed in rank
+// order in fp32 and rounded once; the new row is also written to hx (the
+// exit head's input).  Skipped and inactive tokens are untouched.
+template <typename ST>
+__global__ __launch_bounds__(256) void k_combine(LayerParams p) {
+  __shared__ int s_row[KMAX];
+  __shared__ float s_w[KMAX];
+  __shared__ int s_n;
+  const int n_x = p.counts[kCntExec];
+  ST* h = static_cast<ST*>(p.h);
+  ST* hx = static_cast<ST*>(p.hx);
+  for (int j = blockIdx.x; j < n_x; j += gridDim.x) {
+    const int pos = p.exec_pos[j];
+    const int t = p.exec_list[j];
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int n = 0;
+      for (int s = 0; s < p.k; ++s) {
+        const int e = p.tok_exec[(size_t)pos * p.k + s];
+        if (e < 0) break;
+        s_row[n] = p.tok_row[(size_t)pos * p.k + s];
+        s_w[n] = p.tok_w[(size_t)pos * p.k + s];
+        ++n;
+      }
+      s_n = n;
+    }
+    __syncthreads();
+    const int n = s_n;
+    for (int c = threadIdx.x; c < p.d; c += blockDim.x) {
+      float acc = 0.f;
+      for (int s = 0; s < n; ++s) acc += s_w[s] * p.y_buf[(size_t)s_row[s] * p.d + c];
+      if (p.Fs > 0) acc += p.y_s[(size_t)j * p.d + c];
+      const float v = to_f32<ST>(h[(size_t)t * p.d + c]) + acc;
+      const ST o = from_f32<ST>(v);
+      h[(size_t)t * p.d + c] = o;
+      hx[(size_t)j * p.d + c] = o;
+    }
+  }
+}
+
+// -------------------------------------------- exit confidence and gate --
+// xi = 1 / sum_tiles s_i exp(m_i - M) (softmax max-probability from the
+// per-tile partial maxima and sums), or sigmoid of the single logit;
+// exit iff xi >= p_J (Eq. (8)).  One wavefront per executed token.
+__global__ __launch_bounds__(256) void k_exit_reduce(LayerParams p) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int j = blockIdx.x * 4 + wave;
+  const int n_x = p.counts[kCntExec];
+  if (j >= n_x) return;
+  const int nv = p.n_vtiles;
+  const float2* pr = p.partials + (size_t)j * nv;
+  float m = -__builtin_inff();
+  for (int u = lane; u < nv; u += 64) m = fmaxf(m, pr[u].x);
+  for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  float s = 0.f;
+  for (int u = lane; u < nv; u += 64) {
+    const float2 v = pr[u];
+    if (v.y > 0.f) s += v.y * expf(v.x - m);
+  }
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  if (lane == 0) {
+    const float xi = p.conf_mode == TRIMMOE_CONF_SIGMOID ? 1.f / (1.f + expf(-m)) : 1.f / s;
+    const int t = p.exec_list[j];
+    const int pos = p.exec_pos[j];
+    p.xi[t] = xi;
+    if (p.tr_xi) p.tr_xi[t] = xi;
+    const float pj = p.p_exit_tok ? p.p_exit_tok[t] : p.p_exit;
+    if (xi >= pj) {
+      p.exit_layer[t] = p.layer;
+      p.tok_keep[pos] = 0;
+    }
+  }
+}
+
+// ------------------------------------- stable compaction of active list --
+// In place, one block, chunk by chunk: every write of a chunk lands before
+// the chunk's own start, and all its reads finish before the first write.
+__global__ __launch_bounds__(1024) void k_compact(LayerParams p) {
+  __shared__ int s_scan[1024];
+  __shared__ int s_total;
+  const int n_a = *p.n_active;
+  int out = 0;
+  for (int c0 = 0; c0 < n_a; c0 += 1024) {
+    const int i = c0 + threadIdx.x;
+    const int keep = i < n_a ? p.tok_keep[i] : 0;
+    const int idx = i < n_a ? p.active_idx[i] : 0;
+    s_scan[threadIdx.x] = keep;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+      const int v = threadIdx.x >= o ? s_scan[threadIdx.x - o] : 0;
+      __syncthreads();
+      s_scan[threadIdx.x] += v;
+      __syncthreads();
+    }
+    const int incl = s_scan[threadIdx.x];
+    if (threadIdx.x == 1023) s_total = incl;
+    __syncthreads();
+    if (keep) p.active_idx[out + incl - 1] = idx;
+    out += s_total;
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    *p.n_active = out;
+    if (p.tr_counters) p.tr_counters[3] = n_a - out;
+  }
+}
+
+// -------------------------------------------------------------- launchers --
+static inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+hipError_t launch_state_reset(const trimmoe_model* m, const trimmoe_state* s, hipStream_t st) {
+  const int T = s->n_tokens;
+  hipLaunchKernelGGL(k_state_reset, dim3(cdiv(T > 0 ? T : 1, 256)), dim3(256), 0, st, T,
+                     m->n_layers, s->d_acc, s->active_idx, s->n_active, s->exit_layer, s->xi);
+  return hipGetLastError();
+}
+
+hipError_t launch_trace_fill(const LayerParams& p, hipStream_t st) {
+  hipLaunchKernelGGL(k_trace_fill, dim3(cdiv(p.T > 0 ? p.T : 1, 256)), dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_subst(const LayerParams& p, hipStream_t st) {
+  hipLaunchKernelGGL(k_subst, dim3(1), dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st) {
+  const int nb = cdiv(p.T, RB);
+  const size_t lds = (size_t)RB * p.E * sizeof(float);
+  if (bf16)
+    hipLaunchKernelGGL(k_route<true>, dim3(nb), dim3(256), lds, st, p);
+  else
+    hipLaunchKernelGGL(k_route<false>, dim3(nb), dim3(256), lds, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_scan(const LayerParams& p, hipStream_t st) {
+  hipLaunchKernelGGL(k_scan, dim3(1), dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute(const LayerParams& p, bool bf16, hipStream_t st) {
+  const int nb = cdiv(p.T, RB);
+  if (bf16)
+    hipLaunchKernelGGL(k_permute<bf16_t>, dim3(nb), dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(k_permute<float>, dim3(nb), dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine(const LayerParams& p, bool bf16, hipStream_t st) {
+  const int nb = p.T < 2048 ? p.T : 2048;
+  if (bf16)
+    hipLaunchKernelGGL(k_combine<bf16_t>, dim3(nb), dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(k_combine<float>, dim3(nb), dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_exit_reduce(const LayerParams& p, hipStream_t st) {
+  hipLaunchKernelGGL(k_exit_reduce, dim3(cdiv(p.T, 4)), dim3(256), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_compact(const LayerParams& p, hipStream_t st) {
+  hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, st, p);
+  return hipGetLastError();
+}
+
+}  // namespace trimmoe

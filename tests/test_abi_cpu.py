@@ -1,0 +1,165 @@
+"""Host-side checks of the C ABI: symbols, workspace sizing, validation.
+
+Nothing here launches a kernel: every call either is host-only
+(trimmoe_workspace_size, trimmoe_status_str, trimmoe_abi_version) or fails
+validation, which happens before any HIP call.
+"""
+import ctypes as C
+import os
+import re
+
+import pytest
+import torch
+
+from paper_2608_00573_amd import abi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    txt = open(os.path.join(ROOT, "include", "trimmoe.h")).read()
+    return sorted(set(re.findall(r"^\w[\w\s\*]*?\b(trimmoe_\w+)\s*\(", txt, re.M)))
+
+
+def test_header_declares_the_binding_exports():
+    assert _declared() == sorted(abi.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = abi.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+    assert abi.trimmoe_abi_version() == 1
+    assert abi.trimmoe_status_str(0) == "ok"
+    assert "workspace" in abi.trimmoe_status_str(-6)
+
+
+def _fake_layers(n, E, with_gate=True, shared=False):
+    # host tensors used only for their (non-null, aligned) addresses; no call
+    # below reaches a kernel
+    t = torch.zeros(64, dtype=torch.float32)
+    L = dict(w_router=t, b_router=None, w_up=t, w_gate=t if with_gate else None, w_down=t,
+             ws_up=t if shared else None, ws_gate=t if shared else None,
+             ws_down=t if shared else None, w_exit=t, b_exit=None, local_mask=t, sim=t,
+             theta=0.5, skip_slope=0.01)
+    return [dict(L) for _ in range(n)]
+
+
+DIMS = dict(n_layers=2, d_model=64, n_experts=8, top_k=2, d_ff=128, d_ff_shared=0,
+            vocab_exit=512, dtype="bf16", act="swiglu", normalize_topk=1)
+
+
+def _handle(**over):
+    dims = dict(DIMS, **over)
+    return abi.model_handle(dims, _fake_layers(dims["n_layers"], dims["n_experts"],
+                                               dims["act"] == "swiglu", dims["d_ff_shared"] > 0))
+
+
+def test_workspace_size_grows_with_tokens():
+    mh = _handle()
+    a = abi.trimmoe_workspace_size(mh.model, 64)
+    b = abi.trimmoe_workspace_size(mh.model, 4096)
+    assert 0 < a < b
+    assert abi.trimmoe_workspace_size(mh.model, 0) > 0
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(top_k=9), -2), (dict(n_experts=257, top_k=2), -2), (dict(top_k=9, n_experts=8), -2),
+    (dict(d_model=96), -2), (dict(d_ff=100), -2), (dict(n_layers=0), -2),
+    (dict(dtype="f32", d_model=66), -2),
+])
+def test_workspace_size_rejects_bad_shapes(over, code):
+    mh = _handle(**over)
+    with pytest.raises(abi.TrimmoeError) as ei:
+        abi.trimmoe_workspace_size(mh.model, 16)
+    assert ei.value.status == code
+
+
+def test_bad_enums_rejected():
+    mh = _handle()
+    mh.model.dtype = 7
+    with pytest.raises(abi.TrimmoeError) as ei:
+        abi.trimmoe_workspace_size(mh.model, 16)
+    assert ei.value.status == -3
+    mh = _handle()
+    mh.model.conf_mode = 1  # sigmoid needs V == 1
+    with pytest.raises(abi.TrimmoeError) as ei:
+        abi.trimmoe_workspace_size(mh.model, 16)
+    assert ei.value.status == -2
+
+
+def test_missing_gate_and_shared_pointers():
+    mh = abi.model_handle(dict(DIMS), _fake_layers(2, 8, with_gate=False))
+    with pytest.raises(abi.TrimmoeError) as ei:
+        abi.trimmoe_workspace_size(mh.model, 16)
+    assert ei.value.status == -1
+    mh = abi.model_handle(dict(DIMS, d_ff_shared=128), _fake_layers(2, 8))
+    with pytest.raises(abi.TrimmoeError) as ei:
+        abi.trimmoe_workspace_size(mh.model, 16)
+    assert ei.value.status == -1
+
+
+def _state_stub(T=16):
+    t = torch.zeros(max(T, 1) * 64, dtype=torch.float32)
+    return abi.State(T, t.data_ptr(), t.data_ptr(), t.data_ptr(), t.data_ptr(), t.data_ptr(),
+                     t.data_ptr()), t
+
+
+POL = dict(p_exit=0.9, budget=0.02, omega_t=0.5, t_local=1.0, t_remote=100.0, phi_scale=1.0,
+           sim_min=-1.0)
+
+
+@pytest.mark.parametrize("over,code", [
+    (dict(omega_t=1.5), -4), (dict(budget=-0.1), -4), (dict(p_exit=float("nan")), -4),
+    (dict(t_remote=-1.0), -4), (dict(phi_scale=float("inf")), -4),
+])
+def test_layer_step_rejects_bad_policy_before_launch(over, code):
+    mh = _handle()
+    st, keep = _state_stub()
+    pol = abi.make_policy(**dict(POL, **over))
+    ws = torch.zeros(1 << 20, dtype=torch.uint8)
+    with pytest.raises(abi.TrimmoeError) as ei:
+        abi.trimmoe_layer_step(mh.model, 0, pol, st, None, ws, stream=torch.cuda.Stream
+                               if False else _NullStream())
+    assert ei.value.status == code
+    assert torch.count_nonzero(keep) == 0  # nothing written
+
+
+class _NullStream:
+    cuda_stream = 0
+
+
+def test_layer_step_rejects_bad_layer_workspace_and_state():
+    mh = _handle()
+    st, keep = _state_stub()
+    pol = abi.make_policy(**POL)
+    L = abi.lib()
+    need = abi.trimmoe_workspace_size(mh.model, 16)
+    big = torch.zeros(need + 512, dtype=torch.uint8)
+    off = (-big.data_ptr()) % 256
+    ws = big[off:off + need]
+    # layer out of range
+    rc = L.trimmoe_layer_step(C.byref(mh.model), 2, C.byref(pol), C.byref(st), None,
+                              C.c_void_p(ws.data_ptr()), need, None)
+    assert rc == -5
+    # workspace too small / misaligned / NULL
+    rc = L.trimmoe_layer_step(C.byref(mh.model), 0, C.byref(pol), C.byref(st), None,
+                              C.c_void_p(ws.data_ptr()), need - 1, None)
+    assert rc == -6
+    rc = L.trimmoe_layer_step(C.byref(mh.model), 0, C.byref(pol), C.byref(st), None,
+                              C.c_void_p(ws.data_ptr() + 16), need, None)
+    assert rc == -6
+    rc = L.trimmoe_stack_forward(C.byref(mh.model), C.byref(pol), C.byref(st), None, None,
+                                 need, None)
+    assert rc == -6
+    # NULL state member
+    st.xi = None
+    rc = L.trimmoe_stack_forward(C.byref(mh.model), C.byref(pol), C.byref(st), None,
+                                 C.c_void_p(ws.data_ptr()), need, None)
+    assert rc == -1
+    # NULL model / policy
+    rc = L.trimmoe_stack_forward(None, C.byref(pol), C.byref(st), None,
+                                 C.c_void_p(ws.data_ptr()), need, None)
+    assert rc == -1
+    assert torch.count_nonzero(keep) == 0
+    assert torch.count_nonzero(ws) == 0

@@ -1,0 +1,122 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from synthgen import make_inputs, workload
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from tests.gpu_harness import (GpuRun, check_invariants_gpu, compare_stack, gpu_state_np,
+                                   gpu_trace_np, log, oracle_run, policy32, teacher_forced)
+
+
+def _run_and_compare(cfg, pol=None, **kw):
+    inp = make_inputs(cfg)
+    log(f"[parity] {cfg['name']} T={cfg['n_tokens']} N={cfg['n_layers']} {kw}")
+    g = GpuRun(inp)
+    st, tr = g.stack(pol=pol, **{k: v for k, v in kw.items() if k in ("p_exit_tok", "budget_tok")})
+    gst, gtr = gpu_state_np(st), gpu_trace_np(tr)
+    ref_state, ref_traces = oracle_run(inp, pol=pol, token_budget=kw.get("budget_tok"),
+                                       token_p_exit=kw.get("p_exit_tok"))
+    stats = compare_stack(cfg, ref_state, ref_traces, gst, gtr)
+    check_invariants_gpu(cfg, policy32(inp["policy"] if pol is None else pol), gst, gtr,
+                         kw.get("budget_tok"), kw.get("p_exit_tok"))
+    log(f"[parity] ok {stats}")
+    return inp, gst, gtr, ref_state, ref_traces, stats
+
+
+def test_tiny_fp32_stack():
+    cfg = workload("tiny_fp32")
+    _, gst, gtr, ref, _, stats = _run_and_compare(cfg)
+    assert stats["excluded_tokens"] <= 4
+    # the recipe reaches every branch of the rule on this case
+    assert (gtr["action"] == O.ACT_SKIP).any()
+    assert (gtr["kind"] == O.KIND_SUB).any()
+    assert (gst["exit_layer"] < cfg["n_layers"]).any()
+
+
+def test_tiny_bf16_swiglu_top2_shared():
+    cfg = workload("tiny_fp32", dtype="bf16", act="swiglu", top_k=2, d_ff_shared=128,
+                   normalize_topk=1, n_layers=3)
+    _run_and_compare(cfg)
+
+
+def test_ragged_tokens_bf16_relu():
+    # T not a multiple of any tile (route 32, GEMM 128)
+    cfg = workload("switch_base_8e", n_tokens=333, n_layers=3, d_model=256, d_ff=512,
+                   vocab_exit=1000)
+    _run_and_compare(cfg)
+
+
+def test_single_token():
+    cfg = workload("tiny_fp32", n_tokens=1, n_layers=3)
+    _run_and_compare(cfg)
+
+
+def test_all_tokens_exit_after_first_layer():
+    # p_J = 0: every token exits after layer 0, later layers see n_active = 0
+    cfg = workload("tiny_fp32", n_layers=4)
+    inp = make_inputs(cfg)
+    pol = dict(inp["policy"], p_exit=0.0)
+    _, gst, gtr, _, _, _ = _run_and_compare(cfg, pol=pol)
+    # a token exits right after its first executed layer; a skipped layer
+    # never triggers an exit (Eq. (9)), so skippers stay active until then
+    act = gtr["action"]
+    for t in range(cfg["n_tokens"]):
+        first = int(np.argmax(act[:, t] == O.ACT_EXEC)) if (act[:, t] == O.ACT_EXEC).any() else None
+        if first is not None and first < cfg["n_layers"] - 1:
+            assert gst["exit_layer"][t] == first
+            assert np.all(act[first + 1:, t] == O.ACT_INACTIVE)
+            assert np.all(act[:first, t] == O.ACT_SKIP)
+    assert (act[0] == O.ACT_EXEC).sum() > 0
+
+
+def test_zero_budget_and_per_token_arrays():
+    cfg = workload("tiny_fp32", n_layers=3)
+    inp = make_inputs(cfg)
+    T = cfg["n_tokens"]
+    budget_tok = np.where(np.arange(T) % 2 == 0, 0.0, 0.05).astype(np.float32)
+    pexit_tok = np.where(np.arange(T) % 3 == 0, 2.0, 0.5).astype(np.float32)
+    _, gst, _, _, _, _ = _run_and_compare(cfg, budget_tok=budget_tok, p_exit_tok=pexit_tok)
+    assert np.all(gst["d_acc"][budget_tok == 0] == 0)
+
+
+def test_switch_base_full_size():
+    # the benchmark workload: 6 layers, d=768, 8 experts top-1, 4096 tokens
+    cfg = workload("switch_base_8e")
+    _, gst, gtr, _, _, stats = _run_and_compare(cfg)
+    # a token leaves the comparison at its first decision within 1e-3 of a
+    # threshold; over 6 layers that is ~8% of tokens on this recipe
+    assert stats["excluded_tokens"] < 0.10 * cfg["n_tokens"]
+    c = gtr["counters"]
+    log(f"[switch] counters per layer (active, exec, skip, exit, subst, remote, rows, experts):\n{c}")
+    assert c[:, 2].sum() > 0 and c[:, 3].sum() > 0 and c[:, 4].sum() > 0
+
+
+def test_determinism_bitwise():
+    cfg = workload("switch_base_8e", n_tokens=1024, n_layers=3)
+    inp = make_inputs(cfg)
+    g = GpuRun(inp)
+    st1, tr1 = g.stack()
+    st2, tr2 = g.stack()
+    assert torch.equal(st1.h, st2.h)
+    for k in ("action", "exec", "gate", "xi", "d_acc", "counters"):
+        assert torch.equal(getattr(tr1, k).nan_to_num(0) if getattr(tr1, k).is_floating_point()
+                           else getattr(tr1, k),
+                           getattr(tr2, k).nan_to_num(0) if getattr(tr2, k).is_floating_point()
+                           else getattr(tr2, k)), k
+
+
+def test_switch_base_teacher_forced_layers():
+    # every layer of the benchmark workload on 1024 tokens, fed the oracle's
+    # exact state: decisions bit-exact outside a 1e-5 band
+    cfg = workload("switch_base_8e", n_tokens=1024)
+    stats = teacher_forced(make_inputs(cfg))
+    assert sum(s["excluded_tokens"] for s in stats) < 0.01 * 1024 * cfg["n_layers"]
+
+
+def test_tiny_fp32_teacher_forced():
+    teacher_forced(make_inputs(workload("tiny_fp32", n_layers=3)))
