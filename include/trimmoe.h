@@ -218,6 +218,35 @@ int trimmoe_stack_forward(const trimmoe_model* m, const trimmoe_policy* p,
                           void* workspace, size_t workspace_bytes,
                           void* stream);
 
+/*
+ * Kernel classes of one layer, in launch order, as timed by
+ * trimmoe_stack_forward_timed.
+ */
+#define TRIMMOE_TIMED_CLASSES 8
+#define TRIMMOE_CLASS_ROUTE 0    /* substitution table + route/decide       */
+#define TRIMMOE_CLASS_BUCKET 1   /* expert offsets/tiles + row permutation  */
+#define TRIMMOE_CLASS_UP 2       /* grouped up/gate GEMM + activation       */
+#define TRIMMOE_CLASS_DOWN 3     /* grouped down GEMM                       */
+#define TRIMMOE_CLASS_SHARED 4   /* shared expert up + down GEMMs           */
+#define TRIMMOE_CLASS_COMBINE 5  /* weighted combine + residual             */
+#define TRIMMOE_CLASS_EXIT 6     /* exit-head GEMM with softmax partials    */
+#define TRIMMOE_CLASS_GATE 7     /* exit gate + active-list compaction      */
+
+/*
+ * trimmoe_stack_forward, additionally recording caller-created HIP events
+ * (hipEvent_t passed as void*, created with timing enabled) on `stream`:
+ * events[l * (TRIMMOE_TIMED_CLASSES + 1) + c] before kernel class c of layer
+ * l and events[l * (TRIMMOE_TIMED_CLASSES + 1) + c + 1] after it (a class
+ * with no launch gives two back-to-back records).  n_events must be
+ * N * (TRIMMOE_TIMED_CLASSES + 1).  For measurement: the work is identical
+ * to trimmoe_stack_forward; nothing is synchronised.
+ */
+int trimmoe_stack_forward_timed(const trimmoe_model* m, const trimmoe_policy* p,
+                                trimmoe_state* s, trimmoe_trace* trace,
+                                void* workspace, size_t workspace_bytes,
+                                void* stream, void* const* events,
+                                int32_t n_events);
+
 #ifdef __cplusplus
 }
 #endif

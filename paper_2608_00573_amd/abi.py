@@ -62,7 +62,9 @@ class Trace(C.Structure):
 
 
 EXPORTS = ["trimmoe_abi_version", "trimmoe_status_str", "trimmoe_workspace_size",
-           "trimmoe_state_reset", "trimmoe_layer_step", "trimmoe_stack_forward"]
+           "trimmoe_state_reset", "trimmoe_layer_step", "trimmoe_stack_forward",
+           "trimmoe_stack_forward_timed"]
+TIMED_CLASSES = ["route", "bucket", "up", "down", "shared", "combine", "exit", "gate"]
 
 _lib = None
 
@@ -90,6 +92,11 @@ def lib():
         L.trimmoe_stack_forward.argtypes = [C.POINTER(Model), C.POINTER(Policy),
                                             C.POINTER(State), C.POINTER(Trace), C.c_void_p,
                                             C.c_size_t, C.c_void_p]
+        L.trimmoe_stack_forward_timed.restype = C.c_int
+        L.trimmoe_stack_forward_timed.argtypes = [C.POINTER(Model), C.POINTER(Policy),
+                                                  C.POINTER(State), C.POINTER(Trace),
+                                                  C.c_void_p, C.c_size_t, C.c_void_p,
+                                                  C.POINTER(C.c_void_p), C.c_int32]
         _lib = L
     return _lib
 
@@ -151,6 +158,18 @@ def trimmoe_stack_forward(model: Model, policy: Policy, state: State, trace,
            lib().trimmoe_stack_forward(C.byref(model), C.byref(policy), C.byref(state), tr,
                                        _ptr(workspace), workspace.numel(),
                                        _stream_handle(stream)))
+
+
+def trimmoe_stack_forward_timed(model: Model, policy: Policy, state: State, trace,
+                                workspace: torch.Tensor, events, stream=None):
+    """``events``: list of N * (len(TIMED_CLASSES) + 1) torch.cuda.Event(enable_timing=True)
+    already recorded once (so that their HIP events exist)."""
+    arr = (C.c_void_p * len(events))(*[e.cuda_event for e in events])
+    tr = C.byref(trace) if trace is not None else None
+    _check("trimmoe_stack_forward_timed",
+           lib().trimmoe_stack_forward_timed(C.byref(model), C.byref(policy), C.byref(state), tr,
+                                             _ptr(workspace), workspace.numel(),
+                                             _stream_handle(stream), arr, len(events)))
 
 
 # ------------------------------------------------ struct construction ------

@@ -194,25 +194,69 @@ int check_workspace(const trimmoe_model* m, const trimmoe_state* s, void* ws, si
   return TRIMMOE_OK;
 }
 
+// ev: NULL, or TRIMMOE_TIMED_CLASSES + 1 events recorded around the classes
 int run_layer(const trimmoe_model* m, int l, const trimmoe_policy* pol, const trimmoe_state* s,
-              const trimmoe_trace* tr, void* ws, hipStream_t st) {
+              const trimmoe_trace* tr, void* ws, hipStream_t st, hipEvent_t* ev) {
   if (s->n_tokens == 0) return TRIMMOE_OK;
   LayerParams P;
   memset(&P, 0, sizeof(P));
   carve(m, s->n_tokens, static_cast<char*>(ws), &P);
   fill_params(P, m, l, pol, s, tr);
   const bool bf16 = m->dtype == TRIMMOE_BF16;
-  if (any_trace(tr) && launch_trace_fill(P, st) != hipSuccess) return TRIMMOE_ERR_HIP;
-  if (launch_subst(P, st) != hipSuccess) return TRIMMOE_ERR_HIP;
-  if (launch_route(P, bf16, st) != hipSuccess) return TRIMMOE_ERR_HIP;
-  if (launch_scan(P, st) != hipSuccess) return TRIMMOE_ERR_HIP;
-  if (launch_permute(P, bf16, st) != hipSuccess) return TRIMMOE_ERR_HIP;
-  if (launch_expert_ffn(P, bf16, st) != hipSuccess) return TRIMMOE_ERR_HIP;
-  if (launch_combine(P, bf16, st) != hipSuccess) return TRIMMOE_ERR_HIP;
-  if (l < m->n_layers - 1) {
-    if (launch_exit_head(P, bf16, st) != hipSuccess) return TRIMMOE_ERR_HIP;
-    if (launch_exit_reduce(P, st) != hipSuccess) return TRIMMOE_ERR_HIP;
-    if (launch_compact(P, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  const bool last = l == m->n_layers - 1;
+#define TRIMMOE_TRY(x) \
+  if ((x) != hipSuccess) return TRIMMOE_ERR_HIP
+#define TRIMMOE_MARK(i) \
+  if (ev) TRIMMOE_TRY(hipEventRecord(ev[i], st))
+  TRIMMOE_MARK(0);
+  if (any_trace(tr)) TRIMMOE_TRY(launch_trace_fill(P, st));
+  TRIMMOE_TRY(launch_subst(P, st));
+  TRIMMOE_TRY(launch_route(P, bf16, st));
+  TRIMMOE_MARK(TRIMMOE_CLASS_ROUTE + 1);
+  TRIMMOE_TRY(launch_scan(P, st));
+  TRIMMOE_TRY(launch_permute(P, bf16, st));
+  TRIMMOE_MARK(TRIMMOE_CLASS_BUCKET + 1);
+  TRIMMOE_TRY(launch_expert_up(P, bf16, st));
+  TRIMMOE_MARK(TRIMMOE_CLASS_UP + 1);
+  TRIMMOE_TRY(launch_expert_down(P, bf16, st));
+  TRIMMOE_MARK(TRIMMOE_CLASS_DOWN + 1);
+  if (P.Fs > 0) TRIMMOE_TRY(launch_shared_expert(P, bf16, st));
+  TRIMMOE_MARK(TRIMMOE_CLASS_SHARED + 1);
+  TRIMMOE_TRY(launch_combine(P, bf16, st));
+  TRIMMOE_MARK(TRIMMOE_CLASS_COMBINE + 1);
+  if (!last) TRIMMOE_TRY(launch_exit_head(P, bf16, st));
+  TRIMMOE_MARK(TRIMMOE_CLASS_EXIT + 1);
+  if (!last) {
+    TRIMMOE_TRY(launch_exit_reduce(P, st));
+    TRIMMOE_TRY(launch_compact(P, st));
+  }
+  TRIMMOE_MARK(TRIMMOE_CLASS_GATE + 1);
+#undef TRIMMOE_MARK
+#undef TRIMMOE_TRY
+  return TRIMMOE_OK;
+}
+
+int stack(const trimmoe_model* m, const trimmoe_policy* p, trimmoe_state* s,
+          trimmoe_trace* trace, void* workspace, size_t workspace_bytes, void* stream,
+          void* const* events, int32_t n_events) {
+  int rc = validate_model(m);
+  if (rc) return rc;
+  if ((rc = validate_policy(p))) return rc;
+  if ((rc = validate_state(m, s))) return rc;
+  if ((rc = check_workspace(m, s, workspace, workspace_bytes))) return rc;
+  const int per = TRIMMOE_TIMED_CLASSES + 1;
+  if (events) {
+    if (n_events != m->n_layers * per) return TRIMMOE_ERR_SHAPE;
+    for (int i = 0; i < n_events; ++i)
+      if (!events[i]) return TRIMMOE_ERR_NULL;
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (s->n_tokens == 0) return TRIMMOE_OK;
+  if (launch_state_reset(m, s, st) != hipSuccess) return TRIMMOE_ERR_HIP;
+  for (int l = 0; l < m->n_layers; ++l) {
+    hipEvent_t* ev = events ? reinterpret_cast<hipEvent_t*>(const_cast<void**>(events)) + l * per
+                            : nullptr;
+    if ((rc = run_layer(m, l, p, s, trace, workspace, st, ev))) return rc;
   }
   return TRIMMOE_OK;
 }
@@ -264,23 +308,21 @@ int trimmoe_layer_step(const trimmoe_model* m, int32_t layer, const trimmoe_poli
   if ((rc = validate_state(m, s))) return rc;
   if (layer < 0 || layer >= m->n_layers) return TRIMMOE_ERR_LAYER;
   if ((rc = check_workspace(m, s, workspace, workspace_bytes))) return rc;
-  return run_layer(m, layer, p, s, trace, workspace, static_cast<hipStream_t>(stream));
+  return run_layer(m, layer, p, s, trace, workspace, static_cast<hipStream_t>(stream), nullptr);
 }
 
 int trimmoe_stack_forward(const trimmoe_model* m, const trimmoe_policy* p, trimmoe_state* s,
                           trimmoe_trace* trace, void* workspace, size_t workspace_bytes,
                           void* stream) {
-  int rc = validate_model(m);
-  if (rc) return rc;
-  if ((rc = validate_policy(p))) return rc;
-  if ((rc = validate_state(m, s))) return rc;
-  if ((rc = check_workspace(m, s, workspace, workspace_bytes))) return rc;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  if (s->n_tokens == 0) return TRIMMOE_OK;
-  if (launch_state_reset(m, s, st) != hipSuccess) return TRIMMOE_ERR_HIP;
-  for (int l = 0; l < m->n_layers; ++l)
-    if ((rc = run_layer(m, l, p, s, trace, workspace, st))) return rc;
-  return TRIMMOE_OK;
+  return stack(m, p, s, trace, workspace, workspace_bytes, stream, nullptr, 0);
+}
+
+int trimmoe_stack_forward_timed(const trimmoe_model* m, const trimmoe_policy* p,
+                                trimmoe_state* s, trimmoe_trace* trace, void* workspace,
+                                size_t workspace_bytes, void* stream, void* const* events,
+                                int32_t n_events) {
+  if (!events) return TRIMMOE_ERR_NULL;
+  return stack(m, p, s, trace, workspace, workspace_bytes, stream, events, n_events);
 }
 
 }  // extern "C"

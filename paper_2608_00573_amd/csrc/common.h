@@ -136,7 +136,9 @@ hipError_t launch_exit_reduce(const LayerParams& p, hipStream_t st);
 hipError_t launch_compact(const LayerParams& p, hipStream_t st);
 
 // launchers (gemm.hip)
-hipError_t launch_expert_ffn(const LayerParams& p, bool bf16, hipStream_t st);
+hipError_t launch_expert_up(const LayerParams& p, bool bf16, hipStream_t st);
+hipError_t launch_expert_down(const LayerParams& p, bool bf16, hipStream_t st);
+hipError_t launch_shared_expert(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st);
 
 }  // namespace trimmoe

@@ -422,15 +422,18 @@ static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared
   return hipGetLastError();
 }
 
-hipError_t launch_expert_ffn(const LayerParams& p, bool bf16, hipStream_t st) {
-  hipError_t e;
-  if ((e = ffn_pass(p, bf16, true, false, st)) != hipSuccess) return e;
-  if ((e = ffn_pass(p, bf16, false, false, st)) != hipSuccess) return e;
-  if (p.Fs > 0) {
-    if ((e = ffn_pass(p, bf16, true, true, st)) != hipSuccess) return e;
-    if ((e = ffn_pass(p, bf16, false, true, st)) != hipSuccess) return e;
-  }
-  return hipSuccess;
+hipError_t launch_expert_up(const LayerParams& p, bool bf16, hipStream_t st) {
+  return ffn_pass(p, bf16, true, false, st);
+}
+
+hipError_t launch_expert_down(const LayerParams& p, bool bf16, hipStream_t st) {
+  return ffn_pass(p, bf16, false, false, st);
+}
+
+hipError_t launch_shared_expert(const LayerParams& p, bool bf16, hipStream_t st) {
+  hipError_t e = ffn_pass(p, bf16, true, true, st);
+  if (e != hipSuccess) return e;
+  return ffn_pass(p, bf16, false, true, st);
 }
 
 hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
