@@ -42,7 +42,25 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain device copy of known size (to scale HBM byte "
+                         "counters) and exit")
     return ap.parse_args()
+
+
+def calibrate_copy():
+    """A plain copy of 512 MiB, five times: the known bytes per dispatch that
+    FETCH_SIZE / WRITE_SIZE of the same run are divided by."""
+    import torch
+    n = 512 << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda:0").fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes_read": n, "calibrate_copy_bytes_written": n,
+                      "dispatches": 5}), flush=True)
 
 
 def algorithmic_work(cfg, counters):
@@ -115,6 +133,9 @@ def main():
         print("bench.py measures one MI355X: this build runs on a single GPU "
               "(no sharding or collectives); run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
 
     import numpy as np
     import torch

@@ -114,7 +114,10 @@ size_t carve(const trimmoe_model* m, int T, char* base, LayerParams* p) {
   P.tiles = (int4*)take((size_t)max_tiles * 16);
   P.x_perm = take(R * d * es);
   P.act_buf = take(R * F * es);
-  P.y_buf = (float*)take(R * d * 4);
+  const int splits = bf16 ? down_splits(max_tiles, d, F) : 1;
+  P.y_buf = (float*)take((size_t)splits * R * d * 4);
+  P.y_split_stride = R * d;
+  P.down_splits = splits;
   P.xs = Fs ? take((size_t)Tm * d * es) : nullptr;
   P.act_s = Fs ? take((size_t)Tm * Fs * es) : nullptr;
   P.y_s = Fs ? (float*)take((size_t)Tm * d * 4) : nullptr;

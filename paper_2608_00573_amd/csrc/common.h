@@ -19,7 +19,7 @@ constexpr int kGemmBM = 128;
 constexpr int kGemmBN = 128;
 constexpr int kGemmBK = 64;
 // vocabulary rows of one exit-head tile (bf16 MFMA path / fp32 path)
-constexpr int kExitTileBF16 = 128;
+constexpr int kExitTileBF16 = 256;
 constexpr int kExitTileF32 = 16;
 // fp32 GEMM tile
 constexpr int kF32Tile = 16;
@@ -113,7 +113,9 @@ struct LayerParams {
   int4* tiles;         // [max_tiles] (expert, row begin, row end, 0)
   void* x_perm;        // [T*k, d]
   void* act_buf;       // [T*k, F]
-  float* y_buf;        // [T*k, d]
+  float* y_buf;        // [down_splits][T*k, d] partial down-projection slices
+  size_t y_split_stride;  // elements between slices of y_buf
+  int down_splits;     // K splits of the routed down GEMM (bf16 path)
   void* xs;            // [T, d]    shared-expert input rows
   void* act_s;         // [T, Fs]
   float* y_s;          // [T, d]
@@ -140,5 +142,6 @@ hipError_t launch_expert_up(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_expert_down(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_shared_expert(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st);
+int down_splits(int max_tiles, int N, int K);
 
 }  // namespace trimmoe

@@ -464,7 +464,13 @@ __global__ __launch_bounds__(256) void k_combine(LayerParams p) {
     const int n = s_n;
     for (int c = threadIdx.x; c < p.d; c += blockDim.x) {
       float acc = 0.f;
-      for (int s = 0; s < n; ++s) acc += s_w[s] * p.y_buf[(size_t)s_row[s] * p.d + c];
+      for (int s = 0; s < n; ++s) {
+        // the down projection's K-split slices, summed in slice order
+        const float* y = p.y_buf + (size_t)s_row[s] * p.d + c;
+        float v = y[0];
+        for (int q = 1; q < p.down_splits; ++q) v += y[q * p.y_split_stride];
+        acc += s_w[s] * v;
+      }
       if (p.Fs > 0) acc += p.y_s[(size_t)j * p.d + c];
       const float v = to_f32<ST>(h[(size_t)t * p.d + c]) + acc;
       const ST o = from_f32<ST>(v);
@@ -475,8 +481,9 @@ __global__ __launch_bounds__(256) void k_combine(LayerParams p) {
 }
 
 // -------------------------------------------- exit confidence and gate --
-// xi = 1 / sum_tiles s_i exp(m_i - M) (softmax max-probability from the
-// per-tile partial maxima and sums), or sigmoid of the single logit;
+// xi = 1 / sum_tiles s_i 2^(m_i - M) (softmax max-probability from the
+// per-tile partial maxima, kept in base 2, and sums), or sigmoid of the
+// single logit;
 // exit iff xi >= p_J (Eq. (8)).  One wavefront per executed token.
 __global__ __launch_bounds__(256) void k_exit_reduce(LayerParams p) {
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -488,14 +495,17 @@ __global__ __launch_bounds__(256) void k_exit_reduce(LayerParams p) {
   float m = -__builtin_inff();
   for (int u = lane; u < nv; u += 64) m = fmaxf(m, pr[u].x);
   for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+  // partial maxima are in base 2 (max z * log2 e)
   float s = 0.f;
   for (int u = lane; u < nv; u += 64) {
     const float2 v = pr[u];
-    if (v.y > 0.f) s += v.y * expf(v.x - m);
+    if (v.y > 0.f) s += v.y * exp2f(v.x - m);
   }
   for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
   if (lane == 0) {
-    const float xi = p.conf_mode == TRIMMOE_CONF_SIGMOID ? 1.f / (1.f + expf(-m)) : 1.f / s;
+    const float xi = p.conf_mode == TRIMMOE_CONF_SIGMOID
+                         ? 1.f / (1.f + exp2f(-m))  // m = logit * log2 e
+                         : 1.f / s;
     const int t = p.exec_list[j];
     const int pos = p.exec_pos[j];
     p.xi[t] = xi;

@@ -1,17 +1,27 @@
 // Matrix kernels of the adaptive-depth MoE step (gfx950):
 //   * grouped expert FFN over the executed (token, expert) rows:
 //       up/gate GEMM with the activation fused in the epilogue, output bf16
-//       (SwiGLU: silu(G) * U; ReLU: relu(U)), then the down GEMM, output fp32;
+//       (SwiGLU: silu(G) * U; ReLU: relu(U)), then the down GEMM, output fp32
+//       (optionally split along K into partial slices that the combine
+//       kernel sums in a fixed order);
 //   * exit head (Sec. III-C, Eq. (7)): logits = W_exit h for the executed
 //     tokens, reduced in the epilogue to a per-(token, vocabulary tile)
 //     (max, sum exp) pair so the logits never reach memory.
-// bf16 path: v_mfma_f32_32x32x16_bf16 with fp32 accumulation, 128x128 block
-// tiles of 4 wavefronts (64x64 each), K staged through LDS in 64-wide slices
-// with double buffering.  Both operands are K-contiguous ("NT"): A is
-// [M, K], B is [N, K] and C = A B^T.  Block ids are remapped so that each
-// XCD works on a contiguous run of tiles ordered in 8-tile-tall column
-// patches, which keeps the operand slices of concurrent blocks in that
-// XCD's L2.  fp32 path: plain FMA kernels for fp32 models.
+//
+// bf16 path.  Both operands are K-contiguous ("NT"): A is [M, K], B is
+// [N, K], C = A B^T, fp32 accumulation in v_mfma_f32_32x32x16_bf16.  A block
+// is 4 wavefronts in a 2x2 grid; K advances in 64-wide slices (one 128-byte
+// row segment per operand row).  Each thread stages its 16-byte pieces of a
+// slice in registers; two register sets and two LDS buffers keep the global
+// loads of slices kt+1 and kt+2 in flight while the MFMAs consume slice kt,
+// and the compiler only waits for the one older set it is about to store.
+// In LDS a row segment keeps its eight 16-byte chunks XOR-swizzled by
+// (row & 7), so 8 consecutive rows' 16-byte fragment reads (and the
+// 128-byte row writes) hit distinct banks.  Rows past the valid range load a
+// clamped valid row (never stored).  Block ids are remapped so that each XCD
+// works on a contiguous run of tiles taken in 8-tile-tall column patches.
+//
+// fp32 path: plain FMA kernels for fp32 models.
 #include <math.h>
 
 #include "common.h"
@@ -20,24 +30,28 @@ namespace trimmoe {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int BM = kGemmBM, BN = kGemmBN, BK = kGemmBK;
-constexpr int LDSK = BK + 8;  // padded LDS row (144 B): conflict-free b128 reads
-constexpr int kPatch = 8;     // tiles per patch column in the block order
-constexpr int kXcd = 8;       // XCDs of an MI355X; blocks are dealt round-robin
+constexpr int BK = kGemmBK;  // 64 bf16 = one 128-byte row segment
+constexpr int kPatch = 8;    // tiles per patch column in the block order
+constexpr int kXcd = 8;      // XCDs of an MI355X; blocks are dealt round-robin
 
-static_assert(BM == 128 && BN == 128 && BK == 64, "tile mapping below assumes 128x128x64");
+static_assert(BK == 64, "the LDS layout assumes 128-byte row segments");
 
 // -------------------------------------------------- block order remapping --
 // Hardware deals block b to XCD b % 8.  Give XCD x the contiguous logical
 // range [x*q + min(x, r), ...) of the `total` live tiles (a bijection on
 // [0, total)), then read the logical index in patch order: kPatch M-tiles of
-// one N-tile, then the next N-tile.
-__device__ __forceinline__ bool map_tile(int b, int total, int n_mt, int n_nt, int& mt, int& nt) {
+// one N-tile, then the next N-tile; the K split (if any) is the slowest index.
+__device__ __forceinline__ bool map_tile(int b, int n_mt, int n_nt, int n_split, int& mt, int& nt,
+                                         int& sp) {
+  const int per = n_mt * n_nt, total = per * n_split;
   if (b >= total) return false;
   const int q = total / kXcd, r = total % kXcd;
   const int x = b % kXcd, i = b / kXcd;
-  const int L = x * q + min(x, r) + i;
+  int L = x * q + min(x, r) + i;
+  sp = L / per;
+  L -= sp * per;
   const int span = kPatch * n_nt;
   const int g = L / span, w = L % span;
   const int gm = min(kPatch, n_mt - g * kPatch);
@@ -46,149 +60,191 @@ __device__ __forceinline__ bool map_tile(int b, int total, int n_mt, int n_nt, i
   return true;
 }
 
-// --------------------------------------------------------------- mainloop --
-template <bool DUAL>
-struct Smem {
-  bf16_t a[2][BM * LDSK];
-  bf16_t b0[2][BN * LDSK];
-  bf16_t b1[DUAL ? 2 : 1][DUAL ? BN * LDSK : 8];
+// ---------------------------------------------------------- pipelined core --
+// BM x BN block tile, NB B operands sharing A, GM x GN wavefronts
+template <int BM_, int BN_, int NB_, int GM_, int GN_>
+struct Tile {
+  static constexpr int BM = BM_, BN = BN_, NB = NB_, GM = GM_, GN = GN_;
+  static constexpr int THREADS = 64 * GM * GN;
+  static constexpr int WM = BM / GM, WN = BN / GN;  // wavefront tile
+  static constexpr int TM = WM / 32, TN = WN / 32;  // MFMA tiles per wavefront
+  static constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128;
+  static constexpr int STAGE = A_BYTES + NB * B_BYTES;
+  static constexpr int LDS = 2 * STAGE;
+  static constexpr int ROWS_PER_PASS = THREADS / 8;  // 8 threads per 128-byte row
+  static constexpr int A_PT = BM / ROWS_PER_PASS, B_PT = BN / ROWS_PER_PASS;
+  static_assert(WM % 32 == 0 && WN % 32 == 0, "wavefront tile");
+  static_assert(BM % ROWS_PER_PASS == 0 && BN % ROWS_PER_PASS == 0, "load passes");
+  static_assert(LDS <= 160 * 1024, "LDS");
 };
 
-// acc0 += A B0^T, acc1 += A B1^T over the full K.  A and B* point at the
-// first row of the tile; rows at or beyond a_valid / b_valid read as zero.
-template <bool DUAL>
-__device__ __forceinline__ void gload(const bf16_t* __restrict__ A, int a_valid,
-                                      const bf16_t* __restrict__ B0,
-                                      const bf16_t* __restrict__ B1, int b_valid, int K, int k0,
-                                      int lr, int lc, uint4 (&ra)[4], uint4 (&rb0)[4],
-                                      uint4 (&rb1)[4]) {
-  // Rows past the valid range load a clamped (valid) row and are zeroed by
-  // a value select, so every load is unconditional and nothing needs memory.
+template <class T>
+struct Regs {
+  u32x4_t a[T::A_PT];
+  u32x4_t b0[T::B_PT];
+  u32x4_t b1[T::NB == 2 ? T::B_PT : 1];
+};
+
+struct CoreArgs {
+  const bf16_t* A;
+  const bf16_t* B0;
+  const bf16_t* B1;
+  int a_valid, b_valid, K, k_begin, nk;
+};
+
+// thread t loads chunk t%8 of rows t/8 + i * ROWS_PER_PASS of slice kt
+template <class T>
+__device__ __forceinline__ void gload(Regs<T>& r, const CoreArgs& c, int kt) {
+  const int t = threadIdx.x;
+  const int col = c.k_begin + kt * BK + 8 * (t & 7);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = lr + 32 * i;
-    const int rowa = min(row, a_valid - 1), rowb = min(row, b_valid - 1);
-    uint4 va = *reinterpret_cast<const uint4*>(A + (size_t)rowa * K + k0 + lc);
-    uint4 vb0 = *reinterpret_cast<const uint4*>(B0 + (size_t)rowb * K + k0 + lc);
-    const bool oka = row < a_valid, okb = row < b_valid;
-    ra[i] = make_uint4(oka ? va.x : 0u, oka ? va.y : 0u, oka ? va.z : 0u, oka ? va.w : 0u);
-    rb0[i] = make_uint4(okb ? vb0.x : 0u, okb ? vb0.y : 0u, okb ? vb0.z : 0u, okb ? vb0.w : 0u);
-    if constexpr (DUAL) {
-      uint4 vb1 = *reinterpret_cast<const uint4*>(B1 + (size_t)rowb * K + k0 + lc);
-      rb1[i] = make_uint4(okb ? vb1.x : 0u, okb ? vb1.y : 0u, okb ? vb1.z : 0u, okb ? vb1.w : 0u);
-    }
+  for (int i = 0; i < T::A_PT; ++i) {
+    const int row = min((t >> 3) + T::ROWS_PER_PASS * i, c.a_valid - 1);
+    r.a[i] = *reinterpret_cast<const u32x4_t*>(c.A + (size_t)row * c.K + col);
+  }
+#pragma unroll
+  for (int i = 0; i < T::B_PT; ++i) {
+    const int row = min((t >> 3) + T::ROWS_PER_PASS * i, c.b_valid - 1);
+    r.b0[i] = *reinterpret_cast<const u32x4_t*>(c.B0 + (size_t)row * c.K + col);
+    if constexpr (T::NB == 2) r.b1[i] = *reinterpret_cast<const u32x4_t*>(c.B1 + (size_t)row * c.K + col);
   }
 }
 
-template <bool DUAL>
-__device__ __forceinline__ void sstore(Smem<DUAL>& sm, int s, int lr, int lc, const uint4 (&ra)[4],
-                                       const uint4 (&rb0)[4], const uint4 (&rb1)[4]) {
+// 16-byte chunk c of row r sits at chunk c ^ swz(r): 8 consecutive rows, or
+// 16 consecutive rows split by parity, then touch distinct bank groups.
+__device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+template <class T>
+__device__ __forceinline__ void sstore(char* sb, const Regs<T>& r) {
+  const int t = threadIdx.x;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = lr + 32 * i;
-    *reinterpret_cast<uint4*>(&sm.a[s][row * LDSK + lc]) = ra[i];
-    *reinterpret_cast<uint4*>(&sm.b0[s][row * LDSK + lc]) = rb0[i];
-    if constexpr (DUAL) *reinterpret_cast<uint4*>(&sm.b1[s][row * LDSK + lc]) = rb1[i];
+  for (int i = 0; i < T::A_PT; ++i) {
+    const int row = (t >> 3) + i * T::ROWS_PER_PASS;
+    *reinterpret_cast<u32x4_t*>(sb + row * 128 + (((t & 7) ^ swz(row)) << 4)) = r.a[i];
+  }
+#pragma unroll
+  for (int i = 0; i < T::B_PT; ++i) {
+    const int row = (t >> 3) + i * T::ROWS_PER_PASS;
+    const int off = row * 128 + (((t & 7) ^ swz(row)) << 4);
+    *reinterpret_cast<u32x4_t*>(sb + T::A_BYTES + off) = r.b0[i];
+    if constexpr (T::NB == 2) *reinterpret_cast<u32x4_t*>(sb + T::A_BYTES + T::B_BYTES + off) = r.b1[i];
   }
 }
 
-template <bool DUAL>
-__device__ __forceinline__ void mma_slice(const Smem<DUAL>& sm, int s, int wm, int wn, int fr,
-                                          int fk, f32x16_t (&acc0)[2][2],
-                                          f32x16_t (&acc1)[2][2]) {
+template <class T>
+__device__ __forceinline__ void mma_slice(const char* sb, int wm, int wn, int lane,
+                                          f32x16_t (&acc0)[T::TM][T::TN],
+                                          f32x16_t (&acc1)[T::TM][T::TN]) {
+  const int fr = lane & 31, hi = lane >> 5;
+  const int sw = swz(fr);  // fragment rows are 32-aligned offsets plus fr
 #pragma unroll
   for (int ks = 0; ks < BK / 16; ++ks) {
-    bf16x8_t af[2], bf0[2], bf1[2];
+    const int ch = ((2 * ks + hi) ^ sw) << 4;
+    bf16x8_t a[T::TM], b0[T::TN], b1[T::TN];
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
-      af[mi] = *reinterpret_cast<const bf16x8_t*>(&sm.a[s][(wm * 64 + mi * 32 + fr) * LDSK + ks * 16 + fk]);
+    for (int i = 0; i < T::TM; ++i)
+      a[i] = *reinterpret_cast<const bf16x8_t*>(sb + (wm * T::WM + i * 32 + fr) * 128 + ch);
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      bf0[ni] = *reinterpret_cast<const bf16x8_t*>(&sm.b0[s][(wn * 64 + ni * 32 + fr) * LDSK + ks * 16 + fk]);
-      if constexpr (DUAL)
-        bf1[ni] = *reinterpret_cast<const bf16x8_t*>(&sm.b1[s][(wn * 64 + ni * 32 + fr) * LDSK + ks * 16 + fk]);
+    for (int j = 0; j < T::TN; ++j) {
+      b0[j] = *reinterpret_cast<const bf16x8_t*>(sb + T::A_BYTES +
+                                                 (wn * T::WN + j * 32 + fr) * 128 + ch);
+      if constexpr (T::NB == 2)
+        b1[j] = *reinterpret_cast<const bf16x8_t*>(sb + T::A_BYTES + T::B_BYTES +
+                                                   (wn * T::WN + j * 32 + fr) * 128 + ch);
     }
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        acc0[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bf0[ni], acc0[mi][ni], 0, 0, 0);
-        if constexpr (DUAL)
-          acc1[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bf1[ni], acc1[mi][ni], 0, 0, 0);
+      for (int j = 0; j < T::TN; ++j) {
+        acc0[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b0[j], acc0[i][j], 0, 0, 0);
+        if constexpr (T::NB == 2)
+          acc1[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b1[j], acc1[i][j], 0, 0, 0);
       }
   }
 }
 
-template <bool DUAL>
-__device__ __forceinline__ void mma_mainloop(const bf16_t* __restrict__ A, int a_valid,
-                                             const bf16_t* __restrict__ B0,
-                                             const bf16_t* __restrict__ B1, int b_valid, int K,
-                                             f32x16_t (&acc0)[2][2], f32x16_t (&acc1)[2][2],
-                                             Smem<DUAL>& sm) {
-  const int tid = threadIdx.x;
-  const int lr = tid >> 3, lc = (tid & 7) * 8;  // load row / column (elements)
-  const int wave = tid >> 6, lane = tid & 63;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int fr = lane & 31, fk = (lane >> 5) * 8;  // fragment row, k offset
-  uint4 ra[4], rb0[4], rb1[4];
-  const f32x16_t zacc = {};
+// acc0 = A B0^T, acc1 = A B1^T over c.nk slices starting at column c.k_begin.
+// Slice kt is computed from LDS buffer kt % 2 while register set (kt+1) % 2
+// holds slice kt+1 and set kt % 2 receives slice kt+2.  Every refill load is
+// issued unconditionally (past the end it re-reads the last slice, unused),
+// so the compiler's load counting stays exact and each LDS store waits only
+// for its own, older register set.
+template <class T>
+__device__ __forceinline__ void gemm_core(char* lds0, char* lds1, const CoreArgs& c,
+                                          f32x16_t (&acc0)[T::TM][T::TN],
+                                          f32x16_t (&acc1)[T::TM][T::TN]) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wm = wave / T::GN, wn = wave % T::GN;
+  const f32x16_t z = {};
 #pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
+  for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      acc0[mi][ni] = zacc;
-      if constexpr (DUAL) acc1[mi][ni] = zacc;
+    for (int j = 0; j < T::TN; ++j) {
+      acc0[i][j] = z;
+      if constexpr (T::NB == 2) acc1[i][j] = z;
     }
-
-  const int nk = K / BK;
-  gload<DUAL>(A, a_valid, B0, B1, b_valid, K, 0, lr, lc, ra, rb0, rb1);
-  sstore<DUAL>(sm, 0, lr, lc, ra, rb0, rb1);
+  Regs<T> r0, r1;
+  const int nk = c.nk, last = c.nk - 1;
+  gload<T>(r0, c, 0);
+  gload<T>(r1, c, min(1, last));
+  sstore<T>(lds0, r0);
   __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
-    if (kt + 1 < nk) gload<DUAL>(A, a_valid, B0, B1, b_valid, K, (kt + 1) * BK, lr, lc, ra, rb0, rb1);
-    mma_slice<DUAL>(sm, kt & 1, wm, wn, fr, fk, acc0, acc1);
-    if (kt + 1 < nk) sstore<DUAL>(sm, (kt + 1) & 1, lr, lc, ra, rb0, rb1);
+  gload<T>(r0, c, min(2, last));
+  for (int kt = 0; kt < nk; kt += 2) {
+    mma_slice<T>(lds0, wm, wn, lane, acc0, acc1);  // slice kt
+    sstore<T>(lds1, r1);                           // slice kt + 1
     __syncthreads();
+    gload<T>(r1, c, min(kt + 3, last));
+    if (kt + 1 < nk) mma_slice<T>(lds1, wm, wn, lane, acc0, acc1);
+    sstore<T>(lds0, r0);                           // slice kt + 2
+    __syncthreads();
+    gload<T>(r0, c, min(kt + 4, last));
   }
 }
 
+#define TRIMMOE_STAGES(T)                               \
+  __shared__ __align__(16) char lds_buf0[T::STAGE];     \
+  __shared__ __align__(16) char lds_buf1[T::STAGE]
+
 // accumulator element -> tile-local (row, col)
-__device__ __forceinline__ int acc_row(int wm, int mi, int r, int lane) {
-  return wm * 64 + mi * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+template <class T>
+__device__ __forceinline__ int acc_row(int wm, int i, int r, int lane) {
+  return wm * T::WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
 }
-__device__ __forceinline__ int acc_col(int wn, int ni, int lane) { return wn * 64 + ni * 32 + (lane & 31); }
+template <class T>
+__device__ __forceinline__ int acc_col(int wn, int j, int lane) {
+  return wn * T::WN + j * 32 + (lane & 31);
+}
 
 // ------------------------------------------------------ grouped FFN GEMMs --
 // Rows come in expert groups; tile list entry = (expert, row begin, row end).
 // Dense mode (shared expert): one group, rows [0, *dense_rows).
 struct FfnArgs {
-  const bf16_t* X;          // [rows, K]
-  const bf16_t* W0;         // expert 0 of [E, N, K] (up, or down)
-  const bf16_t* W1;         // gate, same layout, or NULL
-  size_t w_stride;          // elements between experts
+  const bf16_t* X;        // [rows, K]
+  const bf16_t* W0;       // expert 0 of [E, N, K] (up, or down)
+  const bf16_t* W1;       // gate, same layout, or NULL
+  size_t w_stride;        // elements between experts
   int K, N;
-  const int4* tiles;        // grouped mode
-  const int* n_tiles;       // grouped mode: live tiles (device)
-  const int* dense_rows;    // dense mode: live rows (device), else NULL
-  void* out;                // up: bf16 [rows, N]; down: f32 [rows, N]
-  int act;                  // up: TRIMMOE_ACT_*
+  const int4* tiles;      // grouped mode
+  const int* n_tiles;     // grouped mode: live tiles (device)
+  const int* dense_rows;  // dense mode: live rows (device), else NULL
+  void* out;              // up: bf16 [rows, N]; down: f32 [split][rows_cap, N]
+  size_t split_stride;    // elements between split slices of `out`
+  int n_split;            // K splits (down GEMM); 1 otherwise
+  int act;                // up: TRIMMOE_ACT_*
 };
 
-template <bool DUAL, bool UP>
-__global__ __launch_bounds__(256) void k_ffn_mma(FfnArgs a) {
-  __shared__ Smem<DUAL> sm;
-  const int n_nt = (a.N + BN - 1) / BN;
-  int n_mt;
-  if (a.dense_rows)
-    n_mt = (*a.dense_rows + BM - 1) / BM;
-  else
-    n_mt = *a.n_tiles;
-  int mt, ntile;
-  if (!map_tile(blockIdx.x, n_mt * n_nt, n_mt, n_nt, mt, ntile)) return;
+template <class T, bool UP>
+__global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
+  TRIMMOE_STAGES(T);
+  const int n_nt = (a.N + T::BN - 1) / T::BN;
+  const int n_mt = a.dense_rows ? (*a.dense_rows + T::BM - 1) / T::BM : *a.n_tiles;
+  int mt, ntile, sp;
+  if (!map_tile(blockIdx.x, n_mt, n_nt, a.n_split, mt, ntile, sp)) return;
   int e, m0, m1;
   if (a.dense_rows) {
     e = 0;
-    m0 = mt * BM;
+    m0 = mt * T::BM;
     m1 = *a.dense_rows;
   } else {
     const int4 tl = a.tiles[mt];
@@ -196,39 +252,42 @@ __global__ __launch_bounds__(256) void k_ffn_mma(FfnArgs a) {
     m0 = tl.y;
     m1 = tl.z;
   }
-  const int n0 = ntile * BN;
-  const int a_valid = min(BM, m1 - m0);
-  const int b_valid = min(BN, a.N - n0);
+  const int n0 = ntile * T::BN;
+  const int a_valid = min(T::BM, m1 - m0);
+  const int b_valid = min(T::BN, a.N - n0);
   const bf16_t* W0 = a.W0 + (size_t)e * a.w_stride + (size_t)n0 * a.K;
-  const bf16_t* W1 = DUAL ? a.W1 + (size_t)e * a.w_stride + (size_t)n0 * a.K : nullptr;
-  f32x16_t acc0[2][2], acc1[2][2];
-  mma_mainloop<DUAL>(a.X + (size_t)m0 * a.K, a_valid, W0, W1, b_valid, a.K, acc0, acc1, sm);
+  const bf16_t* W1 = T::NB == 2 ? a.W1 + (size_t)e * a.w_stride + (size_t)n0 * a.K : nullptr;
+  const int nk = (a.K / BK) / a.n_split;
+  f32x16_t acc0[T::TM][T::TN], acc1[T::TM][T::TN];
+  gemm_core<T>(lds_buf0, lds_buf1,
+               CoreArgs{a.X + (size_t)m0 * a.K, W0, W1, a_valid, b_valid, a.K, sp * nk * BK, nk},
+               acc0, acc1);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / T::GN, wn = wave % T::GN;
 #pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
+  for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      const int col = acc_col(wn, ni, lane);
+    for (int j = 0; j < T::TN; ++j) {
+      const int col = acc_col<T>(wn, j, lane);
       if (col >= b_valid) continue;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = acc_row(wm, mi, r, lane);
+        const int row = acc_row<T>(wm, i, r, lane);
         if (row >= a_valid) continue;
         const size_t o = (size_t)(m0 + row) * a.N + n0 + col;
         if constexpr (UP) {
-          const float u = acc0[mi][ni][r];
+          const float u = acc0[i][j][r];
           float v;
-          if constexpr (DUAL) {
-            const float g = acc1[mi][ni][r];
+          if constexpr (T::NB == 2) {
+            const float g = acc1[i][j][r];
             v = g / (1.f + expf(-g)) * u;  // silu(g) * u
           } else {
             v = fmaxf(u, 0.f);
           }
           static_cast<bf16_t*>(a.out)[o] = f2bf(v);
         } else {
-          static_cast<float*>(a.out)[o] = acc0[mi][ni][r];
+          static_cast<float*>(a.out)[sp * a.split_stride + o] = acc0[i][j][r];
         }
       }
     }
@@ -237,68 +296,78 @@ __global__ __launch_bounds__(256) void k_ffn_mma(FfnArgs a) {
 // ----------------------------------------------------------- exit head --
 // M = vocabulary (A = W_exit [V, d]), N = executed tokens (B = hx [n_x, d]).
 // Epilogue: for every token column, max and sum exp over the tile's
-// vocabulary rows (bias added), written as one partial per vocabulary tile.
+// vocabulary rows (bias added), written as one partial per vocabulary tile
+// as (max z * log2 e, sum exp(z - max z)).
 struct ExitArgs {
-  const bf16_t* W;   // [V, K]
-  const bf16_t* H;   // [n_x, K]
-  const float* bias; // [V] or NULL
-  const int* n_exec; // device
+  const bf16_t* W;    // [V, K]
+  const bf16_t* H;    // [n_x, K]
+  const float* bias;  // [V] or NULL
+  const int* n_exec;  // device
   int V, K, n_vtiles;
-  float2* partials;  // [n_x, n_vtiles]
+  float2* partials;   // [n_x, n_vtiles]
 };
 
-__global__ __launch_bounds__(256) void k_exit_mma(ExitArgs a) {
-  __shared__ Smem<false> sm;
-  __shared__ float2 s_part[2][BN];  // per wm half: (max, sum) per token column
+using ExitTile = Tile<kExitTileBF16, 128, 1, 4, 2>;
+
+__global__ __launch_bounds__(ExitTile::THREADS) void k_exit_mma(ExitArgs a) {
+  using T = ExitTile;
+  TRIMMOE_STAGES(T);
+  __shared__ float2 s_part[T::GM][T::BN];  // per wavefront row: (max, sum) per token column
   const int n_x = *a.n_exec;
-  const int n_mt = a.n_vtiles, n_nt = (n_x + BN - 1) / BN;
-  int mt, nt;
-  if (!map_tile(blockIdx.x, n_mt * n_nt, n_mt, n_nt, mt, nt)) return;
-  const int v0 = mt * BM, j0 = nt * BN;
-  const int a_valid = min(BM, a.V - v0);
-  const int b_valid = min(BN, n_x - j0);
-  f32x16_t acc0[2][2], acc1[2][2];
-  mma_mainloop<false>(a.W + (size_t)v0 * a.K, a_valid, a.H + (size_t)j0 * a.K, nullptr, b_valid,
-                      a.K, acc0, acc1, sm);
+  const int n_mt = a.n_vtiles, n_nt = (n_x + T::BN - 1) / T::BN;
+  int mt, nt, sp;
+  if (!map_tile(blockIdx.x, n_mt, n_nt, 1, mt, nt, sp)) return;
+  const int v0 = mt * T::BM, j0 = nt * T::BN;
+  const int a_valid = min(T::BM, a.V - v0);
+  const int b_valid = min(T::BN, n_x - j0);
+  f32x16_t acc0[T::TM][T::TN], acc1[T::TM][T::TN];
+  gemm_core<T>(lds_buf0, lds_buf1,
+               CoreArgs{a.W + (size_t)v0 * a.K, a.H + (size_t)j0 * a.K, nullptr, a_valid, b_valid,
+                        a.K, 0, a.K / BK},
+               acc0, acc1);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / T::GN, wn = wave % T::GN;
+  // partials in base 2: y = z * log2(e), so exp(z - max z) = exp2(y - max y)
+  // is one FMA and one v_exp_f32 per logit; the pair stored is (max y, sum)
   const float ninf = -__builtin_inff();
+  const float kLog2e = 1.4426950408889634f;
 #pragma unroll
-  for (int ni = 0; ni < 2; ++ni) {
+  for (int j = 0; j < T::TN; ++j) {
     float m = ninf;
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int i = 0; i < T::TM; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = acc_row(wm, mi, r, lane);
-        float x = acc0[mi][ni][r];
-        if (row < a_valid) {
-          if (a.bias) x += a.bias[v0 + row];
-        } else {
-          x = ninf;
-        }
-        acc0[mi][ni][r] = x;
-        m = fmaxf(m, x);
+        const int row = acc_row<T>(wm, i, r, lane);
+        float y = acc0[i][j][r];
+        if (a.bias) y += a.bias[v0 + min(row, a_valid - 1)];
+        y = row < a_valid ? y * kLog2e : ninf;
+        acc0[i][j][r] = y;
+        m = fmaxf(m, y);
       }
     m = fmaxf(m, __shfl_xor(m, 32));
     float s = 0.f;
     if (m != ninf) {
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
+      for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s += expf(acc0[mi][ni][r] - m);
+        for (int r = 0; r < 16; ++r) s += __builtin_amdgcn_exp2f(acc0[i][j][r] - m);
     }
     s += __shfl_xor(s, 32);
-    if (lane < 32) s_part[wm][acc_col(wn, ni, lane)] = make_float2(m, s);
+    if (lane < 32) s_part[wm][acc_col<T>(wn, j, lane)] = make_float2(m, s);
   }
   __syncthreads();
   const int c = threadIdx.x;
   if (c < b_valid) {
-    const float2 p0 = s_part[0][c], p1 = s_part[1][c];
-    const float M = fmaxf(p0.x, p1.x);
+    float M = s_part[0][c].x;
+#pragma unroll
+    for (int g = 1; g < T::GM; ++g) M = fmaxf(M, s_part[g][c].x);
     float S = 0.f;
-    if (p0.y > 0.f) S += p0.y * expf(p0.x - M);
-    if (p1.y > 0.f) S += p1.y * expf(p1.x - M);
+#pragma unroll
+    for (int g = 0; g < T::GM; ++g) {
+      const float2 q = s_part[g][c];
+      if (q.y > 0.f) S += q.y * __builtin_amdgcn_exp2f(q.x - M);
+    }
     a.partials[(size_t)(j0 + c) * a.n_vtiles + mt] = make_float2(M, S);
   }
 }
@@ -313,13 +382,13 @@ __global__ __launch_bounds__(256) void k_ffn_f32(const float* X, const float* W0
                                                  const int* n_tiles, const int* dense_rows,
                                                  void* out, int act) {
   const int n_nt = (N + FT - 1) / FT;
-  const int n_mt = dense_rows ? (*dense_rows + BM - 1) / BM : *n_tiles;
+  const int n_mt = dense_rows ? (*dense_rows + kGemmBM - 1) / kGemmBM : *n_tiles;
   const int mt = blockIdx.x / n_nt, ntile = blockIdx.x % n_nt;
   if (mt >= n_mt) return;
   int e, m0, m1;
   if (dense_rows) {
     e = 0;
-    m0 = mt * BM;
+    m0 = mt * kGemmBM;
     m1 = *dense_rows;
   } else {
     const int4 tl = tiles[mt];
@@ -332,7 +401,7 @@ __global__ __launch_bounds__(256) void k_ffn_f32(const float* X, const float* W0
   if (n >= N) return;
   const float* w0 = W0 + (size_t)e * w_stride + (size_t)n * K;
   const float* w1 = W1 ? W1 + (size_t)e * w_stride + (size_t)n * K : nullptr;
-  for (int m = m0 + ty; m < min(m0 + BM, m1); m += 256 / FT) {
+  for (int m = m0 + ty; m < min(m0 + kGemmBM, m1); m += 256 / FT) {
     const float* x = X + (size_t)m * K;
     float u = 0.f, g = 0.f;
     for (int j = 0; j < K; ++j) {
@@ -376,13 +445,35 @@ __global__ __launch_bounds__(256) void k_exit_f32(const float* W, const float* H
       float s = 0.f;
       if (m != -__builtin_inff())
         for (int u = 0; u < FT; ++u) s += expf(s_z[u][threadIdx.x] - m);
-      partials[(size_t)jj * n_vtiles + vt] = make_float2(m, s);
+      // partials are kept in base 2: (max z * log2 e, sum exp(z - max z))
+      partials[(size_t)jj * n_vtiles + vt] = make_float2(m * 1.4426950408889634f, s);
     }
   }
 }
 
 // ------------------------------------------------------------- launchers --
 static inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+// Tile shapes of the expert GEMMs (BM rows of an expert group x BN outputs)
+using UpDualTile = Tile<kGemmBM, 128, 2, 2, 4>;  // SwiGLU: up and gate share A
+using UpTile = Tile<kGemmBM, 256, 1, 2, 4>;      // ReLU
+using DownTile = Tile<kGemmBM, 128, 1, 2, 2>;
+
+// K splits of the routed down GEMM: enough blocks to cover the CUs twice,
+// each split keeping at least 8 K slices.
+int down_splits(int max_tiles, int N, int K) {
+  const int tiles = max_tiles * cdiv(N, DownTile::BN);
+  const int nk = K / BK;
+  int s = 1;
+  while (s < 4 && tiles * s < 512 && nk % (2 * s) == 0 && nk / (2 * s) >= 8) s *= 2;
+  return s;
+}
+
+template <class T, bool UP>
+static void launch_ffn_mma(const FfnArgs& a, int max_mt, hipStream_t st) {
+  const dim3 grid(max_mt * cdiv(a.N, T::BN) * a.n_split);
+  hipLaunchKernelGGL((k_ffn_mma<T, UP>), grid, dim3(T::THREADS), 0, st, a);
+}
 
 static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared, hipStream_t st) {
   const int K = up ? p.d : (shared ? p.Fs : p.F);
@@ -394,20 +485,20 @@ static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared
   const void* X = up ? (shared ? p.xs : p.x_perm) : (shared ? p.act_s : p.act_buf);
   void* out = up ? (shared ? p.act_s : p.act_buf) : (shared ? (void*)p.y_s : (void*)p.y_buf);
   const int* dense = shared ? &p.counts[kCntExec] : nullptr;
-  const int max_mt = shared ? cdiv(p.T, BM) : p.max_tiles;
+  const int max_mt = shared ? cdiv(p.T, kGemmBM) : p.max_tiles;
   const int act = shared ? TRIMMOE_ACT_SWIGLU : p.act;
   if (max_mt <= 0) return hipSuccess;
   if (bf16) {
+    const int n_split = (!up && !shared) ? p.down_splits : 1;
     FfnArgs a{static_cast<const bf16_t*>(X), static_cast<const bf16_t*>(w0),
               static_cast<const bf16_t*>(w1), w_stride, K, N, p.tiles, &p.counts[kCntTiles],
-              dense, out, act};
-    const dim3 grid(max_mt * cdiv(N, BN));
+              dense, out, p.y_split_stride, n_split, act};
     if (up && dual)
-      hipLaunchKernelGGL((k_ffn_mma<true, true>), grid, dim3(256), 0, st, a);
+      launch_ffn_mma<UpDualTile, true>(a, max_mt, st);
     else if (up)
-      hipLaunchKernelGGL((k_ffn_mma<false, true>), grid, dim3(256), 0, st, a);
+      launch_ffn_mma<UpTile, true>(a, max_mt, st);
     else
-      hipLaunchKernelGGL((k_ffn_mma<false, false>), grid, dim3(256), 0, st, a);
+      launch_ffn_mma<DownTile, false>(a, max_mt, st);
   } else {
     const dim3 grid(max_mt * cdiv(N, FT));
     if (up)
@@ -441,8 +532,8 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
   if (bf16) {
     ExitArgs a{static_cast<const bf16_t*>(p.w_exit), static_cast<const bf16_t*>(p.hx), p.b_exit,
                &p.counts[kCntExec], p.V, p.d, p.n_vtiles, p.partials};
-    const dim3 grid(p.n_vtiles * cdiv(p.T, BN));
-    hipLaunchKernelGGL(k_exit_mma, grid, dim3(256), 0, st, a);
+    const dim3 grid(p.n_vtiles * cdiv(p.T, ExitTile::BN));
+    hipLaunchKernelGGL(k_exit_mma, grid, dim3(ExitTile::THREADS), 0, st, a);
   } else {
     const dim3 grid(p.n_vtiles * cdiv(p.T, FT));
     hipLaunchKernelGGL(k_exit_f32, grid, dim3(256), 0, st, static_cast<const float*>(p.w_exit),
