@@ -105,7 +105,7 @@ typedef struct trimmoe_layer {
 
 typedef struct trimmoe_model {
   int32_t n_layers;       /* N                                                  */
-  int32_t d_model;        /* d; bf16: multiple of 64, f32: multiple of 4        */
+  int32_t d_model;        /* d; bf16: multiple of 64, f32: multiple of 8        */
   int32_t n_experts;      /* E, 1..256                                          */
   int32_t top_k;          /* k, 1..min(8, E)                                    */
   int32_t d_ff;           /* F; bf16: multiple of 64                            */

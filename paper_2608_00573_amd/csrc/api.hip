@@ -6,8 +6,9 @@
 // the worst case (every kernel reads the live counts from device memory
 // and retires early, so the host never waits on the device):
 //   [trace fill] -> substitution table -> route+decide -> offsets/tiles ->
-//   permute -> up/gate GEMM -> down GEMM (-> shared expert) -> combine ->
-//   (not the last layer) exit GEMM -> exit gate -> compaction.
+//   row bucketing -> up/gate GEMM (gathers h rows) -> down GEMM (-> shared
+//   expert) -> combine (updates h) -> (not the last layer) exit GEMM
+//   (gathers the executed tokens' h rows) -> exit gate -> compaction.
 #include <math.h>
 #include <string.h>
 
@@ -36,7 +37,7 @@ int validate_model(const trimmoe_model* m) {
   if (m->dtype == TRIMMOE_BF16) {
     if (m->d_model % 64 || m->d_ff % 64 || m->d_ff_shared % 64) return TRIMMOE_ERR_SHAPE;
   } else {
-    if (m->d_model % 4) return TRIMMOE_ERR_SHAPE;
+    if (m->d_model % 8) return TRIMMOE_ERR_SHAPE;
   }
   const bool swiglu = m->act == TRIMMOE_ACT_SWIGLU;
   for (int l = 0; l < m->n_layers; ++l) {
@@ -112,13 +113,12 @@ size_t carve(const trimmoe_model* m, int T, char* base, LayerParams* p) {
   P.exp_off = (int32_t*)take((size_t)(E + 1) * 4);
   P.counts = (int32_t*)take(kCntSlots * 4);
   P.tiles = (int4*)take((size_t)max_tiles * 16);
-  P.x_perm = take(R * d * es);
+  P.row_src = (int32_t*)take(R * 4);
   P.act_buf = take(R * F * es);
   const int splits = bf16 ? down_splits(max_tiles, d, F) : 1;
   P.y_buf = (float*)take((size_t)splits * R * d * 4);
   P.y_split_stride = R * d;
   P.down_splits = splits;
-  P.xs = Fs ? take((size_t)Tm * d * es) : nullptr;
   P.act_s = Fs ? take((size_t)Tm * Fs * es) : nullptr;
   P.y_s = Fs ? (float*)take((size_t)Tm * d * 4) : nullptr;
   P.hx = take((size_t)Tm * d * es);
@@ -205,6 +205,12 @@ int run_layer(const trimmoe_model* m, int l, const trimmoe_policy* pol, const tr
   memset(&P, 0, sizeof(P));
   carve(m, s->n_tokens, static_cast<char*>(ws), &P);
   fill_params(P, m, l, pol, s, tr);
+  int dev = 0, ncu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      ncu <= 0)
+    return TRIMMOE_ERR_HIP;
+  P.n_cu = ncu;
   const bool bf16 = m->dtype == TRIMMOE_BF16;
   const bool last = l == m->n_layers - 1;
 #define TRIMMOE_TRY(x) \
@@ -217,7 +223,7 @@ int run_layer(const trimmoe_model* m, int l, const trimmoe_policy* pol, const tr
   TRIMMOE_TRY(launch_route(P, bf16, st));
   TRIMMOE_MARK(TRIMMOE_CLASS_ROUTE + 1);
   TRIMMOE_TRY(launch_scan(P, st));
-  TRIMMOE_TRY(launch_permute(P, bf16, st));
+  TRIMMOE_TRY(launch_bucket(P, st));
   TRIMMOE_MARK(TRIMMOE_CLASS_BUCKET + 1);
   TRIMMOE_TRY(launch_expert_up(P, bf16, st));
   TRIMMOE_MARK(TRIMMOE_CLASS_UP + 1);

@@ -111,18 +111,18 @@ struct LayerParams {
   int32_t* exp_off;    // [E+1]
   int32_t* counts;     // [kCntSlots]
   int4* tiles;         // [max_tiles] (expert, row begin, row end, 0)
-  void* x_perm;        // [T*k, d]
+  int32_t* row_src;    // [T*k] token whose h row feeds each permuted row
   void* act_buf;       // [T*k, F]
   float* y_buf;        // [down_splits][T*k, d] partial down-projection slices
   size_t y_split_stride;  // elements between slices of y_buf
   int down_splits;     // K splits of the routed down GEMM (bf16 path)
-  void* xs;            // [T, d]    shared-expert input rows
   void* act_s;         // [T, Fs]
   float* y_s;          // [T, d]
-  void* hx;            // [T, d]    updated rows of executed tokens
+  void* hx;            // [T, d]    updated rows of executed tokens (exit input)
   float2* partials;    // [T, n_vtiles] (max, sum exp) per vocabulary tile
   int n_vtiles;
   int max_tiles;
+  int n_cu;            // compute units of the device (persistent grids)
 };
 
 // launchers (decide.hip)
@@ -132,7 +132,7 @@ hipError_t launch_trace_fill(const LayerParams& p, hipStream_t st);
 hipError_t launch_subst(const LayerParams& p, hipStream_t st);
 hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_scan(const LayerParams& p, hipStream_t st);
-hipError_t launch_permute(const LayerParams& p, bool bf16, hipStream_t st);
+hipError_t launch_bucket(const LayerParams& p, hipStream_t st);
 hipError_t launch_combine(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_exit_reduce(const LayerParams& p, hipStream_t st);
 hipError_t launch_compact(const LayerParams& p, hipStream_t st);

@@ -91,7 +91,7 @@ __global__ void k_subst(LayerParams p) {
 // the decision.  Phase 3: per-block expert histogram for the bucketing.
 template <bool BF16>
 __global__ __launch_bounds__(256) void k_route(LayerParams p) {
-  extern __shared__ float zs[];  // [RB][E]
+  extern __shared__ float zs[];  // [RB][E] logits (+ [RB][E] second K half)
   __shared__ int s_cnt[TRIMMOE_MAX_EXPERTS];
   __shared__ int s_xcnt;
   __shared__ int sS[RB][KMAX];
@@ -110,33 +110,53 @@ __global__ __launch_bounds__(256) void k_route(LayerParams p) {
   if (threadIdx.x == 0) s_xcnt = 0;
 
   if constexpr (BF16) {
+    // logits of RB tokens x E experts as 16x16 MFMA tiles (2 token tiles x
+    // ceil(E/16) expert tiles); with fewer tiles than wavefronts the K range
+    // is split in two and the halves are added in a fixed order.  Rows past
+    // the live tokens / experts load a clamped valid row (never stored).
     const bf16_t* h = static_cast<const bf16_t*>(p.h);
     const bf16_t* W = static_cast<const bf16_t*>(p.w_router);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int nct = (E + 15) >> 4;
-    for (int tile = wave; tile < 2 * nct; tile += 4) {
+    const int nct = (E + 15) >> 4, ntile = 2 * nct;
+    const int ks = ntile >= 4 ? 1 : 2;
+    const int dk = d / ks;
+    float* part = zs + RB * E;
+    for (int w = wave; w < ntile * ks; w += 4) {
+      const int tile = w % ntile, kh = w / ntile;
       const int rt = tile & 1, ct = tile >> 1;
       const int tl = rt * 16 + (lane & 15);
-      const bool tv = tl < nt;
-      const int t = tv ? p.active_idx[base + tl] : 0;
+      const int t = p.active_idx[base + min(tl, nt - 1)];
       const int e = ct * 16 + (lane & 15);
-      const bool ev = e < E;
-      const bf16_t* hr = h + (size_t)t * d + 8 * (lane >> 4);
-      const bf16_t* wr = W + (size_t)(ev ? e : 0) * d + 8 * (lane >> 4);
+      const bf16_t* hr = h + (size_t)t * d + kh * dk + 8 * (lane >> 4);
+      const bf16_t* wr = W + (size_t)min(e, E - 1) * d + kh * dk + 8 * (lane >> 4);
       f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-      for (int k0 = 0; k0 < d; k0 += 32) {
-        uint4 av = tv ? *reinterpret_cast<const uint4*>(hr + k0) : make_uint4(0, 0, 0, 0);
-        uint4 bv = ev ? *reinterpret_cast<const uint4*>(wr + k0) : make_uint4(0, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
-                                                      __builtin_bit_cast(bf16x8_t, bv),
-                                                      acc, 0, 0, 0);
+      int k0 = 0;
+      for (; k0 + 128 <= dk; k0 += 128) {
+        bf16x8_t av[4], bv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          av[u] = *reinterpret_cast<const bf16x8_t*>(hr + k0 + 32 * u);
+          bv[u] = *reinterpret_cast<const bf16x8_t*>(wr + k0 + 32 * u);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u], bv[u], acc, 0, 0, 0);
       }
+      for (; k0 < dk; k0 += 32)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8_t*>(hr + k0),
+                                                      *reinterpret_cast<const bf16x8_t*>(wr + k0),
+                                                      acc, 0, 0, 0);
       // accumulator: column = lane % 16 (expert), row = 4 * (lane / 16) + r (token)
+      float* dst = kh == 0 ? zs : part;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = rt * 16 + 4 * (lane >> 4) + r;
-        if (row < nt && ev) zs[row * E + e] = acc[r];
+        if (row < nt && e < E) dst[row * E + e] = acc[r];
       }
+    }
+    if (ks == 2) {
+      __syncthreads();
+      for (int idx = threadIdx.x; idx < nt * E; idx += blockDim.x) zs[idx] = zs[idx] + part[idx];
     }
   } else {
     const float* h = static_cast<const float*>(p.h);
@@ -305,70 +325,120 @@ __global__ __launch_bounds__(256) void k_route(LayerParams p) {
 }
 
 // ------------------------------------------- expert offsets and tile list --
-__global__ __launch_bounds__(256) void k_scan(LayerParams p) {
+// Exclusive scan of a value per thread over a 1024-thread block (wavefront
+// prefix with shuffles, then the 16 wavefront totals); returns the block
+// total in *total.
+__device__ __forceinline__ int block_exclusive_scan(int v, int* s_wave, int* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) s_wave[wave] = x;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int run = 0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) {
+      const int c = s_wave[w];
+      s_wave[w] = run;
+      run += c;
+    }
+    s_wave[16] = run;
+  }
+  __syncthreads();
+  const int r = s_wave[wave] + x - v;
+  *total = s_wave[16];
+  __syncthreads();
+  return r;
+}
+
+// Per-expert offsets of every route block's rows, expert row offsets, the
+// grouped-GEMM tile list and the executed-token offsets, in one block of
+// 1024 threads: thread (segment g, expert e) sums its run of route blocks,
+// the segments of an expert are scanned in order, and the expert totals
+// and block exec counts go through block-wide scans.
+__global__ __launch_bounds__(1024) void k_scan(LayerParams p) {
+  __shared__ int s_seg[1024];
+  __shared__ int s_wave[17];
   __shared__ int s_tot[TRIMMOE_MAX_EXPERTS];
-  __shared__ int s_off[TRIMMOE_MAX_EXPERTS + 1];
-  __shared__ int s_toff[TRIMMOE_MAX_EXPERTS + 1];
+  __shared__ int s_off[TRIMMOE_MAX_EXPERTS];
+  __shared__ int s_toff[TRIMMOE_MAX_EXPERTS];
   const int n_a = *p.n_active;
   const int nb = (n_a + RB - 1) / RB;
   const int E = p.E;
-  const int e = threadIdx.x;
+  int ep = 1;
+  while (ep < E) ep <<= 1;
+  const int S = 1024 / ep;               // segments per expert
+  const int L = (nb + S - 1) / S;        // route blocks per segment
+  const int e = threadIdx.x % ep, g = threadIdx.x / ep;
+  const int b0 = g * L, b1 = min(nb, b0 + L);
+  int sum = 0;
+  if (e < E)
+    for (int b = b0; b < b1; ++b) sum += p.blk_cnt[(size_t)b * E + e];
+  s_seg[g * ep + e] = sum;
+  __syncthreads();
   if (e < E) {
     int run = 0;
-    for (int b = 0; b < nb; ++b) {
+    for (int q = 0; q < g; ++q) run += s_seg[q * ep + e];
+    for (int b = b0; b < b1; ++b) {
       const int c = p.blk_cnt[(size_t)b * E + e];
       p.blk_off[(size_t)b * E + e] = run;
       run += c;
     }
-    s_tot[e] = run;
+    if (g == S - 1) s_tot[e] = run;
   }
   __syncthreads();
+  // expert row offsets and tile offsets (threads 0..E-1 carry one expert)
+  int total = 0, ttotal = 0;
+  const int tot = threadIdx.x < E ? s_tot[threadIdx.x] : 0;
+  const int off = block_exclusive_scan(tot, s_wave, &total);
+  const int nt_e = (tot + kGemmBM - 1) / kGemmBM;
+  const int toff = block_exclusive_scan(nt_e, s_wave, &ttotal);
+  if (threadIdx.x < E) {
+    s_off[threadIdx.x] = off;
+    s_toff[threadIdx.x] = toff;
+    p.exp_off[threadIdx.x] = off;
+    for (int u = 0; u < nt_e; ++u)
+      p.tiles[toff + u] = make_int4(threadIdx.x, off + u * kGemmBM, off + tot, 0);
+  }
+  // executed-token offsets of the route blocks
+  int xrun = 0;
+  for (int c0 = 0; c0 < nb; c0 += 1024) {
+    const int b = c0 + threadIdx.x;
+    const int v = b < nb ? p.blk_xcnt[b] : 0;
+    int chunk = 0;
+    const int o = block_exclusive_scan(v, s_wave, &chunk);
+    if (b < nb) p.blk_xoff[b] = xrun + o;
+    xrun += chunk;
+  }
   if (threadIdx.x == 0) {
-    int off = 0, toff = 0, distinct = 0;
+    p.exp_off[E] = total;
+    p.counts[kCntRows] = total;
+    int nt_all = 0, distinct = 0;
     for (int x = 0; x < E; ++x) {
-      s_off[x] = off;
-      s_toff[x] = toff;
-      off += s_tot[x];
-      toff += (s_tot[x] + kGemmBM - 1) / kGemmBM;
+      nt_all += (s_tot[x] + kGemmBM - 1) / kGemmBM;
       distinct += s_tot[x] > 0;
     }
-    s_off[E] = off;
-    s_toff[E] = toff;
-    int xo = 0;
-    for (int b = 0; b < nb; ++b) {
-      p.blk_xoff[b] = xo;
-      xo += p.blk_xcnt[b];
-    }
-    p.counts[kCntRows] = off;
-    p.counts[kCntTiles] = toff;
-    p.counts[kCntExec] = xo;
-    p.exp_off[E] = off;
+    p.counts[kCntTiles] = nt_all;
+    p.counts[kCntExec] = xrun;
     if (p.tr_counters) {
-      p.tr_counters[6] = off;
+      p.tr_counters[6] = total;
       p.tr_counters[7] = distinct;
     }
-  }
-  __syncthreads();
-  if (e < E) {
-    p.exp_off[e] = s_off[e];
-    const int n = s_toff[e + 1] - s_toff[e];
-    for (int u = 0; u < n; ++u)
-      p.tiles[s_toff[e] + u] = make_int4(e, s_off[e] + u * kGemmBM, s_off[e] + s_tot[e], 0);
   }
 }
 
 // ------------------------------------------------- stable row permutation --
 // Row of (active position pos, merged row j with expert e) =
 //   exp_off[e] + (rows of e in earlier blocks) + (rows of e earlier in block),
-// i.e. rows of one expert stay in token order.  Copies h rows into x_perm
-// (and into xs for the shared expert) with 16-byte vectors.
-template <typename ST>
-__global__ __launch_bounds__(256) void k_permute(LayerParams p) {
+// i.e. rows of one expert stay in token order.  No hidden state is copied:
+// row_src[row] names the token whose h row the grouped GEMM gathers, and
+// exec_list / exec_pos list the executed tokens in active order.
+__global__ __launch_bounds__(256) void k_bucket(LayerParams p) {
   __shared__ int s_exec[RB * KMAX];
-  __shared__ int s_row[RB * KMAX];
-  __shared__ int s_tok[RB];
   __shared__ int s_act[RB];
-  __shared__ int s_xidx[RB];
   const int n_a = *p.n_active;
   const int base = blockIdx.x * RB;
   if (base >= n_a) return;
@@ -377,105 +447,83 @@ __global__ __launch_bounds__(256) void k_permute(LayerParams p) {
   const int i = threadIdx.x;
   if (i < nt) {
     const int pos = base + i;
-    s_tok[i] = p.active_idx[pos];
     s_act[i] = p.tok_action[pos];
     for (int j = 0; j < k; ++j) s_exec[i * k + j] = p.tok_exec[(size_t)pos * k + j];
   }
   __syncthreads();
   if (i < nt) {
     const int pos = base + i;
+    const int t = p.active_idx[pos];
     for (int j = 0; j < k; ++j) {
       const int e = s_exec[i * k + j];
-      if (e < 0) {
-        s_row[i * k + j] = -1;
-        continue;
-      }
+      if (e < 0) break;
       int rank = 0;
       for (int i2 = 0; i2 < i; ++i2)
         for (int j2 = 0; j2 < k; ++j2) rank += (s_exec[i2 * k + j2] == e);
       const int row = p.exp_off[e] + p.blk_off[(size_t)blockIdx.x * E + e] + rank;
-      s_row[i * k + j] = row;
       p.tok_row[(size_t)pos * k + j] = row;
+      p.row_src[row] = t;
     }
     if (s_act[i] == TRIMMOE_ACT_EXEC) {
       int xr = 0;
       for (int i2 = 0; i2 < i; ++i2) xr += (s_act[i2] == TRIMMOE_ACT_EXEC);
       const int xidx = p.blk_xoff[blockIdx.x] + xr;
-      p.exec_list[xidx] = s_tok[i];
+      p.exec_list[xidx] = t;
       p.exec_pos[xidx] = pos;
-      s_xidx[i] = xidx;
-    } else {
-      s_xidx[i] = -1;
-    }
-  }
-  __syncthreads();
-  const ST* h = static_cast<const ST*>(p.h);
-  ST* xp = static_cast<ST*>(p.x_perm);
-  const int vec = 16 / sizeof(ST);
-  const int nchunk = p.d / vec;
-  for (int idx = threadIdx.x; idx < nt * k * nchunk; idx += blockDim.x) {
-    const int q = idx / nchunk, c = idx % nchunk;
-    const int row = s_row[q];
-    if (row < 0) continue;
-    const int t = s_tok[q / k];
-    reinterpret_cast<uint4*>(xp + (size_t)row * p.d)[c] =
-        reinterpret_cast<const uint4*>(h + (size_t)t * p.d)[c];
-  }
-  if (p.Fs > 0) {
-    ST* xs = static_cast<ST*>(p.xs);
-    for (int idx = threadIdx.x; idx < nt * nchunk; idx += blockDim.x) {
-      const int q = idx / nchunk, c = idx % nchunk;
-      const int xidx = s_xidx[q];
-      if (xidx < 0) continue;
-      reinterpret_cast<uint4*>(xs + (size_t)xidx * p.d)[c] =
-          reinterpret_cast<const uint4*>(h + (size_t)s_tok[q] * p.d)[c];
     }
   }
 }
 
 // ------------------------------------------------ weighted combine (R4) --
 // h[t] <- round(h[t] + sum_rows w * Y[row] (+ shared Y)), summed in rank
-// order in fp32 and rounded once; the new row is also written to hx (the
-// exit head's input).  Skipped and inactive tokens are untouched.
+// order in fp32 (each row's K-split slices first, in slice order) and
+// rounded once; the new row also goes to hx, the exit head's compact input.
+// One thread handles 8 consecutive features of one token.  Skipped and
+// inactive tokens are untouched.
 template <typename ST>
 __global__ __launch_bounds__(256) void k_combine(LayerParams p) {
-  __shared__ int s_row[KMAX];
-  __shared__ float s_w[KMAX];
-  __shared__ int s_n;
   const int n_x = p.counts[kCntExec];
+  const int per_tok = p.d / 8;
+  const size_t total = (size_t)n_x * per_tok;
   ST* h = static_cast<ST*>(p.h);
-  ST* hx = static_cast<ST*>(p.hx);
-  for (int j = blockIdx.x; j < n_x; j += gridDim.x) {
+  for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+       idx += (size_t)gridDim.x * blockDim.x) {
+    const int j = (int)(idx / per_tok), c = (int)(idx % per_tok) * 8;
     const int pos = p.exec_pos[j];
     const int t = p.exec_list[j];
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      int n = 0;
-      for (int s = 0; s < p.k; ++s) {
-        const int e = p.tok_exec[(size_t)pos * p.k + s];
-        if (e < 0) break;
-        s_row[n] = p.tok_row[(size_t)pos * p.k + s];
-        s_w[n] = p.tok_w[(size_t)pos * p.k + s];
-        ++n;
+    float acc[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc[u] = 0.f;
+    for (int s = 0; s < p.k; ++s) {
+      const int e = p.tok_exec[(size_t)pos * p.k + s];
+      if (e < 0) break;
+      const int row = p.tok_row[(size_t)pos * p.k + s];
+      const float w = p.tok_w[(size_t)pos * p.k + s];
+      const float4* y = reinterpret_cast<const float4*>(p.y_buf + (size_t)row * p.d + c);
+      float4 v0 = y[0], v1 = y[1];
+      for (int q = 1; q < p.down_splits; ++q) {
+        const float4* yq = reinterpret_cast<const float4*>(p.y_buf + q * p.y_split_stride +
+                                                           (size_t)row * p.d + c);
+        const float4 a0 = yq[0], a1 = yq[1];
+        v0.x += a0.x; v0.y += a0.y; v0.z += a0.z; v0.w += a0.w;
+        v1.x += a1.x; v1.y += a1.y; v1.z += a1.z; v1.w += a1.w;
       }
-      s_n = n;
+      acc[0] += w * v0.x; acc[1] += w * v0.y; acc[2] += w * v0.z; acc[3] += w * v0.w;
+      acc[4] += w * v1.x; acc[5] += w * v1.y; acc[6] += w * v1.z; acc[7] += w * v1.w;
     }
-    __syncthreads();
-    const int n = s_n;
-    for (int c = threadIdx.x; c < p.d; c += blockDim.x) {
-      float acc = 0.f;
-      for (int s = 0; s < n; ++s) {
-        // the down projection's K-split slices, summed in slice order
-        const float* y = p.y_buf + (size_t)s_row[s] * p.d + c;
-        float v = y[0];
-        for (int q = 1; q < p.down_splits; ++q) v += y[q * p.y_split_stride];
-        acc += s_w[s] * v;
-      }
-      if (p.Fs > 0) acc += p.y_s[(size_t)j * p.d + c];
-      const float v = to_f32<ST>(h[(size_t)t * p.d + c]) + acc;
-      const ST o = from_f32<ST>(v);
-      h[(size_t)t * p.d + c] = o;
-      hx[(size_t)j * p.d + c] = o;
+    if (p.Fs > 0) {
+      const float4* ys = reinterpret_cast<const float4*>(p.y_s + (size_t)j * p.d + c);
+      const float4 a0 = ys[0], a1 = ys[1];
+      acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
+      acc[4] += a1.x; acc[5] += a1.y; acc[6] += a1.z; acc[7] += a1.w;
+    }
+    ST* hr = h + (size_t)t * p.d + c;
+    ST* xr = static_cast<ST*>(p.hx) + (size_t)j * p.d + c;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const ST o = from_f32<ST>(to_f32<ST>(hr[u]) + acc[u]);
+      hr[u] = o;
+      xr[u] = o;
     }
   }
 }
@@ -521,28 +569,33 @@ __global__ __launch_bounds__(256) void k_exit_reduce(LayerParams p) {
 // ------------------------------------- stable compaction of active list --
 // In place, one block, chunk by chunk: every write of a chunk lands before
 // the chunk's own start, and all its reads finish before the first write.
+// Positions come from a wavefront ballot/popcount plus the scanned
+// wavefront totals.
 __global__ __launch_bounds__(1024) void k_compact(LayerParams p) {
-  __shared__ int s_scan[1024];
-  __shared__ int s_total;
+  __shared__ int s_wave[17];
   const int n_a = *p.n_active;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int out = 0;
   for (int c0 = 0; c0 < n_a; c0 += 1024) {
     const int i = c0 + threadIdx.x;
-    const int keep = i < n_a ? p.tok_keep[i] : 0;
+    const bool keep = i < n_a && p.tok_keep[i];
     const int idx = i < n_a ? p.active_idx[i] : 0;
-    s_scan[threadIdx.x] = keep;
+    const unsigned long long m = __ballot(keep);
+    const int before = __popcll(m & ((1ull << lane) - 1ull));
+    if (lane == 0) s_wave[wave] = __popcll(m);
     __syncthreads();
-    for (int o = 1; o < 1024; o <<= 1) {
-      const int v = threadIdx.x >= o ? s_scan[threadIdx.x - o] : 0;
-      __syncthreads();
-      s_scan[threadIdx.x] += v;
-      __syncthreads();
+    if (threadIdx.x == 0) {
+      int run = 0;
+      for (int w = 0; w < 16; ++w) {
+        const int c = s_wave[w];
+        s_wave[w] = run;
+        run += c;
+      }
+      s_wave[16] = run;
     }
-    const int incl = s_scan[threadIdx.x];
-    if (threadIdx.x == 1023) s_total = incl;
     __syncthreads();
-    if (keep) p.active_idx[out + incl - 1] = idx;
-    out += s_total;
+    if (keep) p.active_idx[out + s_wave[wave] + before] = idx;
+    out += s_wave[16];
     __syncthreads();
   }
   if (threadIdx.x == 0) {
@@ -573,7 +626,7 @@ hipError_t launch_subst(const LayerParams& p, hipStream_t st) {
 
 hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st) {
   const int nb = cdiv(p.T, RB);
-  const size_t lds = (size_t)RB * p.E * sizeof(float);
+  const size_t lds = 2 * (size_t)RB * p.E * sizeof(float);
   if (bf16)
     hipLaunchKernelGGL(k_route<true>, dim3(nb), dim3(256), lds, st, p);
   else
@@ -582,21 +635,17 @@ hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st) {
 }
 
 hipError_t launch_scan(const LayerParams& p, hipStream_t st) {
-  hipLaunchKernelGGL(k_scan, dim3(1), dim3(256), 0, st, p);
+  hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, st, p);
   return hipGetLastError();
 }
 
-hipError_t launch_permute(const LayerParams& p, bool bf16, hipStream_t st) {
-  const int nb = cdiv(p.T, RB);
-  if (bf16)
-    hipLaunchKernelGGL(k_permute<bf16_t>, dim3(nb), dim3(256), 0, st, p);
-  else
-    hipLaunchKernelGGL(k_permute<float>, dim3(nb), dim3(256), 0, st, p);
+hipError_t launch_bucket(const LayerParams& p, hipStream_t st) {
+  hipLaunchKernelGGL(k_bucket, dim3(cdiv(p.T, RB)), dim3(256), 0, st, p);
   return hipGetLastError();
 }
 
 hipError_t launch_combine(const LayerParams& p, bool bf16, hipStream_t st) {
-  const int nb = p.T < 2048 ? p.T : 2048;
+  const int nb = cdiv(p.T * (p.d / 8), 256) < 4096 ? cdiv(p.T * (p.d / 8), 256) : 4096;
   if (bf16)
     hipLaunchKernelGGL(k_combine<bf16_t>, dim3(nb), dim3(256), 0, st, p);
   else

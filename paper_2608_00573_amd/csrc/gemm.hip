@@ -85,28 +85,55 @@ struct Regs {
   u32x4_t b1[T::NB == 2 ? T::B_PT : 1];
 };
 
+// A / B* point at row 0 of their matrices.  Tile row r of A is matrix row
+// a_idx[r] (a gather through a token list) or a_row0 + r; likewise for B.
 struct CoreArgs {
   const bf16_t* A;
   const bf16_t* B0;
   const bf16_t* B1;
+  const int* a_idx;
+  const int* b_idx;
+  int a_row0, b_row0;
   int a_valid, b_valid, K, k_begin, nk;
 };
 
-// thread t loads chunk t%8 of rows t/8 + i * ROWS_PER_PASS of slice kt
+// Per-thread source pointers: thread t loads chunk t%8 of tile rows
+// t/8 + i * ROWS_PER_PASS; rows past the valid range use the last valid row.
 template <class T>
-__device__ __forceinline__ void gload(Regs<T>& r, const CoreArgs& c, int kt) {
+struct Ptrs {
+  const bf16_t* a[T::A_PT];
+  const bf16_t* b0[T::B_PT];
+  const bf16_t* b1[T::NB == 2 ? T::B_PT : 1];
+};
+
+template <class T>
+__device__ __forceinline__ void make_ptrs(Ptrs<T>& q, const CoreArgs& c) {
   const int t = threadIdx.x;
-  const int col = c.k_begin + kt * BK + 8 * (t & 7);
+  const size_t col = (size_t)c.k_begin + 8 * (t & 7);
 #pragma unroll
   for (int i = 0; i < T::A_PT; ++i) {
-    const int row = min((t >> 3) + T::ROWS_PER_PASS * i, c.a_valid - 1);
-    r.a[i] = *reinterpret_cast<const u32x4_t*>(c.A + (size_t)row * c.K + col);
+    const int r = min((t >> 3) + T::ROWS_PER_PASS * i, c.a_valid - 1);
+    const int src = c.a_idx ? c.a_idx[r] : c.a_row0 + r;
+    q.a[i] = c.A + (size_t)src * c.K + col;
   }
 #pragma unroll
   for (int i = 0; i < T::B_PT; ++i) {
-    const int row = min((t >> 3) + T::ROWS_PER_PASS * i, c.b_valid - 1);
-    r.b0[i] = *reinterpret_cast<const u32x4_t*>(c.B0 + (size_t)row * c.K + col);
-    if constexpr (T::NB == 2) r.b1[i] = *reinterpret_cast<const u32x4_t*>(c.B1 + (size_t)row * c.K + col);
+    const int r = min((t >> 3) + T::ROWS_PER_PASS * i, c.b_valid - 1);
+    const int src = c.b_idx ? c.b_idx[r] : c.b_row0 + r;
+    q.b0[i] = c.B0 + (size_t)src * c.K + col;
+    if constexpr (T::NB == 2) q.b1[i] = c.B1 + (size_t)src * c.K + col;
+  }
+}
+
+template <class T>
+__device__ __forceinline__ void gload(Regs<T>& r, const Ptrs<T>& q, int kt) {
+  const int o = kt * BK;
+#pragma unroll
+  for (int i = 0; i < T::A_PT; ++i) r.a[i] = *reinterpret_cast<const u32x4_t*>(q.a[i] + o);
+#pragma unroll
+  for (int i = 0; i < T::B_PT; ++i) {
+    r.b0[i] = *reinterpret_cast<const u32x4_t*>(q.b0[i] + o);
+    if constexpr (T::NB == 2) r.b1[i] = *reinterpret_cast<const u32x4_t*>(q.b1[i] + o);
   }
 }
 
@@ -183,22 +210,24 @@ __device__ __forceinline__ void gemm_core(char* lds0, char* lds1, const CoreArgs
       acc0[i][j] = z;
       if constexpr (T::NB == 2) acc1[i][j] = z;
     }
+  Ptrs<T> q;
+  make_ptrs<T>(q, c);
   Regs<T> r0, r1;
   const int nk = c.nk, last = c.nk - 1;
-  gload<T>(r0, c, 0);
-  gload<T>(r1, c, min(1, last));
+  gload<T>(r0, q, 0);
+  gload<T>(r1, q, min(1, last));
   sstore<T>(lds0, r0);
   __syncthreads();
-  gload<T>(r0, c, min(2, last));
+  gload<T>(r0, q, min(2, last));
   for (int kt = 0; kt < nk; kt += 2) {
     mma_slice<T>(lds0, wm, wn, lane, acc0, acc1);  // slice kt
     sstore<T>(lds1, r1);                           // slice kt + 1
     __syncthreads();
-    gload<T>(r1, c, min(kt + 3, last));
+    gload<T>(r1, q, min(kt + 3, last));
     if (kt + 1 < nk) mma_slice<T>(lds1, wm, wn, lane, acc0, acc1);
     sstore<T>(lds0, r0);                           // slice kt + 2
     __syncthreads();
-    gload<T>(r0, c, min(kt + 4, last));
+    gload<T>(r0, q, min(kt + 4, last));
   }
 }
 
@@ -220,7 +249,8 @@ __device__ __forceinline__ int acc_col(int wn, int j, int lane) {
 // Rows come in expert groups; tile list entry = (expert, row begin, row end).
 // Dense mode (shared expert): one group, rows [0, *dense_rows).
 struct FfnArgs {
-  const bf16_t* X;        // [rows, K]
+  const bf16_t* X;        // [rows, K], or h [T, K] when x_idx is set
+  const int* x_idx;       // row -> source row of X (gather), or NULL
   const bf16_t* W0;       // expert 0 of [E, N, K] (up, or down)
   const bf16_t* W1;       // gate, same layout, or NULL
   size_t w_stride;        // elements between experts
@@ -260,7 +290,8 @@ __global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
   const int nk = (a.K / BK) / a.n_split;
   f32x16_t acc0[T::TM][T::TN], acc1[T::TM][T::TN];
   gemm_core<T>(lds_buf0, lds_buf1,
-               CoreArgs{a.X + (size_t)m0 * a.K, W0, W1, a_valid, b_valid, a.K, sp * nk * BK, nk},
+               CoreArgs{a.X, W0, W1, a.x_idx ? a.x_idx + m0 : nullptr, nullptr, m0, 0, a_valid,
+                        b_valid, a.K, sp * nk * BK, nk},
                acc0, acc1);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -294,10 +325,18 @@ __global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
 }
 
 // ----------------------------------------------------------- exit head --
-// M = vocabulary (A = W_exit [V, d]), N = executed tokens (B = hx [n_x, d]).
+// M = vocabulary (A = W_exit [V, d]), N = executed tokens (B = hx [n_x, d],
+// the executed tokens' updated rows written by the combine kernel).
 // Epilogue: for every token column, max and sum exp over the tile's
 // vocabulary rows (bias added), written as one partial per vocabulary tile
 // as (max z * log2 e, sum exp(z - max z)).
+//
+// Persistent: the grid has one block per CU; block b walks the tiles
+// tb + i0, tb + i0 + bx, ... of its XCD's contiguous tile range (bx = blocks
+// on that XCD), so the bx blocks of an XCD work on bx consecutive tiles of
+// the patch order at any time.  Its K slices form one continuous load
+// stream across tiles: the first slices of the next tile are already in
+// flight while the current tile's epilogue runs.
 struct ExitArgs {
   const bf16_t* W;    // [V, K]
   const bf16_t* H;    // [n_x, K]
@@ -309,52 +348,88 @@ struct ExitArgs {
 
 using ExitTile = Tile<kExitTileBF16, 128, 1, 4, 2>;
 
-__global__ __launch_bounds__(ExitTile::THREADS) void k_exit_mma(ExitArgs a) {
+struct ExitSched {
+  int tb, i0, bx, n_mt, n_nt, n_x, nk;
+  // tile j of this block -> vocabulary tile mt, token tile nt (patch order)
+  __device__ __forceinline__ void decode(int j, int& mt, int& nt) const {
+    const int L = tb + i0 + j * bx;
+    const int span = kPatch * n_nt;
+    const int g = L / span, w = L % span;
+    const int gm = min(kPatch, n_mt - g * kPatch);
+    nt = w / gm;
+    mt = g * kPatch + w % gm;
+  }
+};
+
+// load slice g of the block's stream (clamped to the last one) into rr,
+// switching the row pointers when the stream enters a new tile
+__device__ __forceinline__ void exit_load(Regs<ExitTile>& rr, int g, int G, Ptrs<ExitTile>& q,
+                                          int& lt, const ExitSched& S, const ExitArgs& a) {
   using T = ExitTile;
-  TRIMMOE_STAGES(T);
-  __shared__ float2 s_part[T::GM][T::BN];  // per wavefront row: (max, sum) per token column
-  const int n_x = *a.n_exec;
-  const int n_mt = a.n_vtiles, n_nt = (n_x + T::BN - 1) / T::BN;
-  int mt, nt, sp;
-  if (!map_tile(blockIdx.x, n_mt, n_nt, 1, mt, nt, sp)) return;
+  g = min(g, G - 1);
+  const int j = g / S.nk;
+  if (j != lt) {
+    int mt, nt;
+    S.decode(j, mt, nt);
+    const CoreArgs c{a.W, a.H, nullptr, nullptr, nullptr, mt * T::BM, nt * T::BN,
+                     min(T::BM, a.V - mt * T::BM), min(T::BN, S.n_x - nt * T::BN), a.K, 0, S.nk};
+    make_ptrs<T>(q, c);
+    lt = j;
+  }
+  gload<T>(rr, q, g - j * S.nk);
+}
+
+__device__ __forceinline__ void exit_epilogue(int j, const ExitSched& S, const ExitArgs& a,
+                                              f32x16_t (&acc)[ExitTile::TM][ExitTile::TN],
+                                              float2 (&s_part)[ExitTile::GM][ExitTile::BN]) {
+  using T = ExitTile;
+  int mt, nt;
+  S.decode(j, mt, nt);
   const int v0 = mt * T::BM, j0 = nt * T::BN;
   const int a_valid = min(T::BM, a.V - v0);
-  const int b_valid = min(T::BN, n_x - j0);
-  f32x16_t acc0[T::TM][T::TN], acc1[T::TM][T::TN];
-  gemm_core<T>(lds_buf0, lds_buf1,
-               CoreArgs{a.W + (size_t)v0 * a.K, a.H + (size_t)j0 * a.K, nullptr, a_valid, b_valid,
-                        a.K, 0, a.K / BK},
-               acc0, acc1);
+  const int b_valid = min(T::BN, S.n_x - j0);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / T::GN, wn = wave % T::GN;
   // partials in base 2: y = z * log2(e), so exp(z - max z) = exp2(y - max y)
   // is one FMA and one v_exp_f32 per logit; the pair stored is (max y, sum)
   const float ninf = -__builtin_inff();
   const float kLog2e = 1.4426950408889634f;
+  const bool full = a_valid == T::BM && !a.bias;
 #pragma unroll
-  for (int j = 0; j < T::TN; ++j) {
+  for (int jj = 0; jj < T::TN; ++jj) {
     float m = ninf;
+    if (full) {
 #pragma unroll
-    for (int i = 0; i < T::TM; ++i)
+      for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = acc_row<T>(wm, i, r, lane);
-        float y = acc0[i][j][r];
-        if (a.bias) y += a.bias[v0 + min(row, a_valid - 1)];
-        y = row < a_valid ? y * kLog2e : ninf;
-        acc0[i][j][r] = y;
-        m = fmaxf(m, y);
-      }
+        for (int r = 0; r < 16; ++r) {
+          const float y = acc[i][jj][r] * kLog2e;
+          acc[i][jj][r] = y;
+          m = fmaxf(m, y);
+        }
+    } else {
+#pragma unroll
+      for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = acc_row<T>(wm, i, r, lane);
+          float y = acc[i][jj][r];
+          if (a.bias) y += a.bias[v0 + min(row, a_valid - 1)];
+          y = row < a_valid ? y * kLog2e : ninf;
+          acc[i][jj][r] = y;
+          m = fmaxf(m, y);
+        }
+    }
     m = fmaxf(m, __shfl_xor(m, 32));
-    float s = 0.f;
+    float sum = 0.f;
     if (m != ninf) {
 #pragma unroll
       for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s += __builtin_amdgcn_exp2f(acc0[i][j][r] - m);
+        for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(acc[i][jj][r] - m);
     }
-    s += __shfl_xor(s, 32);
-    if (lane < 32) s_part[wm][acc_col<T>(wn, j, lane)] = make_float2(m, s);
+    sum += __shfl_xor(sum, 32);
+    if (lane < 32) s_part[wm][acc_col<T>(wn, jj, lane)] = make_float2(m, sum);
   }
   __syncthreads();
   const int c = threadIdx.x;
@@ -362,13 +437,73 @@ __global__ __launch_bounds__(ExitTile::THREADS) void k_exit_mma(ExitArgs a) {
     float M = s_part[0][c].x;
 #pragma unroll
     for (int g = 1; g < T::GM; ++g) M = fmaxf(M, s_part[g][c].x);
-    float S = 0.f;
+    float S2 = 0.f;
 #pragma unroll
     for (int g = 0; g < T::GM; ++g) {
-      const float2 q = s_part[g][c];
-      if (q.y > 0.f) S += q.y * __builtin_amdgcn_exp2f(q.x - M);
+      const float2 v = s_part[g][c];
+      if (v.y > 0.f) S2 += v.y * __builtin_amdgcn_exp2f(v.x - M);
     }
-    a.partials[(size_t)(j0 + c) * a.n_vtiles + mt] = make_float2(M, S);
+    a.partials[(size_t)(j0 + c) * a.n_vtiles + mt] = make_float2(M, S2);
+  }
+  const f32x16_t z = {};
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+    for (int jj = 0; jj < T::TN; ++jj) acc[i][jj] = z;
+}
+
+__global__ __launch_bounds__(ExitTile::THREADS) void k_exit_mma(ExitArgs a) {
+  using T = ExitTile;
+  TRIMMOE_STAGES(T);
+  __shared__ float2 s_part[T::GM][T::BN];  // per wavefront row: (max, sum) per token column
+  const int n_x = *a.n_exec;
+  ExitSched S;
+  S.n_mt = a.n_vtiles;
+  S.n_nt = (n_x + T::BN - 1) / T::BN;
+  S.n_x = n_x;
+  S.nk = a.K / BK;
+  const int total = S.n_mt * S.n_nt;
+  // XCD groups (fewer when the grid is smaller than the XCD count)
+  const int nx = min(kXcd, (int)gridDim.x);
+  const int x = blockIdx.x % nx;
+  S.i0 = blockIdx.x / nx;
+  S.bx = ((int)gridDim.x - x + nx - 1) / nx;
+  const int q = total / nx, r = total % nx;
+  S.tb = x * q + min(x, r);
+  const int te = S.tb + q + (x < r ? 1 : 0);
+  if (S.tb + S.i0 >= te) return;
+  const int ntiles = (te - (S.tb + S.i0) + S.bx - 1) / S.bx;
+  const int nk = S.nk, G = ntiles * nk;
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wm = wave / T::GN, wn = wave % T::GN;
+  f32x16_t acc[T::TM][T::TN], unused[T::TM][T::TN];
+  const f32x16_t z = {};
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+    for (int jj = 0; jj < T::TN; ++jj) acc[i][jj] = z;
+  Ptrs<T> qp;
+  int lt = -1;
+  Regs<T> r0, r1;
+  exit_load(r0, 0, G, qp, lt, S, a);
+  exit_load(r1, 1, G, qp, lt, S, a);
+  sstore<T>(lds_buf0, r0);
+  __syncthreads();
+  exit_load(r0, 2, G, qp, lt, S, a);
+  for (int gc = 0; gc < G; gc += 2) {
+    mma_slice<T>(lds_buf0, wm, wn, lane, acc, unused);  // slice gc
+    if (gc % nk == nk - 1) exit_epilogue(gc / nk, S, a, acc, s_part);
+    sstore<T>(lds_buf1, r1);  // slice gc + 1
+    __syncthreads();
+    exit_load(r1, gc + 3, G, qp, lt, S, a);
+    if (gc + 1 < G) {
+      mma_slice<T>(lds_buf1, wm, wn, lane, acc, unused);
+      if ((gc + 1) % nk == nk - 1) exit_epilogue((gc + 1) / nk, S, a, acc, s_part);
+    }
+    sstore<T>(lds_buf0, r0);  // slice gc + 2
+    __syncthreads();
+    exit_load(r0, gc + 4, G, qp, lt, S, a);
   }
 }
 
@@ -377,10 +512,10 @@ constexpr int FT = kF32Tile;
 
 // out[m][n] = X[m] . W[e][n] over a 128-row group tile, 16 columns per block.
 template <bool UP>
-__global__ __launch_bounds__(256) void k_ffn_f32(const float* X, const float* W0, const float* W1,
-                                                 size_t w_stride, int K, int N, const int4* tiles,
-                                                 const int* n_tiles, const int* dense_rows,
-                                                 void* out, int act) {
+__global__ __launch_bounds__(256) void k_ffn_f32(const float* X, const int* x_idx, const float* W0,
+                                                 const float* W1, size_t w_stride, int K, int N,
+                                                 const int4* tiles, const int* n_tiles,
+                                                 const int* dense_rows, void* out, int act) {
   const int n_nt = (N + FT - 1) / FT;
   const int n_mt = dense_rows ? (*dense_rows + kGemmBM - 1) / kGemmBM : *n_tiles;
   const int mt = blockIdx.x / n_nt, ntile = blockIdx.x % n_nt;
@@ -402,7 +537,7 @@ __global__ __launch_bounds__(256) void k_ffn_f32(const float* X, const float* W0
   const float* w0 = W0 + (size_t)e * w_stride + (size_t)n * K;
   const float* w1 = W1 ? W1 + (size_t)e * w_stride + (size_t)n * K : nullptr;
   for (int m = m0 + ty; m < min(m0 + kGemmBM, m1); m += 256 / FT) {
-    const float* x = X + (size_t)m * K;
+    const float* x = X + (size_t)(x_idx ? x_idx[m] : m) * K;
     float u = 0.f, g = 0.f;
     for (int j = 0; j < K; ++j) {
       u = fmaf(x[j], w0[j], u);
@@ -418,9 +553,9 @@ __global__ __launch_bounds__(256) void k_ffn_f32(const float* X, const float* W0
 }
 
 // exit head, fp32: block = 16 vocabulary rows x 16 tokens
-__global__ __launch_bounds__(256) void k_exit_f32(const float* W, const float* H, const float* bias,
-                                                  const int* n_exec, int V, int K, int n_vtiles,
-                                                  float2* partials) {
+__global__ __launch_bounds__(256) void k_exit_f32(const float* W, const float* H, const int* tok,
+                                                  const float* bias, const int* n_exec, int V,
+                                                  int K, int n_vtiles, float2* partials) {
   __shared__ float s_z[FT][FT + 1];
   const int n_x = *n_exec;
   const int vt = blockIdx.x % n_vtiles, jt = blockIdx.x / n_vtiles;
@@ -430,7 +565,7 @@ __global__ __launch_bounds__(256) void k_exit_f32(const float* W, const float* H
   float z = -__builtin_inff();
   if (v < V && j < n_x) {
     const float* w = W + (size_t)v * K;
-    const float* h = H + (size_t)j * K;
+    const float* h = H + (size_t)tok[j] * K;
     float acc = 0.f;
     for (int c = 0; c < K; ++c) acc = fmaf(w[c], h[c], acc);
     z = acc + (bias ? bias[v] : 0.f);
@@ -482,7 +617,10 @@ static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared
   const void* w0 = shared ? (up ? p.ws_up : p.ws_down) : (up ? p.w_up : p.w_down);
   const void* w1 = dual ? (shared ? p.ws_gate : p.w_gate) : nullptr;
   const size_t w_stride = shared ? 0 : (size_t)N * K;
-  const void* X = up ? (shared ? p.xs : p.x_perm) : (shared ? p.act_s : p.act_buf);
+  // up projections gather h rows: routed rows through row_src, shared-expert
+  // rows through the executed-token list
+  const void* X = up ? p.h : (shared ? p.act_s : p.act_buf);
+  const int* x_idx = up ? (shared ? p.exec_list : p.row_src) : nullptr;
   void* out = up ? (shared ? p.act_s : p.act_buf) : (shared ? (void*)p.y_s : (void*)p.y_buf);
   const int* dense = shared ? &p.counts[kCntExec] : nullptr;
   const int max_mt = shared ? cdiv(p.T, kGemmBM) : p.max_tiles;
@@ -490,7 +628,7 @@ static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared
   if (max_mt <= 0) return hipSuccess;
   if (bf16) {
     const int n_split = (!up && !shared) ? p.down_splits : 1;
-    FfnArgs a{static_cast<const bf16_t*>(X), static_cast<const bf16_t*>(w0),
+    FfnArgs a{static_cast<const bf16_t*>(X), x_idx, static_cast<const bf16_t*>(w0),
               static_cast<const bf16_t*>(w1), w_stride, K, N, p.tiles, &p.counts[kCntTiles],
               dense, out, p.y_split_stride, n_split, act};
     if (up && dual)
@@ -503,11 +641,11 @@ static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared
     const dim3 grid(max_mt * cdiv(N, FT));
     if (up)
       hipLaunchKernelGGL(k_ffn_f32<true>, grid, dim3(256), 0, st, static_cast<const float*>(X),
-                         static_cast<const float*>(w0), static_cast<const float*>(w1), w_stride, K,
-                         N, p.tiles, &p.counts[kCntTiles], dense, out, act);
+                         x_idx, static_cast<const float*>(w0), static_cast<const float*>(w1),
+                         w_stride, K, N, p.tiles, &p.counts[kCntTiles], dense, out, act);
     else
       hipLaunchKernelGGL(k_ffn_f32<false>, grid, dim3(256), 0, st, static_cast<const float*>(X),
-                         static_cast<const float*>(w0), nullptr, w_stride, K, N, p.tiles,
+                         x_idx, static_cast<const float*>(w0), nullptr, w_stride, K, N, p.tiles,
                          &p.counts[kCntTiles], dense, out, act);
   }
   return hipGetLastError();
@@ -532,13 +670,15 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
   if (bf16) {
     ExitArgs a{static_cast<const bf16_t*>(p.w_exit), static_cast<const bf16_t*>(p.hx), p.b_exit,
                &p.counts[kCntExec], p.V, p.d, p.n_vtiles, p.partials};
-    const dim3 grid(p.n_vtiles * cdiv(p.T, ExitTile::BN));
+    // persistent: one block per CU (at most one tile per block in the worst case)
+    const int max_tiles = p.n_vtiles * cdiv(p.T, ExitTile::BN);
+    const dim3 grid(min(max_tiles, p.n_cu));
     hipLaunchKernelGGL(k_exit_mma, grid, dim3(ExitTile::THREADS), 0, st, a);
   } else {
     const dim3 grid(p.n_vtiles * cdiv(p.T, FT));
     hipLaunchKernelGGL(k_exit_f32, grid, dim3(256), 0, st, static_cast<const float*>(p.w_exit),
-                       static_cast<const float*>(p.hx), p.b_exit, &p.counts[kCntExec], p.V, p.d,
-                       p.n_vtiles, p.partials);
+                       static_cast<const float*>(p.h), p.exec_list, p.b_exit, &p.counts[kCntExec],
+                       p.V, p.d, p.n_vtiles, p.partials);
   }
   return hipGetLastError();
 }
