@@ -158,34 +158,65 @@ __device__ __forceinline__ void sstore(char* sb, const Regs<T>& r) {
   }
 }
 
+// store piece p of register set r (A rows first, then B0, then B1) into LDS
+// stage sb, at the swizzled position sstore uses
 template <class T>
-__device__ __forceinline__ void mma_slice(const char* sb, int wm, int wn, int lane,
+__device__ __forceinline__ void sstore_piece(char* sb, const Regs<T>& r, int p) {
+  const int t = threadIdx.x;
+  if (p < T::A_PT) {
+    const int row = (t >> 3) + p * T::ROWS_PER_PASS;
+    *reinterpret_cast<u32x4_t*>(sb + row * 128 + (((t & 7) ^ swz(row)) << 4)) = r.a[p];
+    return;
+  }
+  p -= T::A_PT;
+  const int i = p % T::B_PT, which = p / T::B_PT;
+  const int row = (t >> 3) + i * T::ROWS_PER_PASS;
+  const int off = T::A_BYTES + which * T::B_BYTES + row * 128 + (((t & 7) ^ swz(row)) << 4);
+  if (which == 0) *reinterpret_cast<u32x4_t*>(sb + off) = r.b0[i];
+  else if constexpr (T::NB == 2) *reinterpret_cast<u32x4_t*>(sb + off) = r.b1[i];
+}
+
+// One BK slice from LDS stage sb.  Fragments for k-step ks+1 are read while
+// the MFMAs of k-step ks run, and the next slice's register set rn goes into
+// stage nxt, spread over the k-steps so that the LDS writes overlap
+// the MFMAs instead of stalling every wavefront at once; nxt was last read
+// before the previous barrier, so it is free.
+template <class T>
+__device__ __forceinline__ void mma_slice(const char* sb, char* nxt, const Regs<T>& rn,
+                                          int wm, int wn, int lane,
                                           f32x16_t (&acc0)[T::TM][T::TN],
                                           f32x16_t (&acc1)[T::TM][T::TN]) {
+  constexpr int KS = BK / 16;
+  constexpr int NP = T::A_PT + T::B_PT * T::NB;
   const int fr = lane & 31, hi = lane >> 5;
   const int sw = swz(fr);  // fragment rows are 32-aligned offsets plus fr
-#pragma unroll
-  for (int ks = 0; ks < BK / 16; ++ks) {
+  bf16x8_t a[2][T::TM], b0[2][T::TN], b1[2][T::NB == 2 ? T::TN : 1];
+  auto frag = [&](int ks, int buf) {
     const int ch = ((2 * ks + hi) ^ sw) << 4;
-    bf16x8_t a[T::TM], b0[T::TN], b1[T::TN];
 #pragma unroll
     for (int i = 0; i < T::TM; ++i)
-      a[i] = *reinterpret_cast<const bf16x8_t*>(sb + (wm * T::WM + i * 32 + fr) * 128 + ch);
+      a[buf][i] = *reinterpret_cast<const bf16x8_t*>(sb + (wm * T::WM + i * 32 + fr) * 128 + ch);
 #pragma unroll
     for (int j = 0; j < T::TN; ++j) {
-      b0[j] = *reinterpret_cast<const bf16x8_t*>(sb + T::A_BYTES +
-                                                 (wn * T::WN + j * 32 + fr) * 128 + ch);
-      if constexpr (T::NB == 2)
-        b1[j] = *reinterpret_cast<const bf16x8_t*>(sb + T::A_BYTES + T::B_BYTES +
-                                                   (wn * T::WN + j * 32 + fr) * 128 + ch);
+      const int o = T::A_BYTES + (wn * T::WN + j * 32 + fr) * 128 + ch;
+      b0[buf][j] = *reinterpret_cast<const bf16x8_t*>(sb + o);
+      if constexpr (T::NB == 2) b1[buf][j] = *reinterpret_cast<const bf16x8_t*>(sb + T::B_BYTES + o);
     }
+  };
+  frag(0, 0);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const int buf = ks & 1;
+    if (ks + 1 < KS) frag(ks + 1, buf ^ 1);
+#pragma unroll
+    for (int p = ks * NP / KS; p < (ks + 1) * NP / KS; ++p) sstore_piece<T>(nxt, rn, p);
 #pragma unroll
     for (int i = 0; i < T::TM; ++i)
 #pragma unroll
       for (int j = 0; j < T::TN; ++j) {
-        acc0[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b0[j], acc0[i][j], 0, 0, 0);
+        acc0[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b0[buf][j], acc0[i][j], 0, 0, 0);
         if constexpr (T::NB == 2)
-          acc1[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b1[j], acc1[i][j], 0, 0, 0);
+          acc1[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b1[buf][j], acc1[i][j], 0, 0, 0);
       }
   }
 }
@@ -220,12 +251,11 @@ __device__ __forceinline__ void gemm_core(char* lds0, char* lds1, const CoreArgs
   __syncthreads();
   gload<T>(r0, q, min(2, last));
   for (int kt = 0; kt < nk; kt += 2) {
-    mma_slice<T>(lds0, wm, wn, lane, acc0, acc1);  // slice kt
-    sstore<T>(lds1, r1);                           // slice kt + 1
+    mma_slice<T>(lds0, lds1, r1, wm, wn, lane, acc0, acc1);  // slice kt; store kt + 1
     __syncthreads();
     gload<T>(r1, q, min(kt + 3, last));
-    if (kt + 1 < nk) mma_slice<T>(lds1, wm, wn, lane, acc0, acc1);
-    sstore<T>(lds0, r0);                           // slice kt + 2
+    if (kt + 1 < nk) mma_slice<T>(lds1, lds0, r0, wm, wn, lane, acc0, acc1);
+    else sstore<T>(lds0, r0);                                        // slice kt + 2
     __syncthreads();
     gload<T>(r0, q, min(kt + 4, last));
   }
@@ -452,6 +482,9 @@ __device__ __forceinline__ void exit_epilogue(int j, const ExitSched& S, const E
     for (int jj = 0; jj < T::TN; ++jj) acc[i][jj] = z;
 }
 
+// EVEN: K / BK is even, so every tile ends on the second slice of a pair and
+// only one copy of the epilogue is needed in the loop body
+template <bool EVEN>
 __global__ __launch_bounds__(ExitTile::THREADS) void k_exit_mma(ExitArgs a) {
   using T = ExitTile;
   TRIMMOE_STAGES(T);
@@ -492,16 +525,16 @@ __global__ __launch_bounds__(ExitTile::THREADS) void k_exit_mma(ExitArgs a) {
   __syncthreads();
   exit_load(r0, 2, G, qp, lt, S, a);
   for (int gc = 0; gc < G; gc += 2) {
-    mma_slice<T>(lds_buf0, wm, wn, lane, acc, unused);  // slice gc
-    if (gc % nk == nk - 1) exit_epilogue(gc / nk, S, a, acc, s_part);
-    sstore<T>(lds_buf1, r1);  // slice gc + 1
+    mma_slice<T>(lds_buf0, lds_buf1, r1, wm, wn, lane, acc, unused);  // slice gc; store gc + 1
+    if (!EVEN && gc % nk == nk - 1) exit_epilogue(gc / nk, S, a, acc, s_part);
     __syncthreads();
     exit_load(r1, gc + 3, G, qp, lt, S, a);
-    if (gc + 1 < G) {
-      mma_slice<T>(lds_buf1, wm, wn, lane, acc, unused);
+    if (EVEN || gc + 1 < G) {
+      mma_slice<T>(lds_buf1, lds_buf0, r0, wm, wn, lane, acc, unused);  // store gc + 2
       if ((gc + 1) % nk == nk - 1) exit_epilogue((gc + 1) / nk, S, a, acc, s_part);
+    } else {
+      sstore<T>(lds_buf0, r0);
     }
-    sstore<T>(lds_buf0, r0);  // slice gc + 2
     __syncthreads();
     exit_load(r0, gc + 4, G, qp, lt, S, a);
   }
@@ -673,7 +706,10 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
     // persistent: one block per CU (at most one tile per block in the worst case)
     const int max_tiles = p.n_vtiles * cdiv(p.T, ExitTile::BN);
     const dim3 grid(min(max_tiles, p.n_cu));
-    hipLaunchKernelGGL(k_exit_mma, grid, dim3(ExitTile::THREADS), 0, st, a);
+    if ((p.d / BK) % 2 == 0)
+      hipLaunchKernelGGL(k_exit_mma<true>, grid, dim3(ExitTile::THREADS), 0, st, a);
+    else
+      hipLaunchKernelGGL(k_exit_mma<false>, grid, dim3(ExitTile::THREADS), 0, st, a);
   } else {
     const dim3 grid(p.n_vtiles * cdiv(p.T, FT));
     hipLaunchKernelGGL(k_exit_f32, grid, dim3(256), 0, st, static_cast<const float*>(p.w_exit),
