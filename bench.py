@@ -99,6 +99,31 @@ def algorithmic_work(cfg, counters):
     return out
 
 
+def counter_traffic(kernel, workload):
+    """Calibrated HBM-side bytes per launch of ``kernel`` on ``workload`` from
+    the committed rocprofv3 counter summaries (FETCH_SIZE and WRITE_SIZE
+    passes scaled by a plain copy), or (None, None) when no summary covers it
+    or the kernel's source file has changed since the counters were taken."""
+    import glob
+    import hashlib
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        fields = {}
+        for line in open(path):
+            k, sep, v = line.strip().partition(": ")
+            if sep and k in ("kernel", "workload", "traffic_bytes_per_launch", "source",
+                             "source_sha256"):
+                fields[k] = v.strip()
+        if fields.get("kernel") != kernel or fields.get("workload") != workload:
+            continue
+        src = os.path.join(ROOT, fields.get("source", ""))
+        if not os.path.isfile(src):
+            return None, None
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != fields.get("source_sha256"):
+            return None, None
+        return float(fields["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
+    return None, None
+
+
 def cpu_baseline(inp, target_s):
     """The oracle as it stands, one BLAS thread, on the first S tokens."""
     import numpy as np
@@ -130,8 +155,9 @@ def cpu_baseline(inp, target_s):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one MI355X: this build runs on a single GPU "
-              "(no sharding or collectives); run it with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no sharding or collectives "
+              "(tokens are independent; shard them across processes yourself); "
+              "run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
     if args.calibrate_copy:
         calibrate_copy()
@@ -213,6 +239,9 @@ def main():
                               w["flop_shared"] + w["flop_exit"]) / (peak * 1e12),
                              w["bytes"] / (PEAK_HBM_GBS * 1e9)) for w in work) * 1e3
     active_layers = sum(w["n_active"] for w in work)
+    dom_kernel = {"up": "k_ffn_mma", "down": "k_ffn_mma", "exit": "k_exit_mma",
+                  "shared": "k_ffn_mma"}[dom]
+    traffic, traffic_src = counter_traffic(dom_kernel, cfg["name"])
 
     out = {
         "metric": METRIC,
@@ -241,7 +270,9 @@ def main():
             "peak": peak,
             "unit": "TFLOP/s",
             "frac": dom_tflops / peak,
-            "traffic": None,
+            "traffic": traffic,
+            "traffic_unit": "bytes per launch",
+            "traffic_source": traffic_src,
             "avg_launch_ms": dom_ms / launches[dom] if launches[dom] else None,
             "algorithmic_flop_per_step": flops[dom],
         },

@@ -18,8 +18,7 @@ horizon H = 1 (Sec. V-E: with H = 1 the look-ahead term vanishes):
 * exit head confidence and exit gate              -- Sec. III-C, Eq. (7)-(9)
 * residual bypass of a skipped layer              -- Sec. III-B
 
-Readings taken where the paper is silent or ambiguous (each is also listed,
-with its reason, in the design notes of the repository):
+Readings taken where the paper is silent or ambiguous:
 
 A1  exit head: xi = max softmax(W_exit h + b) (a vocabulary head); the
     paper's own linear+sigmoid head (Sec. IV-A) is the "sigmoid" mode.
