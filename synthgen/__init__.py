@@ -9,7 +9,7 @@ from it without sharing any code of the method.
 """
 from .rng import splitmix64_stream, normal_f32, uniform_f64, key_for
 from .configs import WORKLOADS, workload
-from .inputs import make_inputs
+from .inputs import make_inputs, mid_state
 
 __all__ = ["splitmix64_stream", "normal_f32", "uniform_f64", "key_for",
-           "WORKLOADS", "workload", "make_inputs"]
+           "WORKLOADS", "workload", "make_inputs", "mid_state"]

@@ -205,16 +205,53 @@ def make_tokens(cfg, token_seed: int | None = None, device="cpu") -> torch.Tenso
 
 
 def make_inputs(cfg, device="cpu", token_seed: int | None = None,
-                with_layers: bool = True) -> dict:
-    """All inputs of one workload: {"cfg", "layers", "h0", "policy"}."""
+                with_layers: bool = True, layers=None) -> dict:
+    """All inputs of one workload: {"cfg", "layers", "h0", "policy"}.
+
+    ``layers`` (an iterable of layer indices) generates only those layers;
+    the other entries of the returned list are None.  A layer's tensors do
+    not depend on which other layers are generated.
+    """
     w_lm = exit_lm(cfg, device)
-    layers = []
+    out_layers = []
     if with_layers:
+        want = set(range(cfg["n_layers"])) if layers is None else set(layers)
         for l in range(cfg["n_layers"]):
-            layers.append(make_layer(cfg, l, w_lm, device))
+            out_layers.append(make_layer(cfg, l, w_lm, device) if l in want else None)
+    layers = out_layers
     del w_lm
     h0 = make_tokens(cfg, token_seed, device)
     policy = {k: cfg[k] for k in ("budget", "omega_t", "t_local", "t_remote",
                                   "phi_scale", "sim_min")}
     policy["p_exit"] = cfg["p_exit"]
     return dict(cfg=cfg, layers=layers, h0=h0, policy=policy)
+
+
+_ID_STATE_ACTIVE = (1 << 40) + 32
+_ID_STATE_DACC = (1 << 40) + 33
+
+
+def mid_state(cfg, layer: int, seed: int, active_frac: float = 0.85,
+              spent_frac: float = 0.9) -> dict:
+    """A seeded stack state as it could stand before layer ``layer`` (> 0):
+    a ragged subset of the tokens still active (each with probability
+    ``active_frac``, at least one), the others marked as exited at an earlier
+    layer; budget already spent per active token uniform over
+    [0, spent_frac * budget].  Plain draws: no decision is computed here.
+    Returns numpy arrays in the oracle's state layout (h is filled in by the
+    caller from the generated tokens)."""
+    import numpy as np
+    if layer < 1:
+        raise ValueError("mid_state: every token is active before layer 0")
+    T, N = cfg["n_tokens"], cfg["n_layers"]
+    ua = uniform_f64(seed, _ID_STATE_ACTIVE, T).numpy()
+    ud = uniform_f64(seed, _ID_STATE_DACC, T).numpy()
+    active = ua < active_frac
+    if not active.any():
+        active[int(np.argmin(ua))] = True
+    budget = float(np.float32(cfg["budget"]))
+    d_acc = np.where(active, ud * spent_frac * budget, 0.0).astype(np.float32).astype(np.float64)
+    exit_layer = np.where(active, N, (np.arange(T) % layer)).astype(np.int64)
+    xi = np.full(T, np.nan)
+    return dict(d_acc=d_acc, active=np.nonzero(active)[0].tolist(),
+                exit_layer=exit_layer, xi=xi)
