@@ -3,17 +3,23 @@
 
 A step is one trimmoe_stack_forward over one batch of synthetic tokens (all
 layers: route/decide, bucketing, grouped expert FFN, combine, exit head,
-exit gate, compaction), inputs already resident in HBM.  Prints one JSON
-line:
+exit gate, compaction), inputs already resident in HBM.  For the decode
+workload each step takes a fresh batch (32 tokens, its own seed).  Prints
+one JSON line:
 
 * value: tokens/s = tokens per batch * steps / timed seconds;
-* roofline: the dominant kernel class (by measured time) against its
-  roofline, from HIP events recorded around each kernel class on the
+* roofline: the dominant kernel class (by measured time) against its own
+  roofline (MFMA or HBM, whichever its algorithmic FLOPs and bytes make
+  binding), from HIP events recorded around each kernel class on the
   library's stream (trimmoe_stack_forward_timed) over a second timed pass;
+  traffic from the committed rocprofv3 counter summaries when they match;
 * cpu_baseline: the CPU oracle (single BLAS thread) on a bounded sample of
-  the same tokens, scaled to tokens/s (tokens are independent in this step);
-* grouped_gemm_mfma_frac: algorithmic FLOPs of the grouped up/gate and down
-  GEMMs over their measured time, against the bf16 dense MFMA peak.
+  the same tokens (and, for stacks too large to hold in fp64, of the first
+  layers), scaled to tokens/s (tokens are independent in this step);
+* grouped_gemm_mfma_frac / grouped_gemm_hbm_frac: algorithmic FLOPs and
+  weight bytes of the grouped up/gate and down GEMMs over their measured
+  time, against the bf16 dense MFMA peak and the HBM bandwidth;
+* class_hbm_frac: algorithmic bytes over measured time for every class.
 """
 from __future__ import annotations
 
@@ -36,7 +42,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default 20; the decode workload: its step count, 128)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="switch_base_8e")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -64,14 +71,17 @@ def calibrate_copy():
 
 
 def algorithmic_work(cfg, counters):
-    """Per-layer algorithmic FLOPs and bytes from the traced counters.
+    """Per-layer algorithmic FLOPs and bytes, per kernel class, from the
+    traced counters.
 
     counters[l] = (active, executed, skipped, exited, substituted slots,
     remote slots, merged rows, distinct experts).  Only the work the method
     must do: router over active tokens; expert FFN over merged rows; shared
     expert and exit head over executed tokens (exit head not at the last
-    layer); weight bytes of each matrix touched once; h read per active and
-    written per executed token.
+    layer); every weight matrix touched read once; h read per active token
+    and written per executed token; index lists of the bucketing.
+    Intermediates (activations, split-K partials, softmax partials) are
+    implementation bytes and not counted.
     """
     N, d, E, F, Fs, V = (cfg[k] for k in ("n_layers", "d_model", "n_experts", "d_ff",
                                           "d_ff_shared", "vocab_exit"))
@@ -81,21 +91,20 @@ def algorithmic_work(cfg, counters):
     for l in range(N):
         n_a, n_x, rows, distinct = (int(counters[l][i]) for i in (0, 1, 6, 7))
         last = l == N - 1
-        f_route = 2 * n_a * d * E
-        f_up = 2 * rows * d * F * (m - 1)
-        f_down = 2 * rows * d * F
-        f_shared = 6 * n_x * d * Fs
-        f_exit = 0 if last else 2 * n_x * d * V
-        by_route = (E * d * b if n_a else 0) + n_a * d * b
-        by_experts = distinct * m * d * F * b
-        by_shared = 3 * d * Fs * b if (n_x and Fs) else 0
-        by_exit = 0 if (last or not n_x) else V * d * b
-        by_out = n_x * d * b
+        flop = dict(route=2 * n_a * d * E, bucket=0,
+                    up=2 * rows * d * F * (m - 1), down=2 * rows * d * F,
+                    shared=6 * n_x * d * Fs, combine=0,
+                    exit=0 if last else 2 * n_x * d * V, gate=0)
+        byt = dict(route=(E * d * b if n_a else 0) + n_a * d * b,
+                   bucket=8 * (rows + n_a),
+                   up=distinct * (m - 1) * d * F * b + rows * d * b,
+                   down=distinct * d * F * b,
+                   shared=(3 * d * Fs * b + n_x * d * b) if (n_x and Fs) else 0,
+                   combine=2 * n_x * d * b,
+                   exit=0 if (last or not n_x) else V * d * b + n_x * d * b,
+                   gate=0 if last else 8 * n_a)
         out.append(dict(layer=l, n_active=n_a, n_exec=n_x, rows=rows, distinct=distinct,
-                        flop_route=f_route, flop_up=f_up, flop_down=f_down,
-                        flop_shared=f_shared, flop_exit=f_exit,
-                        bytes=by_route + by_experts + by_shared + by_exit + by_out,
-                        bytes_exit=by_exit + (0 if last else n_x * d * b)))
+                        flop=flop, bytes=byt))
     return out
 
 
@@ -124,32 +133,54 @@ def counter_traffic(kernel, workload):
     return None, None
 
 
-def cpu_baseline(inp, target_s):
-    """The oracle as it stands, one BLAS thread, on the first S tokens."""
+def _f64_layer_bytes(cfg):
+    m = 3 if cfg["act"] == "swiglu" else 2
+    d, E = cfg["d_model"], cfg["n_experts"]
+    return 8 * (E * m * d * cfg["d_ff"] + 3 * d * cfg["d_ff_shared"] +
+                cfg["vocab_exit"] * d + E * d + E * E)
+
+
+def cpu_baseline(inp, target_s, max_f64_bytes=24e9):
+    """The oracle as it stands, one BLAS thread, on the first S tokens.
+
+    The oracle works on fp64 copies of the weights.  When the whole stack
+    would not fit in ``max_f64_bytes`` it runs the first layers only and the
+    time is scaled to all layers (early layers have the most active tokens,
+    so this errs towards a slower oracle).  Weight conversion is outside the
+    timed part; only the oracle's layer steps are timed."""
     import numpy as np
     from threadpoolctl import threadpool_limits
 
     import oracle as O
 
     cfg = inp["cfg"]
-    model = O.model_from_inputs(inp)
+    N = cfg["n_layers"]
+    n_l = min(N, max(1, int(max_f64_bytes // _f64_layer_bytes(cfg))))
+    models = {l: O.model_from_inputs(inp, layers=[l]) for l in range(n_l)}
     pol = {k: float(np.float32(v)) for k, v in inp["policy"].items()}
     h0 = inp["h0"].double().cpu().numpy()
     T = h0.shape[0]
     with threadpool_limits(limits=1):
-        # size the sample from a small probe, then refine once
-        S = min(T, 64)
+        # size the sample from a small probe, then refine
+        S = min(T, 64 if n_l == N else 8)
         for _ in range(3):
-            t0 = time.perf_counter()
-            O.stack_forward(model, pol, h0[:S])
-            dt = time.perf_counter() - t0
+            state = O.init_state(h0[:S], N)
+            dt = 0.0
+            for l in range(n_l):
+                t0 = time.perf_counter()
+                O.layer_step(models[l], l, pol, state)
+                dt += time.perf_counter() - t0
             if dt >= 0.6 * target_s or S == T:
                 break
             S = min(T, max(S + 1, int(S * target_s / max(dt, 1e-3))))
-    return dict(value=S / dt, unit="tokens/s", cores=1, kind="oracle",
-                sample=f"first {S} of {T} tokens of the {cfg['name']} batch through all "
-                       f"{cfg['n_layers']} layers, fp64 numpy oracle, 1 BLAS thread, "
-                       f"{dt:.1f} s; tokens are independent so tokens/s scales to the batch")
+    scale = N / n_l
+    layers = f"all {N} layers" if n_l == N else \
+        f"layers 0-{n_l - 1} of {N} (fp64 weights of the whole stack exceed " \
+        f"{max_f64_bytes / 1e9:.0f} GB; time scaled by {scale:g})"
+    return dict(value=S / (dt * scale), unit="tokens/s", cores=1, kind="oracle",
+                sample=f"first {S} of {T} tokens of the {cfg['name']} batch through "
+                       f"{layers}, fp64 numpy oracle, 1 BLAS thread, {dt:.1f} s timed; "
+                       f"tokens are independent so tokens/s scales to the batch")
 
 
 def main():
@@ -168,46 +199,57 @@ def main():
 
     from paper_2608_00573_amd import abi
     from synthgen import make_inputs, workload
+    from synthgen.inputs import make_tokens
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     cfg = workload(args.workload)
+    decode = "decode_steps" in cfg
+    K = args.steps if args.steps is not None else (cfg["decode_steps"] if decode else 20)
+    W = args.warmup
     t_gen = time.perf_counter()
     inp = make_inputs(cfg, device=dev)
+    T, N = cfg["n_tokens"], cfg["n_layers"]
+    # one token batch per step for decode (fresh tokens, seeds base + s), else
+    # the one batch every step
+    if decode:
+        batches = [make_tokens(cfg, cfg["token_seed_base"] + s, dev) for s in range(K)]
+    else:
+        batches = [inp["h0"].to(dev)]
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
-    T, N = cfg["n_tokens"], cfg["n_layers"]
     mh = abi.model_handle(cfg, inp["layers"])
     policy = abi.make_policy(**inp["policy"])
     ws = abi.alloc_workspace(mh.model, T, dev)
-    h0 = inp["h0"].to(dev)
-    K, W = args.steps, args.warmup
-    states = [abi.StateBuffers(h0.clone()) for _ in range(K + W)]
+    nb = len(batches)
+    states = [abi.StateBuffers(batches[i % nb].clone()) for i in range(K + W)]
     stream = torch.cuda.current_stream()
 
     # warmup, then the timed region (inputs resident, no host sync inside)
     for i in range(W):
-        abi.trimmoe_stack_forward(mh.model, policy, states[i].state, None, ws)
+        abi.trimmoe_stack_forward(mh.model, policy, states[K + i].state, None, ws)
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     e0.record(stream)
-    for i in range(W, W + K):
+    for i in range(K):
         abi.trimmoe_stack_forward(mh.model, policy, states[i].state, None, ws)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_total = e0.elapsed_time(e1)
     ms_step = ms_total / K
+    del states
 
     # per-kernel-class timing: HIP events on the same stream, same work
-    per = len(abi.TIMED_CLASSES) + 1
+    classes = list(abi.TIMED_CLASSES)
+    per = len(classes) + 1
     events = [torch.cuda.Event(enable_timing=True) for _ in range(N * per)]
     for e in events:
         e.record(stream)
     class_ms = np.zeros((N, per - 1))
     for i in range(K):
-        st = abi.StateBuffers(h0.clone())
+        st = abi.StateBuffers(batches[i % nb].clone())
         abi.trimmoe_stack_forward_timed(mh.model, policy, st.state, None, ws, events)
         torch.cuda.synchronize()
         for l in range(N):
@@ -215,33 +257,45 @@ def main():
                 class_ms[l, c] += events[l * per + c].elapsed_time(events[l * per + c + 1])
     class_ms /= K
 
-    # one traced step for the per-layer counts of the algorithmic work
-    st = abi.StateBuffers(h0.clone())
-    tr = abi.TraceBuffers(N, T, cfg["top_k"], dev)
-    abi.trimmoe_stack_forward(mh.model, policy, st.state, tr.trace, ws)
-    torch.cuda.synchronize()
-    counters = tr.counters.cpu().numpy()
-    work = algorithmic_work(cfg, counters)
+    # traced passes (one per distinct batch) for the algorithmic work
+    work_steps = []
+    for bt in batches:
+        st = abi.StateBuffers(bt.clone())
+        tr = abi.TraceBuffers(N, T, cfg["top_k"], dev)
+        abi.trimmoe_stack_forward(mh.model, policy, st.state, tr.trace, ws)
+        torch.cuda.synchronize()
+        work_steps.append(algorithmic_work(cfg, tr.counters.cpu().numpy()))
+    # per-step averages, per class and per layer
+    flop = {c: sum(w["flop"][c] for ws_ in work_steps for w in ws_) / nb for c in classes}
+    byts = {c: sum(w["bytes"][c] for ws_ in work_steps for w in ws_) / nb for c in classes}
 
     peak = PEAK_BF16_TFLOPS if cfg["dtype"] == "bf16" else PEAK_FP32_TFLOPS
-    ci = {n: i for i, n in enumerate(abi.TIMED_CLASSES)}
     t_class = class_ms.sum(axis=0)  # ms per step per class
-    flops = {"up": sum(w["flop_up"] for w in work), "down": sum(w["flop_down"] for w in work),
-             "exit": sum(w["flop_exit"] for w in work),
-             "shared": sum(w["flop_shared"] for w in work)}
-    launches = {"up": N, "down": N, "exit": N - 1, "shared": N if cfg["d_ff_shared"] else 0}
-    dom = max(("up", "down", "exit", "shared"), key=lambda c: t_class[ci[c]])
-    dom_ms = t_class[ci[dom]]
-    dom_tflops = flops[dom] / (dom_ms * 1e-3) / 1e12 if dom_ms > 0 else 0.0
-    gg_ms = t_class[ci["up"]] + t_class[ci["down"]]
-    gg_frac = (flops["up"] + flops["down"]) / (gg_ms * 1e-3) / 1e12 / peak if gg_ms else 0.0
-    stack_bound_ms = sum(max((w["flop_route"] + w["flop_up"] + w["flop_down"] +
-                              w["flop_shared"] + w["flop_exit"]) / (peak * 1e12),
-                             w["bytes"] / (PEAK_HBM_GBS * 1e9)) for w in work) * 1e3
-    active_layers = sum(w["n_active"] for w in work)
-    dom_kernel = {"up": "k_ffn_mma", "down": "k_ffn_mma", "exit": "k_exit_mma",
-                  "shared": "k_ffn_mma"}[dom]
+    ci = {n: i for i, n in enumerate(classes)}
+    launches = {c: N for c in classes}
+    launches["exit"] = N - 1
+    launches["gate"] = N - 1
+    if not cfg["d_ff_shared"]:
+        launches["shared"] = 0
+    dom = max((c for c in classes if launches[c]), key=lambda c: t_class[ci[c]])
+    dom_s = t_class[ci[dom]] * 1e-3
+    mfma_bound = flop[dom] / (peak * 1e12) >= byts[dom] / (PEAK_HBM_GBS * 1e9)
+    dom_kernel = {"route": "k_route", "bucket": "k_bucket", "up": "k_ffn_mma",
+                  "down": "k_ffn_mma", "shared": "k_ffn_mma", "combine": "k_combine",
+                  "exit": "k_exit_mma", "gate": "k_exit_reduce"}[dom]
     traffic, traffic_src = counter_traffic(dom_kernel, cfg["name"])
+    if mfma_bound:
+        achieved, pk, unit = flop[dom] / dom_s / 1e12, peak, "TFLOP/s"
+    else:
+        achieved, pk, unit = byts[dom] / dom_s / 1e9, PEAK_HBM_GBS, "GB/s"
+    gg_s = (t_class[ci["up"]] + t_class[ci["down"]]) * 1e-3
+    gg_frac = (flop["up"] + flop["down"]) / gg_s / 1e12 / peak if gg_s else 0.0
+    gg_hbm = (byts["up"] + byts["down"]) / gg_s / 1e9 / PEAK_HBM_GBS if gg_s else 0.0
+    stack_bound_s = sum(max(sum(w["flop"].values()) / (peak * 1e12),
+                            sum(w["bytes"].values()) / (PEAK_HBM_GBS * 1e9))
+                        for ws_ in work_steps for w in ws_) / nb
+    active_layers = sum(w["n_active"] for ws_ in work_steps for w in ws_) / nb
+    step_bytes = sum(byts.values())
 
     out = {
         "metric": METRIC,
@@ -259,32 +313,44 @@ def main():
         "config": {"workload": cfg["name"], "n_layers": N, "d_model": cfg["d_model"],
                    "experts": cfg["n_experts"], "top_k": cfg["top_k"], "d_ff": cfg["d_ff"],
                    "d_ff_shared": cfg["d_ff_shared"], "vocab_exit": cfg["vocab_exit"],
-                   "tokens_per_step": T, "parallelism": "single-gpu"},
+                   "tokens_per_step": T, "fresh_batch_per_step": decode,
+                   "parallelism": "single-gpu"},
         "roofline": {
-            "kernel": {"up": "k_ffn_mma (grouped up/gate + activation)",
+            "kernel": {"route": "k_subst + k_route (route, substitution, skip)",
+                       "bucket": "k_scan + k_bucket (bucketing)",
+                       "up": "k_ffn_mma (grouped up/gate + activation)",
                        "down": "k_ffn_mma (grouped down)",
+                       "shared": "k_ffn_mma (shared expert)",
+                       "combine": "k_combine (weighted combine)",
                        "exit": "k_exit_mma (exit head + softmax partials)",
-                       "shared": "k_ffn_mma (shared expert)"}[dom],
-            "bound": "mfma",
-            "achieved": dom_tflops,
-            "peak": peak,
-            "unit": "TFLOP/s",
-            "frac": dom_tflops / peak,
+                       "gate": "k_exit_reduce + k_compact (exit gate)"}[dom],
+            "bound": "mfma" if mfma_bound else "hbm",
+            "achieved": achieved,
+            "peak": pk,
+            "unit": unit,
+            "frac": achieved / pk,
             "traffic": traffic,
             "traffic_unit": "bytes per launch",
             "traffic_source": traffic_src,
-            "avg_launch_ms": dom_ms / launches[dom] if launches[dom] else None,
-            "algorithmic_flop_per_step": flops[dom],
+            "avg_launch_ms": t_class[ci[dom]] / launches[dom],
+            "algorithmic_flop_per_launch": flop[dom] / launches[dom],
+            "algorithmic_bytes_per_launch": byts[dom] / launches[dom],
         },
         "grouped_gemm_mfma_frac": gg_frac,
+        "grouped_gemm_hbm_frac": gg_hbm,
+        "class_hbm_frac": {c: (byts[c] / (t_class[ci[c]] * 1e-3) / 1e9 / PEAK_HBM_GBS
+                               if t_class[ci[c]] > 0 else 0.0) for c in classes},
+        "step_algorithmic_gb_per_s": step_bytes / (ms_step * 1e-3) / 1e9,
         "active_token_layers_per_s": active_layers * K / (ms_total * 1e-3),
-        "stack_roofline_frac": stack_bound_ms / ms_step,
-        "kernel_ms_per_step": {n: float(t_class[i]) for i, n in enumerate(abi.TIMED_CLASSES)},
-        "per_layer": [{k: w[k] for k in ("n_active", "n_exec", "rows", "distinct")} for w in work],
+        "stack_roofline_frac": stack_bound_s / (ms_step * 1e-3),
+        "kernel_ms_per_step": {n: float(t_class[i]) for i, n in enumerate(classes)},
+        "per_layer": [{k: w[k] for k in ("n_active", "n_exec", "rows", "distinct")}
+                      for w in work_steps[0]],
         "wall_s_timed_region": wall,
         "input_generation_s": t_gen,
     }
     if not args.no_cpu_baseline:
+        inp["h0"] = batches[0]
         out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 

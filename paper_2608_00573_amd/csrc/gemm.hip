@@ -275,6 +275,168 @@ __device__ __forceinline__ int acc_col(int wn, int j, int lane) {
   return wn * T::WN + j * 32 + (lane & 31);
 }
 
+// ------------------------------------------------ direct-to-LDS pipeline --
+// gfx950's global_load_lds_dwordx4 moves a wavefront's 64 x 16 bytes from
+// global memory straight into LDS at a wave-uniform base (lane l at base +
+// 16 l): no staging VGPRs and no ds_write, which is what the register-staged
+// core above spends most of its non-MFMA issue time on.  Three LDS stages
+// form a ring: slice g+2 is in flight while slice g is computed and slice
+// g+1 has landed.  Lane l of the DMA that covers tile rows r..r+7 loads row
+// r + l/8, chunk (l % 8) ^ swz(row), so the LDS image is the same swizzled
+// layout the fragment reads expect.
+//
+// Waits are explicit.  The compiler cannot tell that a DMA into one stage
+// does not alias a read of another, and would wait for every outstanding DMA
+// before each fragment read; the fragment reads are therefore inline-asm
+// ds_read_b128, and
+//   * lgkm_wait<N> (s_waitcnt lgkmcnt(N)) takes the fragments as in/out
+//     operands, so the MFMAs that use them cannot be scheduled above it;
+//   * slice_barrier<N> (s_waitcnt vmcnt(N) lgkmcnt(0); s_barrier) ends a
+//     slice: this wave's DMAs older than the last N have landed and its
+//     fragment reads are done, and after the barrier the same holds for all
+//     waves, so the next stage may be read and the oldest one rewritten.
+// Only LDS DMAs and rare stores are outstanding vector-memory operations in
+// these loops; extra newer operations only make a vmcnt wait stricter.
+typedef __attribute__((address_space(3))) char lds_char;
+
+__device__ __forceinline__ void dma16(const bf16_t* g, char* l) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)(g),
+                                   (lds_char*)(l), 16, 0, 0);
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const char* p) {
+  return (uint32_t)(uintptr_t)(const lds_char*)(p);
+}
+
+__device__ __forceinline__ bf16x8_t lds_read(uint32_t a) {
+  bf16x8_t v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(a));
+  return v;
+}
+
+// the four 32 x 16 fragments one wavefront multiplies per k-step: two A
+// fragments (rows +0, +32) and two B fragments (columns +0, +32 of one
+// operand, or the same columns of two operands)
+struct Frag4 {
+  bf16x8_t a0, a1, b0, b1;
+};
+
+template <int N>
+__device__ __forceinline__ void lgkm_wait(Frag4& f) {
+  asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(f.a0), "+v"(f.a1), "+v"(f.b0), "+v"(f.b1) : "n"(N));
+}
+
+template <int N>
+__device__ __forceinline__ void slice_barrier(Frag4& f) {
+  asm volatile("s_waitcnt vmcnt(%4) lgkmcnt(0)\n\ts_barrier"
+               : "+v"(f.a0), "+v"(f.a1), "+v"(f.b0), "+v"(f.b1) : "n"(N) : "memory");
+}
+
+// barrier for plain LDS traffic that leaves the DMA stream in flight
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <class T>
+struct DmaTile {
+  static_assert(T::TM == 2 && T::TN * T::NB == 2, "Frag4 holds 2 x 2 fragments per k-step");
+  static constexpr int NDMA = T::A_PT + T::B_PT * T::NB;  // DMAs per thread per slice
+  static constexpr int LDS = 3 * T::STAGE;
+  static_assert(LDS + 8 * 1024 <= 160 * 1024, "three stages plus epilogue scratch");
+};
+
+// per-lane global sources of one tile: A rows, then B0 rows (then B1 rows)
+template <class T>
+struct DPtrs {
+  const bf16_t* a[T::A_PT];
+  const bf16_t* b[T::B_PT * T::NB];
+};
+
+template <class T>
+__device__ __forceinline__ void make_dptrs(DPtrs<T>& q, const CoreArgs& c) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < T::A_PT; ++i) {
+    const int row = (t >> 3) + T::ROWS_PER_PASS * i;
+    const int r = min(row, c.a_valid - 1);
+    const int src = c.a_idx ? c.a_idx[r] : c.a_row0 + r;
+    q.a[i] = c.A + (size_t)src * c.K + c.k_begin + 8 * ((t & 7) ^ swz(row));
+  }
+#pragma unroll
+  for (int i = 0; i < T::B_PT; ++i) {
+    const int row = (t >> 3) + T::ROWS_PER_PASS * i;
+    const int r = min(row, c.b_valid - 1);
+    const size_t off = (size_t)(c.b_idx ? c.b_idx[r] : c.b_row0 + r) * c.K + c.k_begin +
+                       8 * ((t & 7) ^ swz(row));
+    q.b[i] = c.B0 + off;
+    if constexpr (T::NB == 2) q.b[T::B_PT + i] = c.B1 + off;
+  }
+}
+
+// DMA slice kt of the tile into stage st
+template <class T>
+__device__ __forceinline__ void dma_slice(char* st, const DPtrs<T>& q, int kt) {
+  const int w = threadIdx.x >> 6;
+  const int o = kt * BK;
+#pragma unroll
+  for (int i = 0; i < T::A_PT; ++i) dma16(q.a[i] + o, st + (T::ROWS_PER_PASS * i + 8 * w) * 128);
+#pragma unroll
+  for (int i = 0; i < T::B_PT * T::NB; ++i)
+    dma16(q.b[i] + o, st + T::A_BYTES + (i / T::B_PT) * T::B_BYTES +
+                          (T::ROWS_PER_PASS * (i % T::B_PT) + 8 * w) * 128);
+}
+
+// per-lane LDS offsets of a wavefront's fragments within a stage
+template <class T>
+struct FragAddr {
+  uint32_t a, b, ch[4];
+  __device__ __forceinline__ FragAddr(int wm, int wn, int lane) {
+    const int fr = lane & 31, hi = lane >> 5;
+    a = (wm * T::WM + fr) * 128;
+    b = T::A_BYTES + (wn * T::WN + fr) * 128;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) ch[ks] = ((2 * ks + hi) ^ swz(fr)) << 4;
+  }
+  __device__ __forceinline__ void read(Frag4& f, uint32_t stage, int ks) const {
+    constexpr uint32_t kB1 = T::NB == 2 ? T::B_BYTES : 32 * 128;
+    const uint32_t pa = stage + a + ch[ks], pb = stage + b + ch[ks];
+    f.a0 = lds_read(pa);
+    f.a1 = lds_read(pa + 32 * 128);
+    f.b0 = lds_read(pb);
+    f.b1 = lds_read(pb + kB1);
+  }
+};
+
+// acc[i][j] += A_i B_j^T for the k-step held in f
+__device__ __forceinline__ void mma4(const Frag4& f, f32x16_t (&acc)[2][2]) {
+  acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a0, f.b0, acc[0][0], 0, 0, 0);
+  acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a0, f.b1, acc[0][1], 0, 0, 0);
+  acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a1, f.b0, acc[1][0], 0, 0, 0);
+  acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a1, f.b1, acc[1][1], 0, 0, 0);
+}
+
+// One slice from stage cur (its k-step-0 fragments already in f0), with the
+// next slice's k-step-0 fragments read from stage nxt under the last
+// k-step's MFMAs.  `issue` starts the DMA of the slice two ahead.
+template <class T, class Issue>
+__device__ __forceinline__ void dma_slice_mma(const FragAddr<T>& fa, uint32_t cur, uint32_t nxt,
+                                              Frag4& f0, Frag4& f1, f32x16_t (&acc)[2][2],
+                                              Issue issue) {
+  issue();
+  fa.read(f1, cur, 1);
+  lgkm_wait<4>(f0);
+  mma4(f0, acc);
+  fa.read(f0, cur, 2);
+  lgkm_wait<4>(f1);
+  mma4(f1, acc);
+  fa.read(f1, cur, 3);
+  lgkm_wait<4>(f0);
+  mma4(f0, acc);
+  slice_barrier<DmaTile<T>::NDMA>(f1);
+  fa.read(f0, nxt, 0);
+  mma4(f1, acc);
+}
+
 // ------------------------------------------------------ grouped FFN GEMMs --
 // Rows come in expert groups; tile list entry = (expert, row begin, row end).
 // Dense mode (shared expert): one group, rows [0, *dense_rows).
@@ -391,26 +553,8 @@ struct ExitSched {
   }
 };
 
-// load slice g of the block's stream (clamped to the last one) into rr,
-// switching the row pointers when the stream enters a new tile
-__device__ __forceinline__ void exit_load(Regs<ExitTile>& rr, int g, int G, Ptrs<ExitTile>& q,
-                                          int& lt, const ExitSched& S, const ExitArgs& a) {
-  using T = ExitTile;
-  g = min(g, G - 1);
-  const int j = g / S.nk;
-  if (j != lt) {
-    int mt, nt;
-    S.decode(j, mt, nt);
-    const CoreArgs c{a.W, a.H, nullptr, nullptr, nullptr, mt * T::BM, nt * T::BN,
-                     min(T::BM, a.V - mt * T::BM), min(T::BN, S.n_x - nt * T::BN), a.K, 0, S.nk};
-    make_ptrs<T>(q, c);
-    lt = j;
-  }
-  gload<T>(rr, q, g - j * S.nk);
-}
-
 __device__ __forceinline__ void exit_epilogue(int j, const ExitSched& S, const ExitArgs& a,
-                                              f32x16_t (&acc)[ExitTile::TM][ExitTile::TN],
+                                              f32x16_t (&acc)[2][2],
                                               float2 (&s_part)[ExitTile::GM][ExitTile::BN]) {
   using T = ExitTile;
   int mt, nt;
@@ -461,7 +605,7 @@ __device__ __forceinline__ void exit_epilogue(int j, const ExitSched& S, const E
     sum += __shfl_xor(sum, 32);
     if (lane < 32) s_part[wm][acc_col<T>(wn, jj, lane)] = make_float2(m, sum);
   }
-  __syncthreads();
+  lds_barrier();
   const int c = threadIdx.x;
   if (c < b_valid) {
     float M = s_part[0][c].x;
@@ -482,12 +626,9 @@ __device__ __forceinline__ void exit_epilogue(int j, const ExitSched& S, const E
     for (int jj = 0; jj < T::TN; ++jj) acc[i][jj] = z;
 }
 
-// EVEN: K / BK is even, so every tile ends on the second slice of a pair and
-// only one copy of the epilogue is needed in the loop body
-template <bool EVEN>
 __global__ __launch_bounds__(ExitTile::THREADS) void k_exit_mma(ExitArgs a) {
   using T = ExitTile;
-  TRIMMOE_STAGES(T);
+  __shared__ __align__(16) char lds[DmaTile<T>::LDS];
   __shared__ float2 s_part[T::GM][T::BN];  // per wavefront row: (max, sum) per token column
   const int n_x = *a.n_exec;
   ExitSched S;
@@ -509,34 +650,52 @@ __global__ __launch_bounds__(ExitTile::THREADS) void k_exit_mma(ExitArgs a) {
   const int nk = S.nk, G = ntiles * nk;
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int wm = wave / T::GN, wn = wave % T::GN;
-  f32x16_t acc[T::TM][T::TN], unused[T::TM][T::TN];
+  const FragAddr<T> fa(wave / T::GN, wave % T::GN, lane);
+  const uint32_t st0 = lds_addr(lds);
+  f32x16_t acc[2][2];
   const f32x16_t z = {};
-#pragma unroll
-  for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-    for (int jj = 0; jj < T::TN; ++jj) acc[i][jj] = z;
-  Ptrs<T> qp;
-  int lt = -1;
-  Regs<T> r0, r1;
-  exit_load(r0, 0, G, qp, lt, S, a);
-  exit_load(r1, 1, G, qp, lt, S, a);
-  sstore<T>(lds_buf0, r0);
-  __syncthreads();
-  exit_load(r0, 2, G, qp, lt, S, a);
-  for (int gc = 0; gc < G; gc += 2) {
-    mma_slice<T>(lds_buf0, lds_buf1, r1, wm, wn, lane, acc, unused);  // slice gc; store gc + 1
-    if (!EVEN && gc % nk == nk - 1) exit_epilogue(gc / nk, S, a, acc, s_part);
-    __syncthreads();
-    exit_load(r1, gc + 3, G, qp, lt, S, a);
-    if (EVEN || gc + 1 < G) {
-      mma_slice<T>(lds_buf1, lds_buf0, r0, wm, wn, lane, acc, unused);  // store gc + 2
-      if ((gc + 1) % nk == nk - 1) exit_epilogue((gc + 1) / nk, S, a, acc, s_part);
-    } else {
-      sstore<T>(lds_buf0, r0);
+  acc[0][0] = acc[0][1] = acc[1][0] = acc[1][1] = z;
+
+  // DMA stream: next slice to issue is slice dk of tile dj; past the end the
+  // last slice is issued again (in bounds, never read)
+  DPtrs<T> qp;
+  int dj = 0, dk = 0, lt = -1;
+  auto issue = [&](int stage) {
+    if (dj != lt) {
+      int mt, nt;
+      S.decode(dj, mt, nt);
+      const CoreArgs c{a.W, a.H, nullptr, nullptr, nullptr, mt * T::BM, nt * T::BN,
+                       min(T::BM, a.V - mt * T::BM), min(T::BN, S.n_x - nt * T::BN), a.K, 0, nk};
+      make_dptrs<T>(qp, c);
+      lt = dj;
     }
-    __syncthreads();
-    exit_load(r0, gc + 4, G, qp, lt, S, a);
+    dma_slice<T>(lds + stage * T::STAGE, qp, dk);
+    if (++dk == nk) {
+      if (dj + 1 < ntiles) {
+        ++dj;
+        dk = 0;
+      } else {
+        dk = nk - 1;
+      }
+    }
+  };
+
+  Frag4 f0, f1;
+  issue(0);
+  issue(1);
+  slice_barrier<DmaTile<T>::NDMA>(f1);
+  fa.read(f0, st0, 0);
+  int sx = 0, kk = 0, j = 0;  // stage, slice within the tile, tile of the compute stream
+  for (int g = 0; g < G; ++g) {
+    const int sn = sx == 2 ? 0 : sx + 1, sp = sn == 2 ? 0 : sn + 1;
+    dma_slice_mma<T>(fa, st0 + sx * T::STAGE, st0 + sn * T::STAGE, f0, f1, acc,
+                     [&] { issue(sp); });
+    if (++kk == nk) {
+      exit_epilogue(j, S, a, acc, s_part);
+      kk = 0;
+      ++j;
+    }
+    sx = sn;
   }
 }
 
@@ -706,10 +865,7 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
     // persistent: one block per CU (at most one tile per block in the worst case)
     const int max_tiles = p.n_vtiles * cdiv(p.T, ExitTile::BN);
     const dim3 grid(min(max_tiles, p.n_cu));
-    if ((p.d / BK) % 2 == 0)
-      hipLaunchKernelGGL(k_exit_mma<true>, grid, dim3(ExitTile::THREADS), 0, st, a);
-    else
-      hipLaunchKernelGGL(k_exit_mma<false>, grid, dim3(ExitTile::THREADS), 0, st, a);
+    hipLaunchKernelGGL(k_exit_mma, grid, dim3(ExitTile::THREADS), 0, st, a);
   } else {
     const dim3 grid(p.n_vtiles * cdiv(p.T, FT));
     hipLaunchKernelGGL(k_exit_f32, grid, dim3(256), 0, st, static_cast<const float*>(p.w_exit),
