@@ -10,16 +10,16 @@
 //
 // bf16 path.  Both operands are K-contiguous ("NT"): A is [M, K], B is
 // [N, K], C = A B^T, fp32 accumulation in v_mfma_f32_32x32x16_bf16.  A block
-// is 4 wavefronts in a 2x2 grid; K advances in 64-wide slices (one 128-byte
-// row segment per operand row).  Each thread stages its 16-byte pieces of a
-// slice in registers; two register sets and two LDS buffers keep the global
-// loads of slices kt+1 and kt+2 in flight while the MFMAs consume slice kt,
-// and the compiler only waits for the one older set it is about to store.
-// In LDS a row segment keeps its eight 16-byte chunks XOR-swizzled by
-// (row & 7), so 8 consecutive rows' 16-byte fragment reads (and the
-// 128-byte row writes) hit distinct banks.  Rows past the valid range load a
-// clamped valid row (never stored).  Block ids are remapped so that each XCD
-// works on a contiguous run of tiles taken in 8-tile-tall column patches.
+// is 8 wavefronts; each owns a 64 x 64 output patch (or 64 x 32 of two B
+// operands) and multiplies two A by two B fragments per 16-wide k-step.  K
+// advances in 64-wide slices (one 128-byte row segment per operand row)
+// that gfx950's direct-to-LDS loads bring into a three-stage LDS ring two
+// slices ahead.  In LDS a row segment keeps its eight 16-byte chunks
+// XOR-swizzled by (row & 7) ^ ((row >> 3) & 1), so the fragment reads of 8
+// consecutive rows hit distinct banks.  Rows past the valid range load a
+// clamped valid row (their results are never stored).  Grids are persistent
+// (one block per CU); each block streams the K slices of its tiles
+// back to back, tiles taken from its XCD's contiguous range in patch order.
 //
 // fp32 path: plain FMA kernels for fp32 models.
 #include <math.h>
@@ -30,37 +30,14 @@ namespace trimmoe {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int BK = kGemmBK;  // 64 bf16 = one 128-byte row segment
-constexpr int kPatch = 8;    // tiles per patch column in the block order
+constexpr int kPatch = 8;    // M-tiles per patch column in the tile order
 constexpr int kXcd = 8;      // XCDs of an MI355X; blocks are dealt round-robin
 
 static_assert(BK == 64, "the LDS layout assumes 128-byte row segments");
 
-// -------------------------------------------------- block order remapping --
-// Hardware deals block b to XCD b % 8.  Give XCD x the contiguous logical
-// range [x*q + min(x, r), ...) of the `total` live tiles (a bijection on
-// [0, total)), then read the logical index in patch order: kPatch M-tiles of
-// one N-tile, then the next N-tile; the K split (if any) is the slowest index.
-__device__ __forceinline__ bool map_tile(int b, int n_mt, int n_nt, int n_split, int& mt, int& nt,
-                                         int& sp) {
-  const int per = n_mt * n_nt, total = per * n_split;
-  if (b >= total) return false;
-  const int q = total / kXcd, r = total % kXcd;
-  const int x = b % kXcd, i = b / kXcd;
-  int L = x * q + min(x, r) + i;
-  sp = L / per;
-  L -= sp * per;
-  const int span = kPatch * n_nt;
-  const int g = L / span, w = L % span;
-  const int gm = min(kPatch, n_mt - g * kPatch);
-  nt = w / gm;
-  mt = g * kPatch + w % gm;
-  return true;
-}
-
-// ---------------------------------------------------------- pipelined core --
+// ------------------------------------------------------------ tile shapes --
 // BM x BN block tile, NB B operands sharing A, GM x GN wavefronts
 template <int BM_, int BN_, int NB_, int GM_, int GN_>
 struct Tile {
@@ -70,200 +47,15 @@ struct Tile {
   static constexpr int TM = WM / 32, TN = WN / 32;  // MFMA tiles per wavefront
   static constexpr int A_BYTES = BM * 128, B_BYTES = BN * 128;
   static constexpr int STAGE = A_BYTES + NB * B_BYTES;
-  static constexpr int LDS = 2 * STAGE;
   static constexpr int ROWS_PER_PASS = THREADS / 8;  // 8 threads per 128-byte row
   static constexpr int A_PT = BM / ROWS_PER_PASS, B_PT = BN / ROWS_PER_PASS;
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wavefront tile");
   static_assert(BM % ROWS_PER_PASS == 0 && BN % ROWS_PER_PASS == 0, "load passes");
-  static_assert(LDS <= 160 * 1024, "LDS");
 };
-
-template <class T>
-struct Regs {
-  u32x4_t a[T::A_PT];
-  u32x4_t b0[T::B_PT];
-  u32x4_t b1[T::NB == 2 ? T::B_PT : 1];
-};
-
-// A / B* point at row 0 of their matrices.  Tile row r of A is matrix row
-// a_idx[r] (a gather through a token list) or a_row0 + r; likewise for B.
-struct CoreArgs {
-  const bf16_t* A;
-  const bf16_t* B0;
-  const bf16_t* B1;
-  const int* a_idx;
-  const int* b_idx;
-  int a_row0, b_row0;
-  int a_valid, b_valid, K, k_begin, nk;
-};
-
-// Per-thread source pointers: thread t loads chunk t%8 of tile rows
-// t/8 + i * ROWS_PER_PASS; rows past the valid range use the last valid row.
-template <class T>
-struct Ptrs {
-  const bf16_t* a[T::A_PT];
-  const bf16_t* b0[T::B_PT];
-  const bf16_t* b1[T::NB == 2 ? T::B_PT : 1];
-};
-
-template <class T>
-__device__ __forceinline__ void make_ptrs(Ptrs<T>& q, const CoreArgs& c) {
-  const int t = threadIdx.x;
-  const size_t col = (size_t)c.k_begin + 8 * (t & 7);
-#pragma unroll
-  for (int i = 0; i < T::A_PT; ++i) {
-    const int r = min((t >> 3) + T::ROWS_PER_PASS * i, c.a_valid - 1);
-    const int src = c.a_idx ? c.a_idx[r] : c.a_row0 + r;
-    q.a[i] = c.A + (size_t)src * c.K + col;
-  }
-#pragma unroll
-  for (int i = 0; i < T::B_PT; ++i) {
-    const int r = min((t >> 3) + T::ROWS_PER_PASS * i, c.b_valid - 1);
-    const int src = c.b_idx ? c.b_idx[r] : c.b_row0 + r;
-    q.b0[i] = c.B0 + (size_t)src * c.K + col;
-    if constexpr (T::NB == 2) q.b1[i] = c.B1 + (size_t)src * c.K + col;
-  }
-}
-
-template <class T>
-__device__ __forceinline__ void gload(Regs<T>& r, const Ptrs<T>& q, int kt) {
-  const int o = kt * BK;
-#pragma unroll
-  for (int i = 0; i < T::A_PT; ++i) r.a[i] = *reinterpret_cast<const u32x4_t*>(q.a[i] + o);
-#pragma unroll
-  for (int i = 0; i < T::B_PT; ++i) {
-    r.b0[i] = *reinterpret_cast<const u32x4_t*>(q.b0[i] + o);
-    if constexpr (T::NB == 2) r.b1[i] = *reinterpret_cast<const u32x4_t*>(q.b1[i] + o);
-  }
-}
 
 // 16-byte chunk c of row r sits at chunk c ^ swz(r): 8 consecutive rows, or
 // 16 consecutive rows split by parity, then touch distinct bank groups.
 __device__ __forceinline__ int swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
-
-template <class T>
-__device__ __forceinline__ void sstore(char* sb, const Regs<T>& r) {
-  const int t = threadIdx.x;
-#pragma unroll
-  for (int i = 0; i < T::A_PT; ++i) {
-    const int row = (t >> 3) + i * T::ROWS_PER_PASS;
-    *reinterpret_cast<u32x4_t*>(sb + row * 128 + (((t & 7) ^ swz(row)) << 4)) = r.a[i];
-  }
-#pragma unroll
-  for (int i = 0; i < T::B_PT; ++i) {
-    const int row = (t >> 3) + i * T::ROWS_PER_PASS;
-    const int off = row * 128 + (((t & 7) ^ swz(row)) << 4);
-    *reinterpret_cast<u32x4_t*>(sb + T::A_BYTES + off) = r.b0[i];
-    if constexpr (T::NB == 2) *reinterpret_cast<u32x4_t*>(sb + T::A_BYTES + T::B_BYTES + off) = r.b1[i];
-  }
-}
-
-// store piece p of register set r (A rows first, then B0, then B1) into LDS
-// stage sb, at the swizzled position sstore uses
-template <class T>
-__device__ __forceinline__ void sstore_piece(char* sb, const Regs<T>& r, int p) {
-  const int t = threadIdx.x;
-  if (p < T::A_PT) {
-    const int row = (t >> 3) + p * T::ROWS_PER_PASS;
-    *reinterpret_cast<u32x4_t*>(sb + row * 128 + (((t & 7) ^ swz(row)) << 4)) = r.a[p];
-    return;
-  }
-  p -= T::A_PT;
-  const int i = p % T::B_PT, which = p / T::B_PT;
-  const int row = (t >> 3) + i * T::ROWS_PER_PASS;
-  const int off = T::A_BYTES + which * T::B_BYTES + row * 128 + (((t & 7) ^ swz(row)) << 4);
-  if (which == 0) *reinterpret_cast<u32x4_t*>(sb + off) = r.b0[i];
-  else if constexpr (T::NB == 2) *reinterpret_cast<u32x4_t*>(sb + off) = r.b1[i];
-}
-
-// One BK slice from LDS stage sb.  Fragments for k-step ks+1 are read while
-// the MFMAs of k-step ks run, and the next slice's register set rn goes into
-// stage nxt, spread over the k-steps so that the LDS writes overlap
-// the MFMAs instead of stalling every wavefront at once; nxt was last read
-// before the previous barrier, so it is free.
-template <class T>
-__device__ __forceinline__ void mma_slice(const char* sb, char* nxt, const Regs<T>& rn,
-                                          int wm, int wn, int lane,
-                                          f32x16_t (&acc0)[T::TM][T::TN],
-                                          f32x16_t (&acc1)[T::TM][T::TN]) {
-  constexpr int KS = BK / 16;
-  constexpr int NP = T::A_PT + T::B_PT * T::NB;
-  const int fr = lane & 31, hi = lane >> 5;
-  const int sw = swz(fr);  // fragment rows are 32-aligned offsets plus fr
-  bf16x8_t a[2][T::TM], b0[2][T::TN], b1[2][T::NB == 2 ? T::TN : 1];
-  auto frag = [&](int ks, int buf) {
-    const int ch = ((2 * ks + hi) ^ sw) << 4;
-#pragma unroll
-    for (int i = 0; i < T::TM; ++i)
-      a[buf][i] = *reinterpret_cast<const bf16x8_t*>(sb + (wm * T::WM + i * 32 + fr) * 128 + ch);
-#pragma unroll
-    for (int j = 0; j < T::TN; ++j) {
-      const int o = T::A_BYTES + (wn * T::WN + j * 32 + fr) * 128 + ch;
-      b0[buf][j] = *reinterpret_cast<const bf16x8_t*>(sb + o);
-      if constexpr (T::NB == 2) b1[buf][j] = *reinterpret_cast<const bf16x8_t*>(sb + T::B_BYTES + o);
-    }
-  };
-  frag(0, 0);
-#pragma unroll
-  for (int ks = 0; ks < KS; ++ks) {
-    const int buf = ks & 1;
-    if (ks + 1 < KS) frag(ks + 1, buf ^ 1);
-#pragma unroll
-    for (int p = ks * NP / KS; p < (ks + 1) * NP / KS; ++p) sstore_piece<T>(nxt, rn, p);
-#pragma unroll
-    for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-      for (int j = 0; j < T::TN; ++j) {
-        acc0[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b0[buf][j], acc0[i][j], 0, 0, 0);
-        if constexpr (T::NB == 2)
-          acc1[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[buf][i], b1[buf][j], acc1[i][j], 0, 0, 0);
-      }
-  }
-}
-
-// acc0 = A B0^T, acc1 = A B1^T over c.nk slices starting at column c.k_begin.
-// Slice kt is computed from LDS buffer kt % 2 while register set (kt+1) % 2
-// holds slice kt+1 and set kt % 2 receives slice kt+2.  Every refill load is
-// issued unconditionally (past the end it re-reads the last slice, unused),
-// so the compiler's load counting stays exact and each LDS store waits only
-// for its own, older register set.
-template <class T>
-__device__ __forceinline__ void gemm_core(char* lds0, char* lds1, const CoreArgs& c,
-                                          f32x16_t (&acc0)[T::TM][T::TN],
-                                          f32x16_t (&acc1)[T::TM][T::TN]) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int wm = wave / T::GN, wn = wave % T::GN;
-  const f32x16_t z = {};
-#pragma unroll
-  for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-    for (int j = 0; j < T::TN; ++j) {
-      acc0[i][j] = z;
-      if constexpr (T::NB == 2) acc1[i][j] = z;
-    }
-  Ptrs<T> q;
-  make_ptrs<T>(q, c);
-  Regs<T> r0, r1;
-  const int nk = c.nk, last = c.nk - 1;
-  gload<T>(r0, q, 0);
-  gload<T>(r1, q, min(1, last));
-  sstore<T>(lds0, r0);
-  __syncthreads();
-  gload<T>(r0, q, min(2, last));
-  for (int kt = 0; kt < nk; kt += 2) {
-    mma_slice<T>(lds0, lds1, r1, wm, wn, lane, acc0, acc1);  // slice kt; store kt + 1
-    __syncthreads();
-    gload<T>(r1, q, min(kt + 3, last));
-    if (kt + 1 < nk) mma_slice<T>(lds1, lds0, r0, wm, wn, lane, acc0, acc1);
-    else sstore<T>(lds0, r0);                                        // slice kt + 2
-    __syncthreads();
-    gload<T>(r0, q, min(kt + 4, last));
-  }
-}
-
-#define TRIMMOE_STAGES(T)                               \
-  __shared__ __align__(16) char lds_buf0[T::STAGE];     \
-  __shared__ __align__(16) char lds_buf1[T::STAGE]
 
 // accumulator element -> tile-local (row, col)
 template <class T>
@@ -352,24 +144,29 @@ struct DPtrs {
   const bf16_t* b[T::B_PT * T::NB];
 };
 
+// tile row a thread's i-th A / B DMA covers, and the 16-byte chunk it loads
+__device__ __forceinline__ int dma_row(int i, int rows_per_pass) {
+  return ((int)threadIdx.x >> 3) + rows_per_pass * i;
+}
+__device__ __forceinline__ int dma_col(int row) { return 8 * (((int)threadIdx.x & 7) ^ swz(row)); }
+
+// A rows a_src[i] (matrix rows, already clamped) of A; B rows b_row0 + r,
+// r clamped to b_valid - 1, of B0 (and B1); K columns from k_begin
 template <class T>
-__device__ __forceinline__ void make_dptrs(DPtrs<T>& q, const CoreArgs& c) {
-  const int t = threadIdx.x;
+__device__ __forceinline__ void make_dptrs(DPtrs<T>& q, const bf16_t* A, const int (&a_src)[T::A_PT],
+                                           const bf16_t* B0, const bf16_t* B1, int b_row0,
+                                           int b_valid, int K, int k_begin) {
 #pragma unroll
   for (int i = 0; i < T::A_PT; ++i) {
-    const int row = (t >> 3) + T::ROWS_PER_PASS * i;
-    const int r = min(row, c.a_valid - 1);
-    const int src = c.a_idx ? c.a_idx[r] : c.a_row0 + r;
-    q.a[i] = c.A + (size_t)src * c.K + c.k_begin + 8 * ((t & 7) ^ swz(row));
+    const int row = dma_row(i, T::ROWS_PER_PASS);
+    q.a[i] = A + (size_t)a_src[i] * K + k_begin + dma_col(row);
   }
 #pragma unroll
   for (int i = 0; i < T::B_PT; ++i) {
-    const int row = (t >> 3) + T::ROWS_PER_PASS * i;
-    const int r = min(row, c.b_valid - 1);
-    const size_t off = (size_t)(c.b_idx ? c.b_idx[r] : c.b_row0 + r) * c.K + c.k_begin +
-                       8 * ((t & 7) ^ swz(row));
-    q.b[i] = c.B0 + off;
-    if constexpr (T::NB == 2) q.b[T::B_PT + i] = c.B1 + off;
+    const int row = dma_row(i, T::ROWS_PER_PASS);
+    const size_t off = (size_t)(b_row0 + min(row, b_valid - 1)) * K + k_begin + dma_col(row);
+    q.b[i] = B0 + off;
+    if constexpr (T::NB == 2) q.b[T::B_PT + i] = B1 + off;
   }
 }
 
@@ -437,9 +234,132 @@ __device__ __forceinline__ void dma_slice_mma(const FragAddr<T>& fa, uint32_t cu
   mma4(f1, acc);
 }
 
+// ------------------------------------------------------- tile scheduling --
+// Persistent grids: one block per CU (or fewer).  The live tiles (a count
+// known only on the device) are split into contiguous ranges, one per XCD
+// (hardware deals block b to XCD b % 8); block b walks tiles tb + i0,
+// tb + i0 + bx, ... of its XCD's range (bx = blocks on that XCD), so the
+// blocks of an XCD work on consecutive tiles and share its L2.  A tile index
+// is read in patch order: kPatch M-tiles of one N-tile, then the next
+// N-tile; the K split (if any) is the slowest index.
+struct TileSched {
+  int tb, i0, bx, n_mt, n_nt;
+  // false when this block has no tile, else its tile count in ntiles
+  __device__ __forceinline__ bool init(int n_mt_, int n_nt_, int n_split, int& ntiles) {
+    n_mt = n_mt_;
+    n_nt = n_nt_;
+    const int total = n_mt * n_nt * n_split;
+    const int nx = min(kXcd, (int)gridDim.x);  // fewer groups for a small grid
+    const int x = blockIdx.x % nx;
+    i0 = blockIdx.x / nx;
+    bx = ((int)gridDim.x - x + nx - 1) / nx;
+    const int q = total / nx, r = total % nx;
+    tb = x * q + min(x, r);
+    const int te = tb + q + (x < r ? 1 : 0);
+    if (tb + i0 >= te) return false;
+    ntiles = (te - (tb + i0) + bx - 1) / bx;
+    return true;
+  }
+  __device__ __forceinline__ void decode(int j, int& mt, int& nt, int& sp) const {
+    int L = tb + i0 + j * bx;
+    const int per = n_mt * n_nt;
+    sp = L / per;
+    L -= sp * per;
+    const int span = kPatch * n_nt;
+    const int g = L / span, w = L % span;
+    const int gm = min(kPatch, n_mt - g * kPatch);
+    nt = w / gm;
+    mt = g * kPatch + w % gm;
+  }
+};
+
+// A persistent block's GEMM over its ntiles tiles of nk slices each: one
+// continuous stream of K slices through the DMA ring, so the next tile's
+// first slices are in flight while the current tile's epilogue runs.
+// Src supplies, for tile j of the block:
+//   Desc desc(int j)                      descriptor (may load from memory);
+//                                         Desc::pick(c, x, y) = c ? x : y
+//   void rows(const Desc&, int (&)[A_PT]) per-thread A source rows (may load)
+//   void ptrs(DPtrs<T>&, const Desc&, const int (&)[A_PT])
+//   void epilogue(const Desc&, f32x16_t (&)[2][2])
+// Descriptors are loaded two tiles and rows one tile ahead of their use, so
+// the compiler's load-count waits for them never drain the DMA ring.
+template <class T, class Src>
+__device__ __forceinline__ void dma_gemm_stream(char* lds, int ntiles, int nk, const Src& src) {
+  using Desc = typename Src::Desc;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const FragAddr<T> fa(wave / T::GN, wave % T::GN, lane);
+  const uint32_t st0 = lds_addr(lds);
+  f32x16_t acc[2][2];
+  const f32x16_t z = {};
+  acc[0][0] = acc[0][1] = acc[1][0] = acc[1][1] = z;
+
+  // DMA side: slice dk of tile dj through pointers qp; n1 / n2 describe
+  // tiles dj+1 / dj+2 and rn1 holds the A rows of dj+1
+  const int last = ntiles - 1;
+  DPtrs<T> qp;
+  int rows[T::A_PT], rn1[T::A_PT];
+  Desc c0 = src.desc(0);
+  src.rows(c0, rows);
+  src.ptrs(qp, c0, rows);
+  Desc n1 = src.desc(min(1, last));
+  src.rows(n1, rn1);
+  Desc n2 = src.desc(min(2, last));
+  int dj = 0, dk = 0;
+  // compute side: c0 describes tile jc; c1 / c2 tiles jc+1 / jc+2 once the
+  // DMA side has entered them (it runs at most two slices ahead)
+  Desc c1 = n1, c2 = n2;
+  int jc = 0;
+  // the DMA side enters a tile when it issues the tile's first slice, at
+  // most two slices ahead of the compute side, so dj - jc is 1 or 2 then
+  auto issue = [&](int stage) {
+    if (dk == nk) {
+      if (dj == last) {  // past the end: the last slice again (in bounds, never read)
+        dk = nk - 1;
+      } else {
+        ++dj;
+        dk = 0;
+        src.ptrs(qp, n1, rn1);
+        const bool next = dj == jc + 1;  // field-wise selects: no indexed copy
+        c1 = Desc::pick(next, n1, c1);
+        c2 = Desc::pick(next, c2, n1);
+        src.rows(n2, rn1);
+        n1 = n2;
+        n2 = src.desc(min(dj + 2, last));
+      }
+    }
+    dma_slice<T>(lds + stage * T::STAGE, qp, dk);
+    ++dk;
+  };
+
+  Frag4 f0, f1;
+  issue(0);
+  issue(1);
+  slice_barrier<DmaTile<T>::NDMA>(f1);
+  fa.read(f0, st0, 0);
+  const int G = ntiles * nk;
+  int sx = 0, kk = 0;  // stage of the slice being computed, its index in the tile
+  for (int g = 0; g < G; ++g) {
+    const int sn = sx == 2 ? 0 : sx + 1, sp = sn == 2 ? 0 : sn + 1;
+    dma_slice_mma<T>(fa, st0 + sx * T::STAGE, st0 + sn * T::STAGE, f0, f1, acc,
+                     [&] { issue(sp); });
+    if (++kk == nk) {
+      src.epilogue(c0, acc);
+      acc[0][0] = acc[0][1] = acc[1][0] = acc[1][1] = z;
+      c0 = c1;
+      c1 = c2;
+      ++jc;
+      kk = 0;
+    }
+    sx = sn;
+  }
+}
+
 // ------------------------------------------------------ grouped FFN GEMMs --
-// Rows come in expert groups; tile list entry = (expert, row begin, row end).
-// Dense mode (shared expert): one group, rows [0, *dense_rows).
+// Row tiles come from the device tile list (expert, first row, end row) of
+// the expert-sorted rows, or (dense mode, shared expert) cover the first
+// *dense_rows rows.  A rows are gathered through x_idx (the token whose h
+// row feeds each sorted row) when it is set.
 struct FfnArgs {
   const bf16_t* X;        // [rows, K], or h [T, K] when x_idx is set
   const int* x_idx;       // row -> source row of X (gather), or NULL
@@ -457,63 +377,87 @@ struct FfnArgs {
 };
 
 template <class T, bool UP>
-__global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
-  TRIMMOE_STAGES(T);
-  const int n_nt = (a.N + T::BN - 1) / T::BN;
-  const int n_mt = a.dense_rows ? (*a.dense_rows + T::BM - 1) / T::BM : *a.n_tiles;
-  int mt, ntile, sp;
-  if (!map_tile(blockIdx.x, n_mt, n_nt, a.n_split, mt, ntile, sp)) return;
-  int e, m0, m1;
-  if (a.dense_rows) {
-    e = 0;
-    m0 = mt * T::BM;
-    m1 = *a.dense_rows;
-  } else {
-    const int4 tl = a.tiles[mt];
-    e = tl.x;
-    m0 = tl.y;
-    m1 = tl.z;
-  }
-  const int n0 = ntile * T::BN;
-  const int a_valid = min(T::BM, m1 - m0);
-  const int b_valid = min(T::BN, a.N - n0);
-  const bf16_t* W0 = a.W0 + (size_t)e * a.w_stride + (size_t)n0 * a.K;
-  const bf16_t* W1 = T::NB == 2 ? a.W1 + (size_t)e * a.w_stride + (size_t)n0 * a.K : nullptr;
-  const int nk = (a.K / BK) / a.n_split;
-  f32x16_t acc0[T::TM][T::TN], acc1[T::TM][T::TN];
-  gemm_core<T>(lds_buf0, lds_buf1,
-               CoreArgs{a.X, W0, W1, a.x_idx ? a.x_idx + m0 : nullptr, nullptr, m0, 0, a_valid,
-                        b_valid, a.K, sp * nk * BK, nk},
-               acc0, acc1);
+struct FfnSrc {
+  struct Desc {
+    int e, m0, m1, nt, sp;
+    static __device__ __forceinline__ Desc pick(bool c, const Desc& x, const Desc& y) {
+      return Desc{c ? x.e : y.e, c ? x.m0 : y.m0, c ? x.m1 : y.m1, c ? x.nt : y.nt,
+                  c ? x.sp : y.sp};
+    }
+  };
+  const FfnArgs& a;
+  const TileSched& S;
+  int dense_m1;  // dense mode: live rows
+  int nk;
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / T::GN, wn = wave % T::GN;
+  __device__ __forceinline__ Desc desc(int j) const {
+    int mt, nt, sp;
+    S.decode(j, mt, nt, sp);
+    if (a.dense_rows) return Desc{0, mt * T::BM, dense_m1, nt, sp};
+    const int4 tl = a.tiles[mt];
+    return Desc{tl.x, tl.y, tl.z, nt, sp};
+  }
+  __device__ __forceinline__ void rows(const Desc& d, int (&src)[T::A_PT]) const {
 #pragma unroll
-  for (int i = 0; i < T::TM; ++i)
+    for (int i = 0; i < T::A_PT; ++i) {
+      const int r = d.m0 + min(dma_row(i, T::ROWS_PER_PASS), d.m1 - d.m0 - 1);
+      src[i] = a.x_idx ? a.x_idx[r] : r;
+    }
+  }
+  __device__ __forceinline__ void ptrs(DPtrs<T>& q, const Desc& d,
+                                       const int (&src)[T::A_PT]) const {
+    const size_t wo = (size_t)d.e * a.w_stride;
+    const int n0 = d.nt * T::BN;
+    make_dptrs<T>(q, a.X, src, a.W0 + wo, T::NB == 2 ? a.W1 + wo : nullptr, n0,
+                  min(T::BN, a.N - n0), a.K, d.sp * nk * BK);
+  }
+  __device__ __forceinline__ void epilogue(const Desc& d, f32x16_t (&acc)[2][2]) const {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave / T::GN, wn = wave % T::GN;
+    const int n0 = d.nt * T::BN;
+    const int a_valid = min(T::BM, d.m1 - d.m0);
+    const int b_valid = min(T::BN, a.N - n0);
 #pragma unroll
-    for (int j = 0; j < T::TN; ++j) {
-      const int col = acc_col<T>(wn, j, lane);
-      if (col >= b_valid) continue;
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = acc_row<T>(wm, i, r, lane);
-        if (row >= a_valid) continue;
-        const size_t o = (size_t)(m0 + row) * a.N + n0 + col;
-        if constexpr (UP) {
-          const float u = acc0[i][j][r];
-          float v;
-          if constexpr (T::NB == 2) {
-            const float g = acc1[i][j][r];
-            v = g / (1.f + expf(-g)) * u;  // silu(g) * u
+      for (int j = 0; j < 2 / T::NB; ++j) {
+        const int col = acc_col<T>(wn, j, lane);
+        if (col >= b_valid) continue;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = acc_row<T>(wm, i, r, lane);
+          if (row >= a_valid) continue;
+          const size_t o = (size_t)(d.m0 + row) * a.N + n0 + col;
+          if constexpr (UP) {
+            const float u = acc[i][j][r];
+            float v;
+            if constexpr (T::NB == 2) {
+              const float g = acc[i][1][r];  // gate, same column
+              v = g / (1.f + expf(-g)) * u;  // silu(g) * u
+            } else {
+              v = fmaxf(u, 0.f);
+            }
+            static_cast<bf16_t*>(a.out)[o] = f2bf(v);
           } else {
-            v = fmaxf(u, 0.f);
+            static_cast<float*>(a.out)[d.sp * a.split_stride + o] = acc[i][j][r];
           }
-          static_cast<bf16_t*>(a.out)[o] = f2bf(v);
-        } else {
-          static_cast<float*>(a.out)[sp * a.split_stride + o] = acc0[i][j][r];
         }
       }
-    }
+  }
+};
+
+template <class T, bool UP>
+__global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
+  __shared__ __align__(16) char lds[DmaTile<T>::LDS];
+  const int n_nt = (a.N + T::BN - 1) / T::BN;
+  const int dense_m1 = a.dense_rows ? *a.dense_rows : 0;
+  const int n_mt = a.dense_rows ? (dense_m1 + T::BM - 1) / T::BM : *a.n_tiles;
+  TileSched S;
+  int ntiles;
+  if (!S.init(n_mt, n_nt, a.n_split, ntiles)) return;
+  const int nk = (a.K / BK) / a.n_split;
+  const FfnSrc<T, UP> src{a, S, dense_m1, nk};
+  dma_gemm_stream<T>(lds, ntiles, nk, src);
 }
 
 // ----------------------------------------------------------- exit head --
@@ -522,13 +466,6 @@ __global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
 // Epilogue: for every token column, max and sum exp over the tile's
 // vocabulary rows (bias added), written as one partial per vocabulary tile
 // as (max z * log2 e, sum exp(z - max z)).
-//
-// Persistent: the grid has one block per CU; block b walks the tiles
-// tb + i0, tb + i0 + bx, ... of its XCD's contiguous tile range (bx = blocks
-// on that XCD), so the bx blocks of an XCD work on bx consecutive tiles of
-// the patch order at any time.  Its K slices form one continuous load
-// stream across tiles: the first slices of the next tile are already in
-// flight while the current tile's epilogue runs.
 struct ExitArgs {
   const bf16_t* W;    // [V, K]
   const bf16_t* H;    // [n_x, K]
@@ -540,163 +477,108 @@ struct ExitArgs {
 
 using ExitTile = Tile<kExitTileBF16, 128, 1, 4, 2>;
 
-struct ExitSched {
-  int tb, i0, bx, n_mt, n_nt, n_x, nk;
-  // tile j of this block -> vocabulary tile mt, token tile nt (patch order)
-  __device__ __forceinline__ void decode(int j, int& mt, int& nt) const {
-    const int L = tb + i0 + j * bx;
-    const int span = kPatch * n_nt;
-    const int g = L / span, w = L % span;
-    const int gm = min(kPatch, n_mt - g * kPatch);
-    nt = w / gm;
-    mt = g * kPatch + w % gm;
+struct ExitSrc {
+  using T = ExitTile;
+  struct Desc {
+    int mt, nt;
+    static __device__ __forceinline__ Desc pick(bool c, const Desc& x, const Desc& y) {
+      return Desc{c ? x.mt : y.mt, c ? x.nt : y.nt};
+    }
+  };
+  const ExitArgs& a;
+  const TileSched& S;
+  int n_x;
+  float2 (*s_part)[T::BN];  // [GM][BN] LDS exchange of the epilogue
+
+  __device__ __forceinline__ Desc desc(int j) const {
+    int mt, nt, sp;
+    S.decode(j, mt, nt, sp);
+    return Desc{mt, nt};
+  }
+  __device__ __forceinline__ void rows(const Desc& d, int (&src)[T::A_PT]) const {
+    const int v0 = d.mt * T::BM, a_valid = min(T::BM, a.V - v0);
+#pragma unroll
+    for (int i = 0; i < T::A_PT; ++i) src[i] = v0 + min(dma_row(i, T::ROWS_PER_PASS), a_valid - 1);
+  }
+  __device__ __forceinline__ void ptrs(DPtrs<T>& q, const Desc& d,
+                                       const int (&src)[T::A_PT]) const {
+    const int j0 = d.nt * T::BN;
+    make_dptrs<T>(q, a.W, src, a.H, nullptr, j0, min(T::BN, n_x - j0), a.K, 0);
+  }
+  __device__ __forceinline__ void epilogue(const Desc& d, f32x16_t (&acc)[2][2]) const {
+    const int v0 = d.mt * T::BM, j0 = d.nt * T::BN;
+    const int a_valid = min(T::BM, a.V - v0);
+    const int b_valid = min(T::BN, n_x - j0);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave / T::GN, wn = wave % T::GN;
+    // partials in base 2: y = z * log2(e), so exp(z - max z) = exp2(y - max y)
+    // is one FMA and one v_exp_f32 per logit; the pair stored is (max y, sum)
+    const float ninf = -__builtin_inff();
+    const float kLog2e = 1.4426950408889634f;
+    const bool full = a_valid == T::BM && !a.bias;
+#pragma unroll
+    for (int jj = 0; jj < T::TN; ++jj) {
+      float m = ninf;
+      if (full) {
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float y = acc[i][jj][r] * kLog2e;
+            acc[i][jj][r] = y;
+            m = fmaxf(m, y);
+          }
+      } else {
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = acc_row<T>(wm, i, r, lane);
+            float y = acc[i][jj][r];
+            if (a.bias) y += a.bias[v0 + min(row, a_valid - 1)];
+            y = row < a_valid ? y * kLog2e : ninf;
+            acc[i][jj][r] = y;
+            m = fmaxf(m, y);
+          }
+      }
+      m = fmaxf(m, __shfl_xor(m, 32));
+      float sum = 0.f;
+      if (m != ninf) {
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(acc[i][jj][r] - m);
+      }
+      sum += __shfl_xor(sum, 32);
+      if (lane < 32) s_part[wm][acc_col<T>(wn, jj, lane)] = make_float2(m, sum);
+    }
+    lds_barrier();
+    const int c = threadIdx.x;
+    if (c < b_valid) {
+      float M = s_part[0][c].x;
+#pragma unroll
+      for (int g = 1; g < T::GM; ++g) M = fmaxf(M, s_part[g][c].x);
+      float S2 = 0.f;
+#pragma unroll
+      for (int g = 0; g < T::GM; ++g) {
+        const float2 v = s_part[g][c];
+        if (v.y > 0.f) S2 += v.y * __builtin_amdgcn_exp2f(v.x - M);
+      }
+      a.partials[(size_t)(j0 + c) * a.n_vtiles + d.mt] = make_float2(M, S2);
+    }
   }
 };
-
-__device__ __forceinline__ void exit_epilogue(int j, const ExitSched& S, const ExitArgs& a,
-                                              f32x16_t (&acc)[2][2],
-                                              float2 (&s_part)[ExitTile::GM][ExitTile::BN]) {
-  using T = ExitTile;
-  int mt, nt;
-  S.decode(j, mt, nt);
-  const int v0 = mt * T::BM, j0 = nt * T::BN;
-  const int a_valid = min(T::BM, a.V - v0);
-  const int b_valid = min(T::BN, S.n_x - j0);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave / T::GN, wn = wave % T::GN;
-  // partials in base 2: y = z * log2(e), so exp(z - max z) = exp2(y - max y)
-  // is one FMA and one v_exp_f32 per logit; the pair stored is (max y, sum)
-  const float ninf = -__builtin_inff();
-  const float kLog2e = 1.4426950408889634f;
-  const bool full = a_valid == T::BM && !a.bias;
-#pragma unroll
-  for (int jj = 0; jj < T::TN; ++jj) {
-    float m = ninf;
-    if (full) {
-#pragma unroll
-      for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float y = acc[i][jj][r] * kLog2e;
-          acc[i][jj][r] = y;
-          m = fmaxf(m, y);
-        }
-    } else {
-#pragma unroll
-      for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = acc_row<T>(wm, i, r, lane);
-          float y = acc[i][jj][r];
-          if (a.bias) y += a.bias[v0 + min(row, a_valid - 1)];
-          y = row < a_valid ? y * kLog2e : ninf;
-          acc[i][jj][r] = y;
-          m = fmaxf(m, y);
-        }
-    }
-    m = fmaxf(m, __shfl_xor(m, 32));
-    float sum = 0.f;
-    if (m != ninf) {
-#pragma unroll
-      for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(acc[i][jj][r] - m);
-    }
-    sum += __shfl_xor(sum, 32);
-    if (lane < 32) s_part[wm][acc_col<T>(wn, jj, lane)] = make_float2(m, sum);
-  }
-  lds_barrier();
-  const int c = threadIdx.x;
-  if (c < b_valid) {
-    float M = s_part[0][c].x;
-#pragma unroll
-    for (int g = 1; g < T::GM; ++g) M = fmaxf(M, s_part[g][c].x);
-    float S2 = 0.f;
-#pragma unroll
-    for (int g = 0; g < T::GM; ++g) {
-      const float2 v = s_part[g][c];
-      if (v.y > 0.f) S2 += v.y * __builtin_amdgcn_exp2f(v.x - M);
-    }
-    a.partials[(size_t)(j0 + c) * a.n_vtiles + mt] = make_float2(M, S2);
-  }
-  const f32x16_t z = {};
-#pragma unroll
-  for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-    for (int jj = 0; jj < T::TN; ++jj) acc[i][jj] = z;
-}
 
 __global__ __launch_bounds__(ExitTile::THREADS) void k_exit_mma(ExitArgs a) {
   using T = ExitTile;
   __shared__ __align__(16) char lds[DmaTile<T>::LDS];
   __shared__ float2 s_part[T::GM][T::BN];  // per wavefront row: (max, sum) per token column
   const int n_x = *a.n_exec;
-  ExitSched S;
-  S.n_mt = a.n_vtiles;
-  S.n_nt = (n_x + T::BN - 1) / T::BN;
-  S.n_x = n_x;
-  S.nk = a.K / BK;
-  const int total = S.n_mt * S.n_nt;
-  // XCD groups (fewer when the grid is smaller than the XCD count)
-  const int nx = min(kXcd, (int)gridDim.x);
-  const int x = blockIdx.x % nx;
-  S.i0 = blockIdx.x / nx;
-  S.bx = ((int)gridDim.x - x + nx - 1) / nx;
-  const int q = total / nx, r = total % nx;
-  S.tb = x * q + min(x, r);
-  const int te = S.tb + q + (x < r ? 1 : 0);
-  if (S.tb + S.i0 >= te) return;
-  const int ntiles = (te - (S.tb + S.i0) + S.bx - 1) / S.bx;
-  const int nk = S.nk, G = ntiles * nk;
-
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const FragAddr<T> fa(wave / T::GN, wave % T::GN, lane);
-  const uint32_t st0 = lds_addr(lds);
-  f32x16_t acc[2][2];
-  const f32x16_t z = {};
-  acc[0][0] = acc[0][1] = acc[1][0] = acc[1][1] = z;
-
-  // DMA stream: next slice to issue is slice dk of tile dj; past the end the
-  // last slice is issued again (in bounds, never read)
-  DPtrs<T> qp;
-  int dj = 0, dk = 0, lt = -1;
-  auto issue = [&](int stage) {
-    if (dj != lt) {
-      int mt, nt;
-      S.decode(dj, mt, nt);
-      const CoreArgs c{a.W, a.H, nullptr, nullptr, nullptr, mt * T::BM, nt * T::BN,
-                       min(T::BM, a.V - mt * T::BM), min(T::BN, S.n_x - nt * T::BN), a.K, 0, nk};
-      make_dptrs<T>(qp, c);
-      lt = dj;
-    }
-    dma_slice<T>(lds + stage * T::STAGE, qp, dk);
-    if (++dk == nk) {
-      if (dj + 1 < ntiles) {
-        ++dj;
-        dk = 0;
-      } else {
-        dk = nk - 1;
-      }
-    }
-  };
-
-  Frag4 f0, f1;
-  issue(0);
-  issue(1);
-  slice_barrier<DmaTile<T>::NDMA>(f1);
-  fa.read(f0, st0, 0);
-  int sx = 0, kk = 0, j = 0;  // stage, slice within the tile, tile of the compute stream
-  for (int g = 0; g < G; ++g) {
-    const int sn = sx == 2 ? 0 : sx + 1, sp = sn == 2 ? 0 : sn + 1;
-    dma_slice_mma<T>(fa, st0 + sx * T::STAGE, st0 + sn * T::STAGE, f0, f1, acc,
-                     [&] { issue(sp); });
-    if (++kk == nk) {
-      exit_epilogue(j, S, a, acc, s_part);
-      kk = 0;
-      ++j;
-    }
-    sx = sn;
-  }
+  TileSched S;
+  int ntiles;
+  if (!S.init(a.n_vtiles, (n_x + T::BN - 1) / T::BN, 1, ntiles)) return;
+  const ExitSrc src{a, S, n_x, s_part};
+  dma_gemm_stream<T>(lds, ntiles, a.K / BK, src);
 }
 
 // ------------------------------------------------------------- fp32 path --
@@ -784,9 +666,9 @@ static inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 // Tile shapes of the expert GEMMs (BM rows of an expert group x BN outputs)
 using UpDualTile = Tile<kGemmBM, 128, 2, 2, 4>;  // SwiGLU: up and gate share A
 using UpTile = Tile<kGemmBM, 256, 1, 2, 4>;      // ReLU
-using DownTile = Tile<kGemmBM, 128, 1, 2, 2>;
+using DownTile = Tile<kGemmBM, 256, 1, 2, 4>;
 
-// K splits of the routed down GEMM: enough blocks to cover the CUs twice,
+// K splits of the routed down GEMM: enough tiles to cover the CUs twice,
 // each split keeping at least 8 K slices.
 int down_splits(int max_tiles, int N, int K) {
   const int tiles = max_tiles * cdiv(N, DownTile::BN);
@@ -796,9 +678,10 @@ int down_splits(int max_tiles, int N, int K) {
   return s;
 }
 
+// persistent: at most one block per CU, none beyond the tile bound
 template <class T, bool UP>
-static void launch_ffn_mma(const FfnArgs& a, int max_mt, hipStream_t st) {
-  const dim3 grid(max_mt * cdiv(a.N, T::BN) * a.n_split);
+static void launch_ffn_mma(const FfnArgs& a, int max_mt, int n_cu, hipStream_t st) {
+  const dim3 grid(min(max_mt * cdiv(a.N, T::BN) * a.n_split, n_cu));
   hipLaunchKernelGGL((k_ffn_mma<T, UP>), grid, dim3(T::THREADS), 0, st, a);
 }
 
@@ -824,11 +707,11 @@ static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared
               static_cast<const bf16_t*>(w1), w_stride, K, N, p.tiles, &p.counts[kCntTiles],
               dense, out, p.y_split_stride, n_split, act};
     if (up && dual)
-      launch_ffn_mma<UpDualTile, true>(a, max_mt, st);
+      launch_ffn_mma<UpDualTile, true>(a, max_mt, p.n_cu, st);
     else if (up)
-      launch_ffn_mma<UpTile, true>(a, max_mt, st);
+      launch_ffn_mma<UpTile, true>(a, max_mt, p.n_cu, st);
     else
-      launch_ffn_mma<DownTile, false>(a, max_mt, st);
+      launch_ffn_mma<DownTile, false>(a, max_mt, p.n_cu, st);
   } else {
     const dim3 grid(max_mt * cdiv(N, FT));
     if (up)
@@ -862,7 +745,7 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
   if (bf16) {
     ExitArgs a{static_cast<const bf16_t*>(p.w_exit), static_cast<const bf16_t*>(p.hx), p.b_exit,
                &p.counts[kCntExec], p.V, p.d, p.n_vtiles, p.partials};
-    // persistent: one block per CU (at most one tile per block in the worst case)
+    // persistent: at most one block per CU, none beyond the tile bound
     const int max_tiles = p.n_vtiles * cdiv(p.T, ExitTile::BN);
     const dim3 grid(min(max_tiles, p.n_cu));
     hipLaunchKernelGGL(k_exit_mma, grid, dim3(ExitTile::THREADS), 0, st, a);
