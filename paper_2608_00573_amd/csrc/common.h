@@ -16,6 +16,8 @@ typedef uint16_t bf16_t;
 constexpr int kRouteTokens = 32;
 // rows of an expert group covered by one grouped-GEMM tile
 constexpr int kGemmBM = 128;
+// batches of this many tokens or more use the 256-token exit-head tile
+constexpr int kWideTokens = 6144;
 constexpr int kGemmBN = 128;
 constexpr int kGemmBK = 64;
 // vocabulary rows of one exit-head tile (bf16 MFMA path / fp32 path)

@@ -106,22 +106,34 @@ __device__ __forceinline__ bf16x8_t lds_read(uint32_t a) {
   return v;
 }
 
-// the four 32 x 16 fragments one wavefront multiplies per k-step: two A
-// fragments (rows +0, +32) and two B fragments (columns +0, +32 of one
-// operand, or the same columns of two operands)
-struct Frag4 {
-  bf16x8_t a0, a1, b0, b1;
+// one k-step's fragments of a wavefront: TM A fragments (rows +32 i) and
+// TN * NB B fragments (operand o, columns +32 j at index o * TN + j)
+template <class T>
+struct Frags {
+  bf16x8_t a[T::TM];
+  bf16x8_t b[T::TN * T::NB];
 };
 
-template <int N>
-__device__ __forceinline__ void lgkm_wait(Frag4& f) {
-  asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(f.a0), "+v"(f.a1), "+v"(f.b0), "+v"(f.b1) : "n"(N));
+// ties every fragment register to the asm statement just before it (volatile
+// asm keeps its order), so no MFMA reading one is scheduled above that wait
+template <class T>
+__device__ __forceinline__ void frags_after(Frags<T>& f) {
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i) asm volatile("" : "+v"(f.a[i]));
+#pragma unroll
+  for (int j = 0; j < T::TN * T::NB; ++j) asm volatile("" : "+v"(f.b[j]));
 }
 
-template <int N>
-__device__ __forceinline__ void slice_barrier(Frag4& f) {
-  asm volatile("s_waitcnt vmcnt(%4) lgkmcnt(0)\n\ts_barrier"
-               : "+v"(f.a0), "+v"(f.a1), "+v"(f.b0), "+v"(f.b1) : "n"(N) : "memory");
+template <int N, class T>
+__device__ __forceinline__ void lgkm_wait(Frags<T>& f) {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N));
+  frags_after(f);
+}
+
+template <int N, class T>
+__device__ __forceinline__ void slice_barrier(Frags<T>& f) {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+  frags_after(f);
 }
 
 // barrier for plain LDS traffic that leaves the DMA stream in flight
@@ -129,12 +141,17 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Ring depth: three stages (two slices in flight ahead of the one being
+// computed) when they fit next to 8 KB of epilogue scratch, else two.
 template <class T>
 struct DmaTile {
-  static_assert(T::TM == 2 && T::TN * T::NB == 2, "Frag4 holds 2 x 2 fragments per k-step");
+  static constexpr int NF = T::TM + T::TN * T::NB;        // fragment reads per k-step
   static constexpr int NDMA = T::A_PT + T::B_PT * T::NB;  // DMAs per thread per slice
-  static constexpr int LDS = 3 * T::STAGE;
-  static_assert(LDS + 8 * 1024 <= 160 * 1024, "three stages plus epilogue scratch");
+  static constexpr int STAGES = 3 * T::STAGE + 8 * 1024 <= 160 * 1024 ? 3 : 2;
+  static constexpr int DEPTH = STAGES - 1;                // slices issued ahead
+  static constexpr int LDS = STAGES * T::STAGE;
+  static_assert(LDS + 8 * 1024 <= 160 * 1024, "stages plus epilogue scratch");
+  static_assert(NF <= 15 && NDMA * (DEPTH - 1) <= 63, "waitcnt fields");
 };
 
 // per-lane global sources of one tile: A rows, then B0 rows (then B1 rows)
@@ -194,44 +211,52 @@ struct FragAddr {
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) ch[ks] = ((2 * ks + hi) ^ swz(fr)) << 4;
   }
-  __device__ __forceinline__ void read(Frag4& f, uint32_t stage, int ks) const {
-    constexpr uint32_t kB1 = T::NB == 2 ? T::B_BYTES : 32 * 128;
+  __device__ __forceinline__ void read(Frags<T>& f, uint32_t stage, int ks) const {
     const uint32_t pa = stage + a + ch[ks], pb = stage + b + ch[ks];
-    f.a0 = lds_read(pa);
-    f.a1 = lds_read(pa + 32 * 128);
-    f.b0 = lds_read(pb);
-    f.b1 = lds_read(pb + kB1);
+#pragma unroll
+    for (int i = 0; i < T::TM; ++i) f.a[i] = lds_read(pa + i * 32 * 128);
+#pragma unroll
+    for (int o = 0; o < T::NB; ++o)
+#pragma unroll
+      for (int j = 0; j < T::TN; ++j) f.b[o * T::TN + j] = lds_read(pb + o * T::B_BYTES + j * 32 * 128);
   }
 };
 
+template <class T>
+using Acc = f32x16_t[T::TM][T::TN * T::NB];
+
 // acc[i][j] += A_i B_j^T for the k-step held in f
-__device__ __forceinline__ void mma4(const Frag4& f, f32x16_t (&acc)[2][2]) {
-  acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a0, f.b0, acc[0][0], 0, 0, 0);
-  acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a0, f.b1, acc[0][1], 0, 0, 0);
-  acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a1, f.b0, acc[1][0], 0, 0, 0);
-  acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a1, f.b1, acc[1][1], 0, 0, 0);
+template <class T>
+__device__ __forceinline__ void mma_step(const Frags<T>& f, Acc<T>& acc) {
+#pragma unroll
+  for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::TN * T::NB; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
 }
 
 // One slice from stage cur (its k-step-0 fragments already in f0), with the
 // next slice's k-step-0 fragments read from stage nxt under the last
-// k-step's MFMAs.  `issue` starts the DMA of the slice two ahead.
+// k-step's MFMAs.  `issue` starts the DMA of the slice DEPTH ahead; the
+// barrier waits for the DMAs of the next slice only.
 template <class T, class Issue>
 __device__ __forceinline__ void dma_slice_mma(const FragAddr<T>& fa, uint32_t cur, uint32_t nxt,
-                                              Frag4& f0, Frag4& f1, f32x16_t (&acc)[2][2],
+                                              Frags<T>& f0, Frags<T>& f1, Acc<T>& acc,
                                               Issue issue) {
+  using D = DmaTile<T>;
   issue();
   fa.read(f1, cur, 1);
-  lgkm_wait<4>(f0);
-  mma4(f0, acc);
+  lgkm_wait<D::NF>(f0);
+  mma_step<T>(f0, acc);
   fa.read(f0, cur, 2);
-  lgkm_wait<4>(f1);
-  mma4(f1, acc);
+  lgkm_wait<D::NF>(f1);
+  mma_step<T>(f1, acc);
   fa.read(f1, cur, 3);
-  lgkm_wait<4>(f0);
-  mma4(f0, acc);
-  slice_barrier<DmaTile<T>::NDMA>(f1);
+  lgkm_wait<D::NF>(f0);
+  mma_step<T>(f0, acc);
+  slice_barrier<D::NDMA * (D::DEPTH - 1)>(f1);
   fa.read(f0, nxt, 0);
-  mma4(f1, acc);
+  mma_step<T>(f1, acc);
 }
 
 // ------------------------------------------------------- tile scheduling --
@@ -281,7 +306,7 @@ struct TileSched {
 //                                         Desc::pick(c, x, y) = c ? x : y
 //   void rows(const Desc&, int (&)[A_PT]) per-thread A source rows (may load)
 //   void ptrs(DPtrs<T>&, const Desc&, const int (&)[A_PT])
-//   void epilogue(const Desc&, f32x16_t (&)[2][2])
+//   void epilogue(const Desc&, Acc<T>&)
 // Descriptors are loaded two tiles and rows one tile ahead of their use, so
 // the compiler's load-count waits for them never drain the DMA ring.
 template <class T, class Src>
@@ -290,9 +315,16 @@ __device__ __forceinline__ void dma_gemm_stream(char* lds, int ntiles, int nk, c
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const FragAddr<T> fa(wave / T::GN, wave % T::GN, lane);
   const uint32_t st0 = lds_addr(lds);
-  f32x16_t acc[2][2];
+  using D = DmaTile<T>;
+  Acc<T> acc;
   const f32x16_t z = {};
-  acc[0][0] = acc[0][1] = acc[1][0] = acc[1][1] = z;
+  auto zero = [&] {
+#pragma unroll
+    for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < T::TN * T::NB; ++j) acc[i][j] = z;
+  };
+  zero();
 
   // DMA side: slice dk of tile dj through pointers qp; n1 / n2 describe
   // tiles dj+1 / dj+2 and rn1 holds the A rows of dj+1
@@ -307,11 +339,11 @@ __device__ __forceinline__ void dma_gemm_stream(char* lds, int ntiles, int nk, c
   Desc n2 = src.desc(min(2, last));
   int dj = 0, dk = 0;
   // compute side: c0 describes tile jc; c1 / c2 tiles jc+1 / jc+2 once the
-  // DMA side has entered them (it runs at most two slices ahead)
+  // DMA side has entered them (it runs at most DEPTH <= 2 slices ahead)
   Desc c1 = n1, c2 = n2;
   int jc = 0;
   // the DMA side enters a tile when it issues the tile's first slice, at
-  // most two slices ahead of the compute side, so dj - jc is 1 or 2 then
+  // most DEPTH <= 2 slices ahead of the compute side, so dj - jc is 1 or 2
   auto issue = [&](int stage) {
     if (dk == nk) {
       if (dj == last) {  // past the end: the last slice again (in bounds, never read)
@@ -332,20 +364,21 @@ __device__ __forceinline__ void dma_gemm_stream(char* lds, int ntiles, int nk, c
     ++dk;
   };
 
-  Frag4 f0, f1;
-  issue(0);
-  issue(1);
-  slice_barrier<DmaTile<T>::NDMA>(f1);
+  Frags<T> f0, f1;
+#pragma unroll
+  for (int s = 0; s < D::DEPTH; ++s) issue(s);
+  slice_barrier<D::NDMA * (D::DEPTH - 1)>(f1);
   fa.read(f0, st0, 0);
   const int G = ntiles * nk;
   int sx = 0, kk = 0;  // stage of the slice being computed, its index in the tile
   for (int g = 0; g < G; ++g) {
-    const int sn = sx == 2 ? 0 : sx + 1, sp = sn == 2 ? 0 : sn + 1;
+    const int sn = sx + 1 == D::STAGES ? 0 : sx + 1;
+    const int sp = (sx + D::DEPTH) % D::STAGES;  // stage of slice g + DEPTH
     dma_slice_mma<T>(fa, st0 + sx * T::STAGE, st0 + sn * T::STAGE, f0, f1, acc,
                      [&] { issue(sp); });
     if (++kk == nk) {
       src.epilogue(c0, acc);
-      acc[0][0] = acc[0][1] = acc[1][0] = acc[1][1] = z;
+      zero();
       c0 = c1;
       c1 = c2;
       ++jc;
@@ -411,16 +444,16 @@ struct FfnSrc {
     make_dptrs<T>(q, a.X, src, a.W0 + wo, T::NB == 2 ? a.W1 + wo : nullptr, n0,
                   min(T::BN, a.N - n0), a.K, d.sp * nk * BK);
   }
-  __device__ __forceinline__ void epilogue(const Desc& d, f32x16_t (&acc)[2][2]) const {
+  __device__ __forceinline__ void epilogue(const Desc& d, Acc<T>& acc) const {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wm = wave / T::GN, wn = wave % T::GN;
     const int n0 = d.nt * T::BN;
     const int a_valid = min(T::BM, d.m1 - d.m0);
     const int b_valid = min(T::BN, a.N - n0);
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-      for (int j = 0; j < 2 / T::NB; ++j) {
+      for (int j = 0; j < T::TN; ++j) {
         const int col = acc_col<T>(wn, j, lane);
         if (col >= b_valid) continue;
 #pragma unroll
@@ -432,8 +465,8 @@ struct FfnSrc {
             const float u = acc[i][j][r];
             float v;
             if constexpr (T::NB == 2) {
-              const float g = acc[i][1][r];  // gate, same column
-              v = g / (1.f + expf(-g)) * u;  // silu(g) * u
+              const float g = acc[i][T::TN + j][r];  // gate, same column
+              v = g / (1.f + expf(-g)) * u;          // silu(g) * u
             } else {
               v = fmaxf(u, 0.f);
             }
@@ -476,9 +509,13 @@ struct ExitArgs {
 };
 
 using ExitTile = Tile<kExitTileBF16, 128, 1, 4, 2>;
+// 256 tokens per tile for large batches: 2/3 of the DMA bytes per MFMA of the
+// 128-token tile, in a two-stage ring (the 128-token tile keeps three stages,
+// and its finer token tiles balance the persistent grid better at small n_x)
+using ExitWide = Tile<kExitTileBF16, 256, 1, 4, 2>;
 
+template <class T>
 struct ExitSrc {
-  using T = ExitTile;
   struct Desc {
     int mt, nt;
     static __device__ __forceinline__ Desc pick(bool c, const Desc& x, const Desc& y) {
@@ -505,7 +542,7 @@ struct ExitSrc {
     const int j0 = d.nt * T::BN;
     make_dptrs<T>(q, a.W, src, a.H, nullptr, j0, min(T::BN, n_x - j0), a.K, 0);
   }
-  __device__ __forceinline__ void epilogue(const Desc& d, f32x16_t (&acc)[2][2]) const {
+  __device__ __forceinline__ void epilogue(const Desc& d, Acc<T>& acc) const {
     const int v0 = d.mt * T::BM, j0 = d.nt * T::BN;
     const int a_valid = min(T::BM, a.V - v0);
     const int b_valid = min(T::BN, n_x - j0);
@@ -569,15 +606,15 @@ struct ExitSrc {
   }
 };
 
-__global__ __launch_bounds__(ExitTile::THREADS) void k_exit_mma(ExitArgs a) {
-  using T = ExitTile;
+template <class T>
+__global__ __launch_bounds__(T::THREADS) void k_exit_mma(ExitArgs a) {
   __shared__ __align__(16) char lds[DmaTile<T>::LDS];
   __shared__ float2 s_part[T::GM][T::BN];  // per wavefront row: (max, sum) per token column
   const int n_x = *a.n_exec;
   TileSched S;
   int ntiles;
   if (!S.init(a.n_vtiles, (n_x + T::BN - 1) / T::BN, 1, ntiles)) return;
-  const ExitSrc src{a, S, n_x, s_part};
+  const ExitSrc<T> src{a, S, n_x, s_part};
   dma_gemm_stream<T>(lds, ntiles, a.K / BK, src);
 }
 
@@ -663,7 +700,9 @@ __global__ __launch_bounds__(256) void k_exit_f32(const float* W, const float* H
 // ------------------------------------------------------------- launchers --
 static inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
-// Tile shapes of the expert GEMMs (BM rows of an expert group x BN outputs)
+// Tile shapes of the expert GEMMs (BM rows of an expert group x BN outputs).
+// Three-stage rings: the expert weights stream from HBM, and two slices in
+// flight measured faster than 256-row two-stage tiles even for large groups.
 using UpDualTile = Tile<kGemmBM, 128, 2, 2, 4>;  // SwiGLU: up and gate share A
 using UpTile = Tile<kGemmBM, 256, 1, 2, 4>;      // ReLU
 using DownTile = Tile<kGemmBM, 256, 1, 2, 4>;
@@ -746,9 +785,13 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
     ExitArgs a{static_cast<const bf16_t*>(p.w_exit), static_cast<const bf16_t*>(p.hx), p.b_exit,
                &p.counts[kCntExec], p.V, p.d, p.n_vtiles, p.partials};
     // persistent: at most one block per CU, none beyond the tile bound
-    const int max_tiles = p.n_vtiles * cdiv(p.T, ExitTile::BN);
-    const dim3 grid(min(max_tiles, p.n_cu));
-    hipLaunchKernelGGL(k_exit_mma, grid, dim3(ExitTile::THREADS), 0, st, a);
+    if (p.T >= kWideTokens) {
+      const dim3 grid(min(p.n_vtiles * cdiv(p.T, ExitWide::BN), p.n_cu));
+      hipLaunchKernelGGL(k_exit_mma<ExitWide>, grid, dim3(ExitWide::THREADS), 0, st, a);
+    } else {
+      const dim3 grid(min(p.n_vtiles * cdiv(p.T, ExitTile::BN), p.n_cu));
+      hipLaunchKernelGGL(k_exit_mma<ExitTile>, grid, dim3(ExitTile::THREADS), 0, st, a);
+    }
   } else {
     const dim3 grid(p.n_vtiles * cdiv(p.T, FT));
     hipLaunchKernelGGL(k_exit_f32, grid, dim3(256), 0, st, static_cast<const float*>(p.w_exit),

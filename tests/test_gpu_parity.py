@@ -44,6 +44,21 @@ def test_tiny_bf16_swiglu_top2_shared():
     _run_and_compare(cfg)
 
 
+def test_large_batch_swiglu_top2_shared():
+    # 6144 tokens: the 256-token exit-head tile; top-2 over 4 experts gives
+    # long, ragged expert groups
+    cfg = workload("tiny_fp32", dtype="bf16", act="swiglu", top_k=2, normalize_topk=1,
+                   n_tokens=6144, d_model=128, d_ff=256, n_experts=4, n_local=2,
+                   vocab_exit=2048, n_layers=3, d_ff_shared=256)
+    _run_and_compare(cfg)
+
+
+def test_large_batch_relu_top1():
+    cfg = workload("switch_base_8e", n_tokens=6500, n_layers=3, d_model=128, d_ff=384,
+                   n_experts=2, n_local=1, vocab_exit=1500)
+    _run_and_compare(cfg)
+
+
 def test_ragged_tokens_bf16_relu():
     # T not a multiple of any tile (route 32, GEMM 128)
     cfg = workload("switch_base_8e", n_tokens=333, n_layers=3, d_model=256, d_ff=512,
