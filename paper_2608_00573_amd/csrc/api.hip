@@ -97,8 +97,6 @@ size_t carve(const trimmoe_model* m, int T, char* base, LayerParams* p) {
   };
   LayerParams tmp;
   LayerParams& P = p ? *p : tmp;
-  P.sub_c = (int32_t*)take(E * 4);
-  P.sub_q = (float*)take(E * 4);
   P.tok_exec = (int32_t*)take(R * 4);
   P.tok_w = (float*)take(R * 4);
   P.tok_row = (int32_t*)take(R * 4);
@@ -219,7 +217,6 @@ int run_layer(const trimmoe_model* m, int l, const trimmoe_policy* pol, const tr
   if (ev) TRIMMOE_TRY(hipEventRecord(ev[i], st))
   TRIMMOE_MARK(0);
   if (any_trace(tr)) TRIMMOE_TRY(launch_trace_fill(P, st));
-  TRIMMOE_TRY(launch_subst(P, st));
   TRIMMOE_TRY(launch_route(P, bf16, st));
   TRIMMOE_MARK(TRIMMOE_CLASS_ROUTE + 1);
   TRIMMOE_TRY(launch_scan(P, st));

@@ -97,8 +97,6 @@ struct LayerParams {
   float* tr_d_acc;
   int32_t* tr_counters;
   // workspace
-  int32_t* sub_c;      // [E]
-  float* sub_q;        // [E]
   int32_t* tok_exec;   // [T*k] merged rows per active position, -1 padded
   float* tok_w;        // [T*k]
   int32_t* tok_row;    // [T*k] permuted row of each merged row
@@ -131,7 +129,6 @@ struct LayerParams {
 hipError_t launch_state_reset(const trimmoe_model* m, const trimmoe_state* s,
                               hipStream_t st);
 hipError_t launch_trace_fill(const LayerParams& p, hipStream_t st);
-hipError_t launch_subst(const LayerParams& p, hipStream_t st);
 hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_scan(const LayerParams& p, hipStream_t st);
 hipError_t launch_bucket(const LayerParams& p, hipStream_t st);

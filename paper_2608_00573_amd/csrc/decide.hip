@@ -63,36 +63,29 @@ __global__ void k_trace_fill(LayerParams p) {
   if (p.tr_d_acc) p.tr_d_acc[t] = qnan;
 }
 
-// ------------------------------------- Eq. (3): best local substitute c(e) --
-// c(e) = argmin over local j != e with Sim[e][j] >= sim_min of
-// Q(e, j) = min(1, phi_scale * (1 - Sim[e][j]) / 2), ties to the lower j.
-__global__ void k_subst(LayerParams p) {
-  int e = threadIdx.x;
-  if (e >= p.E) return;
-  int best = -1;
-  float bq = 0.f;
-  for (int j = 0; j < p.E; ++j) {
-    if (j == e || !p.local_mask[j]) continue;
-    float s = p.sim[(size_t)e * p.E + j];
-    if (!(s >= p.sim_min)) continue;
-    float q = fminf(1.f, p.phi_scale * (1.f - s) * 0.5f);
-    if (best < 0 || q < bq) {
-      best = j;
-      bq = q;
-    }
-  }
-  p.sub_c[e] = best;
-  p.sub_q[e] = bq;
+// ------------------------------------------- route + decide (one layer) --
+constexpr int kRouteWaves = 8;  // wavefronts of a route block
+
+// K splits of the router logits: enough (column tile, K range) items for the
+// wavefronts of a route block, each range a multiple of 32
+static __host__ __device__ inline int route_ks(int E, int d) {
+  const int nct = (E + 15) / 16;
+  int ks = 1;
+  while (nct * ks < kRouteWaves) ks *= 2;
+  while (ks > 1 && d % (32 * ks) != 0) ks /= 2;
+  return ks;
 }
 
-// ------------------------------------------- route + decide (one layer) --
-// One block = RB active tokens.  Phase 1: router logits into LDS (MFMA
-// 16x16x32 bf16 tiles, or fp32 FMA).  Phase 2: one thread per token runs
-// the decision.  Phase 3: per-block expert histogram for the bucketing.
+// One block = RB active tokens.  Phase 0: the layer's substitute table.
+// Phase 1: router logits into LDS (MFMA 16x16x32 bf16 tiles, or fp32 FMA).
+// Phase 2: one thread per token runs the decision.  Phase 3: per-block
+// expert histogram for the bucketing.
 template <bool BF16>
-__global__ __launch_bounds__(256) void k_route(LayerParams p) {
-  extern __shared__ float zs[];  // [RB][E] logits (+ [RB][E] second K half)
+__global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
+  extern __shared__ float zs[];  // [route_ks][RB][E] logits, K partial sums
   __shared__ int s_cnt[TRIMMOE_MAX_EXPERTS];
+  __shared__ int s_subc[TRIMMOE_MAX_EXPERTS];
+  __shared__ float s_subq[TRIMMOE_MAX_EXPERTS];
   __shared__ int s_xcnt;
   __shared__ int sS[RB][KMAX];
   __shared__ float sQ[RB][KMAX];
@@ -109,54 +102,102 @@ __global__ __launch_bounds__(256) void k_route(LayerParams p) {
   for (int e = threadIdx.x; e < E; e += blockDim.x) s_cnt[e] = 0;
   if (threadIdx.x == 0) s_xcnt = 0;
 
+  // Eq. (3): best local substitute c(e) = argmin over local j != e with
+  // Sim[e][j] >= sim_min of Q(e, j) = min(1, phi_scale (1 - Sim[e][j]) / 2),
+  // ties to the lower j (-1: none); Q of it in s_subq
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    int best = -1;
+    float bq = 0.f;
+    for (int j = 0; j < E; ++j) {
+      if (j == e || !p.local_mask[j]) continue;
+      const float sv = p.sim[(size_t)e * E + j];
+      if (!(sv >= p.sim_min)) continue;
+      const float q = fminf(1.f, p.phi_scale * (1.f - sv) * 0.5f);
+      if (best < 0 || q < bq) {
+        best = j;
+        bq = q;
+      }
+    }
+    s_subc[e] = best;
+    s_subq[e] = bq;
+  }
+
   if constexpr (BF16) {
-    // logits of RB tokens x E experts as 16x16 MFMA tiles (2 token tiles x
-    // ceil(E/16) expert tiles); with fewer tiles than wavefronts the K range
-    // is split in two and the halves are added in a fixed order.  Rows past
-    // the live tokens / experts load a clamped valid row (never stored).
+    // logits of RB = 32 tokens x E experts with 16x16x32 MFMAs: a wavefront
+    // takes one 16-expert column tile and one K range for both 16-token row
+    // tiles, so each expert row is read once per 32 tokens.  With few column
+    // tiles the K range is split (route_ks) so that all wavefronts work;
+    // the partial sums are added in K order.  The k-steps run in groups of
+    // four whose loads are issued one group ahead (clamped to the last group:
+    // in bounds, unused).  Rows past the live tokens / experts load a clamped
+    // valid row (never stored).
     const bf16_t* h = static_cast<const bf16_t*>(p.h);
     const bf16_t* W = static_cast<const bf16_t*>(p.w_router);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int nct = (E + 15) >> 4, ntile = 2 * nct;
-    const int ks = ntile >= 4 ? 1 : 2;
-    const int dk = d / ks;
-    float* part = zs + RB * E;
-    for (int w = wave; w < ntile * ks; w += 4) {
-      const int tile = w % ntile, kh = w / ntile;
-      const int rt = tile & 1, ct = tile >> 1;
-      const int tl = rt * 16 + (lane & 15);
-      const int t = p.active_idx[base + min(tl, nt - 1)];
-      const int e = ct * 16 + (lane & 15);
-      const bf16_t* hr = h + (size_t)t * d + kh * dk + 8 * (lane >> 4);
-      const bf16_t* wr = W + (size_t)min(e, E - 1) * d + kh * dk + 8 * (lane >> 4);
-      f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-      int k0 = 0;
-      for (; k0 + 128 <= dk; k0 += 128) {
-        bf16x8_t av[4], bv[4];
+    const int nct = (E + 15) >> 4, ks = route_ks(E, d), dk = d / ks;
+    const int tl = lane & 15, kl = 8 * (lane >> 4);
+    const int t0 = p.active_idx[base + min(tl, nt - 1)];
+    const int t1 = p.active_idx[base + min(16 + tl, nt - 1)];
+    for (int w = wave; w < nct * ks; w += kRouteWaves) {
+      const int ct = w % nct, kq = w / nct;
+      const int e = ct * 16 + tl;
+      const bf16_t* h0 = h + (size_t)t0 * d + kq * dk + kl;
+      const bf16_t* h1 = h + (size_t)t1 * d + kq * dk + kl;
+      const bf16_t* wr = W + (size_t)min(e, E - 1) * d + kq * dk + kl;
+      f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+      const int ng = dk / 128;  // full groups of four k-steps
+      if (ng > 0) {
+        bf16x8_t a0[4], a1[4], b[4], n0[4], n1[4], nb[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          av[u] = *reinterpret_cast<const bf16x8_t*>(hr + k0 + 32 * u);
-          bv[u] = *reinterpret_cast<const bf16x8_t*>(wr + k0 + 32 * u);
+          a0[u] = *reinterpret_cast<const bf16x8_t*>(h0 + 32 * u);
+          a1[u] = *reinterpret_cast<const bf16x8_t*>(h1 + 32 * u);
+          b[u] = *reinterpret_cast<const bf16x8_t*>(wr + 32 * u);
         }
+        for (int g = 0; g < ng; ++g) {
+          const int o = min(g + 1, ng - 1) * 128;
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u], bv[u], acc, 0, 0, 0);
+          for (int u = 0; u < 4; ++u) {
+            n0[u] = *reinterpret_cast<const bf16x8_t*>(h0 + o + 32 * u);
+            n1[u] = *reinterpret_cast<const bf16x8_t*>(h1 + o + 32 * u);
+            nb[u] = *reinterpret_cast<const bf16x8_t*>(wr + o + 32 * u);
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[u], b[u], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[u], b[u], acc1, 0, 0, 0);
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            a0[u] = n0[u];
+            a1[u] = n1[u];
+            b[u] = nb[u];
+          }
+        }
       }
-      for (; k0 < dk; k0 += 32)
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8_t*>(hr + k0),
-                                                      *reinterpret_cast<const bf16x8_t*>(wr + k0),
-                                                      acc, 0, 0, 0);
+      for (int k0 = ng * 128; k0 < dk; k0 += 32) {
+        const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(wr + k0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8_t*>(h0 + k0),
+                                                       bv, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8_t*>(h1 + k0),
+                                                       bv, acc1, 0, 0, 0);
+      }
       // accumulator: column = lane % 16 (expert), row = 4 * (lane / 16) + r (token)
-      float* dst = kh == 0 ? zs : part;
+      float* dst = zs + (size_t)kq * RB * E;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int row = rt * 16 + 4 * (lane >> 4) + r;
-        if (row < nt && e < E) dst[row * E + e] = acc[r];
+        const int row = 4 * (lane >> 4) + r;
+        if (e < E && row < nt) dst[row * E + e] = acc0[r];
+        if (e < E && 16 + row < nt) dst[(16 + row) * E + e] = acc1[r];
       }
     }
-    if (ks == 2) {
+    if (ks > 1) {
       __syncthreads();
-      for (int idx = threadIdx.x; idx < nt * E; idx += blockDim.x) zs[idx] = zs[idx] + part[idx];
+      for (int idx = threadIdx.x; idx < nt * E; idx += blockDim.x) {
+        float v = zs[idx];
+        for (int q = 1; q < ks; ++q) v += zs[(size_t)q * RB * E + idx];
+        zs[idx] = v;
+      }
     }
   } else {
     const float* h = static_cast<const float*>(p.h);
@@ -224,8 +265,8 @@ __global__ __launch_bounds__(256) void k_route(LayerParams p) {
         sQ[i][r] = 0.f;
       } else {
         ++n_rem;
-        const int c = p.sub_c[e];
-        sQ[i][r] = c >= 0 ? p.sub_q[e] : 0.f;
+        const int c = s_subc[e];
+        sQ[i][r] = c >= 0 ? s_subq[e] : 0.f;
         if (c >= 0) sRsub[i][nsub++] = r;
       }
     }
@@ -275,7 +316,7 @@ __global__ __launch_bounds__(256) void k_route(LayerParams p) {
       int x = -1, kind = TRIMMOE_KIND_NONE;
       if (!skip) {
         if ((bmask >> r) & 1) {
-          x = p.sub_c[e];
+          x = s_subc[e];
           kind = TRIMMOE_KIND_SUBST;
           ++nsubst;
         } else {
@@ -619,18 +660,13 @@ hipError_t launch_trace_fill(const LayerParams& p, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_subst(const LayerParams& p, hipStream_t st) {
-  hipLaunchKernelGGL(k_subst, dim3(1), dim3(256), 0, st, p);
-  return hipGetLastError();
-}
-
 hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st) {
   const int nb = cdiv(p.T, RB);
-  const size_t lds = 2 * (size_t)RB * p.E * sizeof(float);
+  const size_t lds = (size_t)(bf16 ? route_ks(p.E, p.d) : 1) * RB * p.E * sizeof(float);
   if (bf16)
-    hipLaunchKernelGGL(k_route<true>, dim3(nb), dim3(256), lds, st, p);
+    hipLaunchKernelGGL(k_route<true>, dim3(nb), dim3(64 * kRouteWaves), lds, st, p);
   else
-    hipLaunchKernelGGL(k_route<false>, dim3(nb), dim3(256), lds, st, p);
+    hipLaunchKernelGGL(k_route<false>, dim3(nb), dim3(64 * kRouteWaves), lds, st, p);
   return hipGetLastError();
 }
 

@@ -328,15 +328,16 @@ __device__ __forceinline__ void dma_gemm_stream(char* lds, int ntiles, int nk, c
 
   // DMA side: slice dk of tile dj through pointers qp; n1 / n2 describe
   // tiles dj+1 / dj+2 and rn1 holds the A rows of dj+1
+  // start-up: the three descriptor loads go out together, and the first
+  // slice's DMA right after tile 0's rows, before tile 1's rows are needed
   const int last = ntiles - 1;
   DPtrs<T> qp;
   int rows[T::A_PT], rn1[T::A_PT];
   Desc c0 = src.desc(0);
+  Desc n1 = src.desc(min(1, last));
+  Desc n2 = src.desc(min(2, last));
   src.rows(c0, rows);
   src.ptrs(qp, c0, rows);
-  Desc n1 = src.desc(min(1, last));
-  src.rows(n1, rn1);
-  Desc n2 = src.desc(min(2, last));
   int dj = 0, dk = 0;
   // compute side: c0 describes tile jc; c1 / c2 tiles jc+1 / jc+2 once the
   // DMA side has entered them (it runs at most DEPTH <= 2 slices ahead)
@@ -365,8 +366,10 @@ __device__ __forceinline__ void dma_gemm_stream(char* lds, int ntiles, int nk, c
   };
 
   Frags<T> f0, f1;
+  issue(0);
+  src.rows(n1, rn1);  // first needed when the stream enters tile 1
 #pragma unroll
-  for (int s = 0; s < D::DEPTH; ++s) issue(s);
+  for (int s = 1; s < D::DEPTH; ++s) issue(s);
   slice_barrier<D::NDMA * (D::DEPTH - 1)>(f1);
   fa.read(f0, st0, 0);
   const int G = ntiles * nk;
