@@ -59,6 +59,17 @@ def test_large_batch_relu_top1():
     _run_and_compare(cfg)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sigmoid_exit_head(dtype):
+    # the paper's own exit head: one logit w . h + b through a sigmoid
+    # (p_J = 0.99: the planted logits cross 4.6 at different depths)
+    cfg = workload("tiny_fp32", dtype=dtype, vocab_exit=1, conf_mode="sigmoid", n_layers=4,
+                   n_tokens=200, p_exit=0.99)
+    _, gst, gtr, _, _, _ = _run_and_compare(cfg)
+    exits = [(gst["exit_layer"] == l).sum() for l in range(cfg["n_layers"])]
+    assert sum(e > 0 for e in exits) >= 2
+
+
 def test_ragged_tokens_bf16_relu():
     # T not a multiple of any tile (route 32, GEMM 128)
     cfg = workload("switch_base_8e", n_tokens=333, n_layers=3, d_model=256, d_ff=512,
