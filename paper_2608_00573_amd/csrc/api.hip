@@ -12,6 +12,8 @@
 #include <math.h>
 #include <string.h>
 
+#include <algorithm>
+
 #include "common.h"
 
 using namespace trimmoe;
@@ -88,7 +90,7 @@ size_t carve(const trimmoe_model* m, int T, char* base, LayerParams* p) {
   const size_t R = (size_t)Tm * k;
   const int nblk = cdiv(Tm, kRouteTokens);
   const int max_tiles = (int)cdiv((int)R, kGemmBM) + E;
-  const int n_vtiles = bf16 ? cdiv(m->vocab_exit, kExitTileBF16) : cdiv(m->vocab_exit, kExitTileF32);
+  const int n_vtiles = cdiv(m->vocab_exit, exit_tile_rows(bf16, Tm));
   size_t off = 0;
   auto take = [&](size_t bytes) -> void* {
     void* q = base ? base + off : nullptr;
@@ -292,7 +294,12 @@ int trimmoe_workspace_size(const trimmoe_model* m, int32_t max_tokens, size_t* b
   int rc = validate_model(m);
   if (rc) return rc;
   if (max_tokens < 0) return TRIMMOE_ERR_SHAPE;
-  *bytes_out = carve(m, max_tokens, nullptr, nullptr);
+  // enough for every token count up to max_tokens: the carve grows with T
+  // except where small batches switch to finer exit-head vocabulary tiles
+  size_t bytes = carve(m, max_tokens, nullptr, nullptr);
+  if (max_tokens > kExitSmallTokens)
+    bytes = std::max(bytes, carve(m, kExitSmallTokens, nullptr, nullptr));
+  *bytes_out = bytes;
   return TRIMMOE_OK;
 }
 

@@ -20,9 +20,17 @@ constexpr int kGemmBM = 128;
 constexpr int kWideTokens = 6144;
 constexpr int kGemmBN = 128;
 constexpr int kGemmBK = 64;
-// vocabulary rows of one exit-head tile (bf16 MFMA path / fp32 path)
+// vocabulary rows of one exit-head tile (bf16 MFMA path / fp32 path); bf16
+// batches of kExitSmallTokens or fewer use kExitTileBF16Small-row tiles, so
+// that a decode-sized batch still spreads W_exit over every CU
 constexpr int kExitTileBF16 = 256;
+constexpr int kExitTileBF16Small = 128;
+constexpr int kExitSmallTokens = 64;
 constexpr int kExitTileF32 = 16;
+
+inline int exit_tile_rows(bool bf16, int T) {
+  return bf16 ? (T <= kExitSmallTokens ? kExitTileBF16Small : kExitTileBF16) : kExitTileF32;
+}
 // fp32 GEMM tile
 constexpr int kF32Tile = 16;
 

@@ -516,6 +516,10 @@ using ExitTile = Tile<kExitTileBF16, 128, 1, 4, 2>;
 // 128-token tile, in a two-stage ring (the 128-token tile keeps three stages,
 // and its finer token tiles balance the persistent grid better at small n_x)
 using ExitWide = Tile<kExitTileBF16, 256, 1, 4, 2>;
+// decode-sized batches (kExitSmallTokens or fewer): 32 token columns, 128
+// vocabulary rows, so the tiles cover the CUs and the MFMA work is not 4x
+// padding; W_exit streaming (HBM) bounds it
+using ExitSmall = Tile<kExitTileBF16Small, 32, 1, 4, 1>;
 
 template <class T>
 struct ExitSrc {
@@ -788,7 +792,10 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
     ExitArgs a{static_cast<const bf16_t*>(p.w_exit), static_cast<const bf16_t*>(p.hx), p.b_exit,
                &p.counts[kCntExec], p.V, p.d, p.n_vtiles, p.partials};
     // persistent: at most one block per CU, none beyond the tile bound
-    if (p.T >= kWideTokens) {
+    if (p.T <= kExitSmallTokens) {
+      const dim3 grid(min(p.n_vtiles * cdiv(p.T, ExitSmall::BN), p.n_cu));
+      hipLaunchKernelGGL(k_exit_mma<ExitSmall>, grid, dim3(ExitSmall::THREADS), 0, st, a);
+    } else if (p.T >= kWideTokens) {
       const dim3 grid(min(p.n_vtiles * cdiv(p.T, ExitWide::BN), p.n_cu));
       hipLaunchKernelGGL(k_exit_mma<ExitWide>, grid, dim3(ExitWide::THREADS), 0, st, a);
     } else {

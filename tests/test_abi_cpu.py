@@ -63,6 +63,15 @@ def test_workspace_size_grows_with_tokens():
     assert abi.trimmoe_workspace_size(mh.model, 0) > 0
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_workspace_size_covers_every_smaller_batch(dtype):
+    # a workspace sized for max_tokens serves any smaller batch, also across
+    # the switch to finer exit-head tiles for decode-sized batches
+    mh = _handle(dtype=dtype)
+    sizes = [abi.trimmoe_workspace_size(mh.model, t) for t in range(1, 200)]
+    assert all(x <= y for x, y in zip(sizes, sizes[1:]))
+
+
 @pytest.mark.parametrize("over,code", [
     (dict(top_k=9), -2), (dict(n_experts=257, top_k=2), -2), (dict(top_k=9, n_experts=8), -2),
     (dict(d_model=96), -2), (dict(d_ff=100), -2), (dict(n_layers=0), -2),
