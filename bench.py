@@ -19,7 +19,14 @@ one JSON line:
 * grouped_gemm_mfma_frac / grouped_gemm_hbm_frac: algorithmic FLOPs and
   weight bytes of the grouped up/gate and down GEMMs over their measured
   time, against the bf16 dense MFMA peak and the HBM bandwidth;
-* class_hbm_frac: algorithmic bytes over measured time for every class.
+* class_hbm_frac: algorithmic bytes over measured time for every class;
+* feedback (decode workload, or --feedback-window > 0): the same batches
+  once more, with the runtime feedback rules closing the loop after every
+  window of passes (observations on the GPU, Eq. (37) and Eq. (43) on the
+  host): the throughput of that loop and the trajectory of p_J and omega_T;
+  and the cost of the observations themselves (the same loop with zero step
+  sizes, so that the policy and the work stay those of the plain loop).
+  Not part of `value`.
 """
 from __future__ import annotations
 
@@ -49,6 +56,13 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--feedback-window", type=int, default=None,
+                    help="passes per runtime-feedback window (default: 16 for the decode "
+                         "workload, else off; 0 = off)")
+    ap.add_argument("--eta", type=float, default=0.2, help="step size of the p_J update")
+    ap.add_argument("--kappa", type=float, default=0.2,
+                    help="step size of the delay/quality weight update")
+    ap.add_argument("--p-floor", type=float, default=0.1, help="lower bound of p_J")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (to scale HBM byte "
                          "counters) and exit")
@@ -181,6 +195,42 @@ def cpu_baseline(inp, target_s, max_f64_bytes=24e9):
                 sample=f"first {S} of {T} tokens of the {cfg['name']} batch through "
                        f"{layers}, fp64 numpy oracle, 1 BLAS thread, {dt:.1f} s timed; "
                        f"tokens are independent so tokens/s scales to the batch")
+
+
+def feedback_loop(abi, cfg, mh, pol0, batches, K, window, ws, eta, kappa, p_floor):
+    """K passes over the batches with the runtime feedback rules applied after
+    every `window` passes; the window's observations accumulate on the GPU and
+    one host copy of six numbers per window feeds the host update.  Returns
+    (ms, per-window trajectory)."""
+    import torch
+    dev = batches[0].device
+    policy = abi.make_policy(**pol0)
+    ct = abi.CounterTrace(cfg["n_layers"], dev)
+    stats = torch.zeros(6, dtype=torch.float64, device=dev)
+    host = torch.zeros(6, dtype=torch.float64).pin_memory()
+    nb = len(batches)
+    states = [abi.StateBuffers(batches[i % nb].clone()) for i in range(K)]
+    traj = []
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(K):
+        abi.trimmoe_stack_forward(mh.model, policy, states[i].state, ct.trace, ws)
+        abi.trimmoe_window_stats(mh.model, policy, states[i].state, ct.trace, stats)
+        if (i + 1) % window == 0 or i == K - 1:
+            host.copy_(stats, non_blocking=True)
+            stats.zero_()
+            stream.synchronize()
+            s = host.tolist()
+            abi.trimmoe_feedback_update(policy, s, eta, kappa, p_floor)
+            traj.append(dict(after_pass=i + 1, p_exit=policy.p_exit, omega_t=policy.omega_t,
+                             exit_frac=s[1] / s[0] if s[0] else 0.0,
+                             util=s[3] / s[0] if s[0] else 0.0,
+                             delay_norm=s[4] / s[5] if s[5] else 0.0))
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1), traj
 
 
 def main():
@@ -316,7 +366,7 @@ def main():
                    "tokens_per_step": T, "fresh_batch_per_step": decode,
                    "parallelism": "single-gpu"},
         "roofline": {
-            "kernel": {"route": "k_subst + k_route (route, substitution, skip)",
+            "kernel": {"route": "k_route (route, substitution, skip)",
                        "bucket": "k_scan + k_bucket (bucketing)",
                        "up": "k_ffn_mma (grouped up/gate + activation)",
                        "down": "k_ffn_mma (grouped down)",
@@ -349,6 +399,18 @@ def main():
         "wall_s_timed_region": wall,
         "input_generation_s": t_gen,
     }
+    fw = args.feedback_window if args.feedback_window is not None else (16 if decode else 0)
+    if fw > 0:
+        ms_obs, _ = feedback_loop(abi, cfg, mh, inp["policy"], batches, K, fw, ws, 0.0, 0.0,
+                                  args.p_floor)
+        ms_fb, traj = feedback_loop(abi, cfg, mh, inp["policy"], batches, K, fw, ws, args.eta,
+                                    args.kappa, args.p_floor)
+        out["feedback"] = {
+            "window": fw, "eta": args.eta, "kappa": args.kappa, "p_floor": args.p_floor,
+            "tokens_per_s": T * K / (ms_fb * 1e-3), "ms_per_step": ms_fb / K,
+            "observation_cost_frac": ms_obs / ms_total - 1.0,
+            "p_exit_start": inp["policy"]["p_exit"], "omega_t_start": inp["policy"]["omega_t"],
+            "windows": traj}
     if not args.no_cpu_baseline:
         inp["h0"] = batches[0]
         out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TRIMMOE_ABI_VERSION 1
+#define TRIMMOE_ABI_VERSION 2
 
 /* status codes */
 #define TRIMMOE_OK 0
@@ -164,8 +164,10 @@ typedef struct trimmoe_state {
  * d_acc NaN.  exec[t][s] is the expert slot s runs (target, substitute, or
  * -1 if skipped); kind per the TRIMMOE_KIND_* codes; gate is the slot
  * weight; xi is NaN where no confidence was evaluated; d_acc is D-hat
- * after the layer.  counters[l][0..7] = active, executed, skipped, exited,
- * substituted slots, remote slots, merged rows, distinct experts.
+ * after the layer.  counters[l][0..8] = active, executed, skipped, exited,
+ * substituted slots, remote slots, merged rows, distinct experts, and remote
+ * targets among the routed slots of the active tokens (what exact execution
+ * of every active token would send remote); counters[l][9..15] are zero.
  */
 typedef struct trimmoe_trace {
   int8_t* action;      /* [N, T]    */
@@ -176,7 +178,7 @@ typedef struct trimmoe_trace {
   float* importance;   /* [N, T]    */
   float* xi;           /* [N, T]    */
   float* d_acc;        /* [N, T]    */
-  int32_t* counters;   /* [N, 8]    */
+  int32_t* counters;   /* [N, 16]   */
 } trimmoe_trace;
 
 /* TRIMMOE_ABI_VERSION of the built library. */
@@ -246,6 +248,43 @@ int trimmoe_stack_forward_timed(const trimmoe_model* m, const trimmoe_policy* p,
                                 void* workspace, size_t workspace_bytes,
                                 void* stream, void* const* events,
                                 int32_t n_events);
+
+
+/*
+ * Runtime feedback (Sec. V-D Eq. (37), Sec. V-F Eq. (43)) over an
+ * observation window of stack passes.
+ *
+ * trimmoe_window_stats adds one pass's observations to stats[0..5] (device
+ * memory, 6 doubles, caller-owned and caller-zeroed at the start of a
+ * window): tokens, tokens that exited, sum of their confidence at exit, sum
+ * over tokens of D-hat / budget (0 where the budget is 0), delay of the
+ * executed slots (t_local per local exact or substitute slot, t_remote per
+ * remote exact slot), and the reference delay of full-depth exact
+ * execution on the same placement (Eq. (21)): per layer, T * k times the
+ * mean per-slot delay of the routed targets of the tokens active there
+ * (the mean over the whole pass for a layer no token reached; 0 for an
+ * empty pass).  Reads the state left by the pass and trace->counters (the
+ * only trace field needed); one small kernel on `stream`, fixed summation
+ * order.
+ */
+int trimmoe_window_stats(const trimmoe_model* m, const trimmoe_policy* p,
+                         const trimmoe_state* s, const trimmoe_trace* trace,
+                         double* stats, void* stream);
+
+/*
+ * Host-only update of p->p_exit and p->omega_t from a window's stats
+ * (host copy of the 6 doubles above):
+ *   Eq. (37): p_J <- clip(p_J + eta (xi_exit_mean - p_J), [p_floor, 1]),
+ *             unchanged when no token exited;
+ *   Eq. (43): omega_D <- clip(omega_D + kappa (D_mean - T_norm), [0, 1]),
+ *             omega_T <- 1 - omega_D, with D_mean = stats[3] / stats[0] and
+ *             T_norm = stats[4] / stats[5]; unchanged when stats[0] or
+ *             stats[5] is 0.
+ * eta, kappa >= 0, p_floor in [0, 1]; stats finite and >= 0; else
+ * TRIMMOE_ERR_POLICY and *p unchanged.
+ */
+int trimmoe_feedback_update(trimmoe_policy* p, const double* stats, double eta,
+                            double kappa, double p_floor);
 
 #ifdef __cplusplus
 }

@@ -9,10 +9,12 @@ never does, and shares no code with it.
 from .trimmoe_oracle import (round_bf16, q_loss, route, substitutes, decide,
                              expert_ffn, exit_confidence, layer_step,
                              stack_forward, init_state, model_from_inputs,
+                             window_stats, feedback_update,
                              ACT_INACTIVE, ACT_EXEC, ACT_SKIP,
                              KIND_NONE, KIND_LOCAL, KIND_SUB, KIND_REMOTE)
 
 __all__ = ["round_bf16", "q_loss", "route", "substitutes", "decide",
            "expert_ffn", "exit_confidence", "layer_step", "stack_forward",
-           "init_state", "model_from_inputs", "ACT_INACTIVE", "ACT_EXEC",
+           "init_state", "model_from_inputs", "window_stats", "feedback_update",
+           "ACT_INACTIVE", "ACT_EXEC",
            "ACT_SKIP", "KIND_NONE", "KIND_LOCAL", "KIND_SUB", "KIND_REMOTE"]

@@ -451,3 +451,74 @@ def model_from_inputs(inputs, layers=None):
             sim=_f64(L["sim"]), theta=float(L["theta"]),
             skip_slope=float(L["skip_slope"]))
     return out
+
+
+# ----------------------------------------------------------------------------
+# runtime feedback over an observation window (Sec. V-D Eq. (37), Sec. V-F
+# Eq. (43))
+#
+# Readings: F1 a window is a run of stack passes; its statistics are sums
+# over them.  F2 xi_exit-bar is the mean confidence at which the window's
+# tokens exited; without exits p_J is left unchanged.  F3 the budget
+# utilisation D-bar is the mean over the window's tokens of D-hat / budget
+# at the end of the pass (a zero budget counts as zero utilisation).  F4 the
+# normalised delay T-bar is the total per-slot delay of the executed slots
+# (t_local for local exact and substitute slots, t_remote for remote exact
+# ones) over T_ref, which Eq. (21) defines as the delay of full-depth exact
+# execution on the same placement.  That strategy is not run: T_ref is
+# estimated from the pass itself, each layer counting T k slots at the mean
+# delay of the routed targets of the tokens active there (skipped tokens
+# included), and a layer that no token reached at the mean over all routed
+# slots of the pass.  With no exit this is exact for the routes observed.
+# A zero T_ref (an empty window, or t_local = t_remote = 0) leaves the
+# weights unchanged.
+# ----------------------------------------------------------------------------
+def window_stats(model, pol, state, traces, token_budget=None):
+    """Sums of one stack pass's observations (add the dicts of a window)."""
+    N, k = model["n_layers"], model["top_k"]
+    T = state["h"].shape[0]
+    exited = state["exit_layer"] < N
+    budget = np.full(T, float(pol["budget"])) if token_budget is None \
+        else np.asarray(token_budget, dtype=np.float64)
+    util = np.where(budget > 0, state["d_acc"] / np.where(budget > 0, budget, 1.0), 0.0)
+    def slot_delay(local):
+        return pol["t_local"] if local else pol["t_remote"]
+
+    delay = 0.0
+    layer_mean = []      # mean routed-target delay per layer (None: nobody active)
+    routed = []          # every routed slot's delay in the pass
+    for l, tr in enumerate(traces):
+        for q in np.nonzero(tr["action"] == ACT_EXEC)[0]:
+            for kind in tr["kind"][q]:
+                delay += slot_delay(kind != KIND_REMOTE)
+        local = model["layers"][l]["local_mask"]
+        here = [slot_delay(local[e]) for q in np.nonzero(tr["action"] != ACT_INACTIVE)[0]
+                for e in tr["target"][q]]
+        routed += here
+        layer_mean.append(sum(here) / len(here) if here else None)
+    ref = 0.0
+    if routed:
+        pooled = sum(routed) / len(routed)
+        ref = sum(T * k * (pooled if m is None else m) for m in layer_mean)
+    return dict(tokens=float(T), exits=float(exited.sum()),
+                xi_exit=float(state["xi"][exited].sum()), util=float(util.sum()),
+                delay=delay, delay_ref=ref)
+
+
+def feedback_update(pol, stats, eta: float, kappa: float, p_floor: float):
+    """New (p_exit, omega_t) after one window.
+
+    Eq. (37): p_J <- clip(p_J + eta (xi_exit-bar - p_J), [p_floor, 1]).
+    Eq. (43): omega_D <- clip(omega_D + kappa (D-bar - T-bar), [0, 1]),
+              omega_T <- 1 - omega_D.
+    """
+    p = pol["p_exit"]
+    if stats["exits"] > 0:
+        xi_bar = stats["xi_exit"] / stats["exits"]
+        p = min(1.0, max(p_floor, p + eta * (xi_bar - p)))
+    omega_d = 1.0 - pol["omega_t"]
+    if stats["tokens"] > 0 and stats["delay_ref"] > 0:
+        d_bar = stats["util"] / stats["tokens"]
+        t_bar = stats["delay"] / stats["delay_ref"]
+        omega_d = min(1.0, max(0.0, omega_d + kappa * (d_bar - t_bar)))
+    return p, 1.0 - omega_d

@@ -16,6 +16,8 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libtrimmoe.so")
 
+ABI_VERSION = 2   # TRIMMOE_ABI_VERSION this binding is written for
+N_COUNTERS = 16   # per-layer trace counters (row stride of trimmoe_trace.counters)
 TRIMMOE_OK = 0
 STATUS = {0: "OK", -1: "ERR_NULL", -2: "ERR_SHAPE", -3: "ERR_DTYPE", -4: "ERR_POLICY",
           -5: "ERR_LAYER", -6: "ERR_WORKSPACE", -7: "ERR_HIP"}
@@ -63,7 +65,7 @@ class Trace(C.Structure):
 
 EXPORTS = ["trimmoe_abi_version", "trimmoe_status_str", "trimmoe_workspace_size",
            "trimmoe_state_reset", "trimmoe_layer_step", "trimmoe_stack_forward",
-           "trimmoe_stack_forward_timed"]
+           "trimmoe_stack_forward_timed", "trimmoe_window_stats", "trimmoe_feedback_update"]
 TIMED_CLASSES = ["route", "bucket", "up", "down", "shared", "combine", "exit", "gate"]
 
 _lib = None
@@ -97,6 +99,16 @@ def lib():
                                                   C.POINTER(State), C.POINTER(Trace),
                                                   C.c_void_p, C.c_size_t, C.c_void_p,
                                                   C.POINTER(C.c_void_p), C.c_int32]
+        L.trimmoe_window_stats.restype = C.c_int
+        L.trimmoe_window_stats.argtypes = [C.POINTER(Model), C.POINTER(Policy),
+                                           C.POINTER(State), C.POINTER(Trace), C.c_void_p,
+                                           C.c_void_p]
+        L.trimmoe_feedback_update.restype = C.c_int
+        L.trimmoe_feedback_update.argtypes = [C.POINTER(Policy), C.POINTER(C.c_double),
+                                              C.c_double, C.c_double, C.c_double]
+        if L.trimmoe_abi_version() != ABI_VERSION:
+            raise RuntimeError(f"{LIB_PATH} has ABI version {L.trimmoe_abi_version()}, the "
+                               f"binding expects {ABI_VERSION}: rebuild it")
         _lib = L
     return _lib
 
@@ -172,6 +184,24 @@ def trimmoe_stack_forward_timed(model: Model, policy: Policy, state: State, trac
                                              _stream_handle(stream), arr, len(events)))
 
 
+def trimmoe_window_stats(model: Model, policy: Policy, state: State, trace,
+                         stats: torch.Tensor, stream=None):
+    """Add one stack pass's observations to ``stats`` (float64 [6] on the GPU)."""
+    assert stats.dtype == torch.float64 and stats.numel() == 6 and stats.is_contiguous()
+    tr = C.byref(trace) if trace is not None else None
+    _check("trimmoe_window_stats",
+           lib().trimmoe_window_stats(C.byref(model), C.byref(policy), C.byref(state), tr,
+                                      _ptr(stats), _stream_handle(stream)))
+
+
+def trimmoe_feedback_update(policy: Policy, stats, eta: float, kappa: float, p_floor: float):
+    """Update policy.p_exit and policy.omega_t in place from a window's stats
+    (six numbers on the host)."""
+    arr = (C.c_double * 6)(*[float(v) for v in stats])
+    _check("trimmoe_feedback_update",
+           lib().trimmoe_feedback_update(C.byref(policy), arr, eta, kappa, p_floor))
+
+
 # ------------------------------------------------ struct construction ------
 class ModelHandle:
     """A Model struct over device tensors; keeps the tensors alive.
@@ -239,10 +269,20 @@ class TraceBuffers:
         self.importance = torch.zeros(n_layers, T, dtype=torch.float32, **z)
         self.xi = torch.zeros(n_layers, T, dtype=torch.float32, **z)
         self.d_acc = torch.zeros(n_layers, T, dtype=torch.float32, **z)
-        self.counters = torch.zeros(n_layers, 8, dtype=torch.int32, **z)
+        self.counters = torch.zeros(n_layers, N_COUNTERS, dtype=torch.int32, **z)
         self.trace = Trace(*(getattr(self, n).data_ptr() for n in
                              ("action", "target", "exec", "kind", "gate", "importance", "xi",
                               "d_acc", "counters")))
+
+
+class CounterTrace:
+    """A trace that records only the per-layer counters (what the runtime
+    feedback observations need)."""
+
+    def __init__(self, n_layers: int, device):
+        self.counters = torch.zeros(n_layers, N_COUNTERS, dtype=torch.int32, device=device)
+        self.trace = Trace(None, None, None, None, None, None, None, None,
+                           self.counters.data_ptr())
 
 
 def alloc_workspace(model: Model, max_tokens: int, device) -> torch.Tensor:

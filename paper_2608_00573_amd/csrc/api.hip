@@ -182,7 +182,7 @@ void fill_params(LayerParams& P, const trimmoe_model* m, int l, const trimmoe_po
   P.tr_importance = tr && tr->importance ? tr->importance + rowT : nullptr;
   P.tr_xi = tr && tr->xi ? tr->xi + rowT : nullptr;
   P.tr_d_acc = tr && tr->d_acc ? tr->d_acc + rowT : nullptr;
-  P.tr_counters = tr && tr->counters ? tr->counters + (size_t)l * 8 : nullptr;
+  P.tr_counters = tr && tr->counters ? tr->counters + (size_t)l * kCounters : nullptr;
 }
 
 bool any_trace(const trimmoe_trace* tr) {
@@ -197,9 +197,12 @@ int check_workspace(const trimmoe_model* m, const trimmoe_state* s, void* ws, si
   return TRIMMOE_OK;
 }
 
-// ev: NULL, or TRIMMOE_TIMED_CLASSES + 1 events recorded around the classes
+// ev: NULL, or TRIMMOE_TIMED_CLASSES + 1 events recorded around the classes;
+// fill_layers: trace rows of this many layers from l on get their inactive
+// defaults first (a stack pass fills all of them at layer 0)
 int run_layer(const trimmoe_model* m, int l, const trimmoe_policy* pol, const trimmoe_state* s,
-              const trimmoe_trace* tr, void* ws, hipStream_t st, hipEvent_t* ev) {
+              const trimmoe_trace* tr, void* ws, hipStream_t st, hipEvent_t* ev,
+              int fill_layers) {
   if (s->n_tokens == 0) return TRIMMOE_OK;
   LayerParams P;
   memset(&P, 0, sizeof(P));
@@ -218,7 +221,7 @@ int run_layer(const trimmoe_model* m, int l, const trimmoe_policy* pol, const tr
 #define TRIMMOE_MARK(i) \
   if (ev) TRIMMOE_TRY(hipEventRecord(ev[i], st))
   TRIMMOE_MARK(0);
-  if (any_trace(tr)) TRIMMOE_TRY(launch_trace_fill(P, st));
+  if (fill_layers > 0 && any_trace(tr)) TRIMMOE_TRY(launch_trace_fill(P, fill_layers, st));
   TRIMMOE_TRY(launch_route(P, bf16, st));
   TRIMMOE_MARK(TRIMMOE_CLASS_ROUTE + 1);
   TRIMMOE_TRY(launch_scan(P, st));
@@ -264,7 +267,8 @@ int stack(const trimmoe_model* m, const trimmoe_policy* p, trimmoe_state* s,
   for (int l = 0; l < m->n_layers; ++l) {
     hipEvent_t* ev = events ? reinterpret_cast<hipEvent_t*>(const_cast<void**>(events)) + l * per
                             : nullptr;
-    if ((rc = run_layer(m, l, p, s, trace, workspace, st, ev))) return rc;
+    if ((rc = run_layer(m, l, p, s, trace, workspace, st, ev, l == 0 ? m->n_layers : 0)))
+      return rc;
   }
   return TRIMMOE_OK;
 }
@@ -321,7 +325,8 @@ int trimmoe_layer_step(const trimmoe_model* m, int32_t layer, const trimmoe_poli
   if ((rc = validate_state(m, s))) return rc;
   if (layer < 0 || layer >= m->n_layers) return TRIMMOE_ERR_LAYER;
   if ((rc = check_workspace(m, s, workspace, workspace_bytes))) return rc;
-  return run_layer(m, layer, p, s, trace, workspace, static_cast<hipStream_t>(stream), nullptr);
+  return run_layer(m, layer, p, s, trace, workspace, static_cast<hipStream_t>(stream), nullptr,
+                   1);
 }
 
 int trimmoe_stack_forward(const trimmoe_model* m, const trimmoe_policy* p, trimmoe_state* s,
@@ -336,6 +341,45 @@ int trimmoe_stack_forward_timed(const trimmoe_model* m, const trimmoe_policy* p,
                                 int32_t n_events) {
   if (!events) return TRIMMOE_ERR_NULL;
   return stack(m, p, s, trace, workspace, workspace_bytes, stream, events, n_events);
+}
+
+int trimmoe_window_stats(const trimmoe_model* m, const trimmoe_policy* p, const trimmoe_state* s,
+                         const trimmoe_trace* trace, double* stats, void* stream) {
+  int rc = validate_model(m);
+  if (rc) return rc;
+  if ((rc = validate_policy(p))) return rc;
+  if ((rc = validate_state(m, s))) return rc;
+  if (!trace || !trace->counters || !stats) return TRIMMOE_ERR_NULL;
+  WindowArgs w{s->n_tokens, m->n_layers, m->top_k, s->exit_layer, s->xi, s->d_acc,
+               p->budget_tok, p->budget, p->t_local, p->t_remote, trace->counters, stats};
+  return launch_window_stats(w, static_cast<hipStream_t>(stream)) == hipSuccess ? TRIMMOE_OK
+                                                                                  : TRIMMOE_ERR_HIP;
+}
+
+int trimmoe_feedback_update(trimmoe_policy* p, const double* stats, double eta, double kappa,
+                            double p_floor) {
+  if (!p || !stats) return TRIMMOE_ERR_NULL;
+  if (validate_policy(p)) return TRIMMOE_ERR_POLICY;
+  if (!(eta >= 0.0) || !(kappa >= 0.0) || isinf(eta) || isinf(kappa) ||
+      !(p_floor >= 0.0 && p_floor <= 1.0))
+    return TRIMMOE_ERR_POLICY;
+  for (int i = 0; i < 6; ++i)
+    if (!(stats[i] >= 0.0) || isinf(stats[i])) return TRIMMOE_ERR_POLICY;
+  const double tokens = stats[0], exits = stats[1], xi_exit = stats[2], util = stats[3],
+               delay = stats[4], delay_ref = stats[5];
+  double pj = p->p_exit;
+  if (exits > 0.0) {  // Eq. (37): towards the mean confidence at exit, within [p_floor, 1]
+    pj += eta * (xi_exit / exits - pj);
+    pj = pj < p_floor ? p_floor : (pj > 1.0 ? 1.0 : pj);
+  }
+  double omega_d = 1.0 - p->omega_t;
+  if (tokens > 0.0 && delay_ref > 0.0) {  // Eq. (43): budget utilisation vs normalised delay
+    omega_d += kappa * (util / tokens - delay / delay_ref);
+    omega_d = omega_d < 0.0 ? 0.0 : (omega_d > 1.0 ? 1.0 : omega_d);
+  }
+  p->p_exit = (float)pj;
+  p->omega_t = (float)(1.0 - omega_d);
+  return TRIMMOE_OK;
 }
 
 }  // extern "C"

@@ -33,6 +33,8 @@ inline int exit_tile_rows(bool bf16, int T) {
 }
 // fp32 GEMM tile
 constexpr int kF32Tile = 16;
+// per-layer trace counters (row stride of trimmoe_trace.counters)
+constexpr int kCounters = 16;
 
 // slots of the small device counter block in the workspace
 enum CountSlot {
@@ -133,16 +135,31 @@ struct LayerParams {
   int n_cu;            // compute units of the device (persistent grids)
 };
 
+// observations of one stack pass for the runtime feedback rules
+struct WindowArgs {
+  int T, N, k;
+  const int32_t* exit_layer;  // [T]
+  const float* xi;            // [T]
+  const float* d_acc;         // [T]
+  const float* budget_tok;    // [T] or NULL
+  float budget, t_local, t_remote;
+  const int32_t* counters;    // trace counters [N, kCounters]
+  double* stats;              // [6], accumulated
+};
+
 // launchers (decide.hip)
 hipError_t launch_state_reset(const trimmoe_model* m, const trimmoe_state* s,
                               hipStream_t st);
-hipError_t launch_trace_fill(const LayerParams& p, hipStream_t st);
+// inactive defaults of the trace rows of n_layers consecutive layers, from
+// the layer p's trace pointers point at
+hipError_t launch_trace_fill(const LayerParams& p, int n_layers, hipStream_t st);
 hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_scan(const LayerParams& p, hipStream_t st);
 hipError_t launch_bucket(const LayerParams& p, hipStream_t st);
 hipError_t launch_combine(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_exit_reduce(const LayerParams& p, hipStream_t st);
 hipError_t launch_compact(const LayerParams& p, hipStream_t st);
+hipError_t launch_window_stats(const WindowArgs& w, hipStream_t st);
 
 // launchers (gemm.hip)
 hipError_t launch_expert_up(const LayerParams& p, bool bf16, hipStream_t st);

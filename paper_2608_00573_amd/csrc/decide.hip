@@ -45,22 +45,25 @@ __global__ void k_state_reset(int T, int N, float* d_acc, int32_t* active_idx,
 }
 
 // ------------------------------------------------ trace: inactive default --
+// Rows of the layers p's trace pointers start at, one per blockIdx.y.
 __global__ void k_trace_fill(LayerParams p) {
-  int t = blockIdx.x * blockDim.x + threadIdx.x;
+  const int t = blockIdx.x * blockDim.x + threadIdx.x;
+  const size_t y = blockIdx.y, rowT = y * p.T, rowTk = rowT * p.k;
   const float qnan = __int_as_float(0x7fc00000);
-  if (blockIdx.x == 0 && threadIdx.x < 8 && p.tr_counters) p.tr_counters[threadIdx.x] = 0;
+  if (blockIdx.x == 0 && threadIdx.x < kCounters && p.tr_counters)
+    p.tr_counters[y * kCounters + threadIdx.x] = 0;
   if (t >= p.T) return;
-  if (p.tr_action) p.tr_action[t] = TRIMMOE_ACT_INACTIVE;
+  if (p.tr_action) p.tr_action[rowT + t] = TRIMMOE_ACT_INACTIVE;
   for (int s = 0; s < p.k; ++s) {
-    size_t o = (size_t)t * p.k + s;
+    const size_t o = rowTk + (size_t)t * p.k + s;
     if (p.tr_target) p.tr_target[o] = -1;
     if (p.tr_exec) p.tr_exec[o] = -1;
     if (p.tr_kind) p.tr_kind[o] = TRIMMOE_KIND_NONE;
     if (p.tr_gate) p.tr_gate[o] = qnan;
   }
-  if (p.tr_importance) p.tr_importance[t] = qnan;
-  if (p.tr_xi) p.tr_xi[t] = qnan;
-  if (p.tr_d_acc) p.tr_d_acc[t] = qnan;
+  if (p.tr_importance) p.tr_importance[rowT + t] = qnan;
+  if (p.tr_xi) p.tr_xi[rowT + t] = qnan;
+  if (p.tr_d_acc) p.tr_d_acc[rowT + t] = qnan;
 }
 
 // ------------------------------------------- route + decide (one layer) --
@@ -310,9 +313,10 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     if (!have) skip = false;  // unreachable: the empty assignment is feasible
 
     // per-slot execution and merged rows (a substitute keeps its target's weight)
-    int nrows = 0, nsubst = 0, nremote = 0;
+    int nrows = 0, nsubst = 0, nremote = 0, nroute_remote = 0;
     for (int r = 0; r < k; ++r) {
       const int e = sS[i][r];
+      nroute_remote += !p.local_mask[e];
       int x = -1, kind = TRIMMOE_KIND_NONE;
       if (!skip) {
         if ((bmask >> r) & 1) {
@@ -358,6 +362,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
       atomicAdd(&p.tr_counters[skip ? 2 : 1], 1);
       if (nsubst) atomicAdd(&p.tr_counters[4], nsubst);
       if (nremote) atomicAdd(&p.tr_counters[5], nremote);
+      if (nroute_remote) atomicAdd(&p.tr_counters[8], nroute_remote);
     }
   }
   __syncthreads();
@@ -655,8 +660,9 @@ hipError_t launch_state_reset(const trimmoe_model* m, const trimmoe_state* s, hi
   return hipGetLastError();
 }
 
-hipError_t launch_trace_fill(const LayerParams& p, hipStream_t st) {
-  hipLaunchKernelGGL(k_trace_fill, dim3(cdiv(p.T > 0 ? p.T : 1, 256)), dim3(256), 0, st, p);
+hipError_t launch_trace_fill(const LayerParams& p, int n_layers, hipStream_t st) {
+  hipLaunchKernelGGL(k_trace_fill, dim3(cdiv(p.T > 0 ? p.T : 1, 256), n_layers), dim3(256), 0, st,
+                     p);
   return hipGetLastError();
 }
 
@@ -696,6 +702,70 @@ hipError_t launch_exit_reduce(const LayerParams& p, hipStream_t st) {
 
 hipError_t launch_compact(const LayerParams& p, hipStream_t st) {
   hipLaunchKernelGGL(k_compact, dim3(1), dim3(1024), 0, st, p);
+  return hipGetLastError();
+}
+
+
+// --------------------------------- runtime feedback observations (window) --
+// Sums over one stack pass, added to stats[0..5] = tokens, exits, confidence
+// at exit, budget utilisation D-hat / budget, executed-slot delay, and the
+// reference delay of full-depth exact execution (Sec. V-D Eq. (37), Sec. V-F
+// Eq. (43), normalised as in Eq. (21)).  The reference prices each layer at
+// T k slots of the mean routed-target delay of the tokens active there; a
+// layer no token reached takes the mean over the whole pass.  One block,
+// fixed summation order: repeated runs give identical sums.
+__global__ __launch_bounds__(1024) void k_window_stats(WindowArgs w) {
+  __shared__ double s_red[3][1024];
+  double v[3] = {0.0, 0.0, 0.0};  // exits, confidence at exit, utilisation
+  for (int t = threadIdx.x; t < w.T; t += 1024) {
+    if (w.exit_layer[t] < w.N) {
+      v[0] += 1.0;
+      v[1] += (double)w.xi[t];
+    }
+    const double b = w.budget_tok ? (double)w.budget_tok[t] : (double)w.budget;
+    if (b > 0.0) v[2] += (double)w.d_acc[t] / b;
+  }
+#pragma unroll
+  for (int i = 0; i < 3; ++i) s_red[i][threadIdx.x] = v[i];
+  __syncthreads();
+  for (int stride = 512; stride > 0; stride >>= 1) {
+    if (threadIdx.x < stride)
+#pragma unroll
+      for (int i = 0; i < 3; ++i) s_red[i][threadIdx.x] += s_red[i][threadIdx.x + stride];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double tl = w.t_local, tr = w.t_remote;
+    double delay = 0.0, routed = 0.0, routed_remote = 0.0;
+    for (int l = 0; l < w.N; ++l) {
+      // executed tokens, remote exact slots; routed slots, their remote targets
+      const int* c = w.counters + kCounters * l;
+      const double slots = (double)c[1] * w.k;
+      delay += (slots - c[5]) * tl + (double)c[5] * tr;
+      routed += (double)c[0] * w.k;
+      routed_remote += (double)c[8];
+    }
+    double ref = 0.0;
+    if (routed > 0.0) {
+      const double pooled = ((routed - routed_remote) * tl + routed_remote * tr) / routed;
+      for (int l = 0; l < w.N; ++l) {
+        const int* c = w.counters + kCounters * l;
+        const double r = (double)c[0] * w.k;
+        const double mean = r > 0.0 ? ((r - c[8]) * tl + (double)c[8] * tr) / r : pooled;
+        ref += (double)w.T * w.k * mean;
+      }
+    }
+    w.stats[0] += (double)w.T;
+    w.stats[1] += s_red[0][0];
+    w.stats[2] += s_red[1][0];
+    w.stats[3] += s_red[2][0];
+    w.stats[4] += delay;
+    w.stats[5] += ref;
+  }
+}
+
+hipError_t launch_window_stats(const WindowArgs& w, hipStream_t st) {
+  hipLaunchKernelGGL(k_window_stats, dim3(1), dim3(1024), 0, st, w);
   return hipGetLastError();
 }
 

@@ -29,7 +29,9 @@ def test_library_exports_every_declared_symbol():
     L = abi.lib()
     for name in _declared():
         assert hasattr(L, name), name
-    assert abi.trimmoe_abi_version() == 1
+    txt = open(os.path.join(ROOT, "include", "trimmoe.h")).read()
+    declared = int(re.search(r"#define TRIMMOE_ABI_VERSION (\d+)", txt).group(1))
+    assert abi.trimmoe_abi_version() == declared == abi.ABI_VERSION
     assert abi.trimmoe_status_str(0) == "ok"
     assert "workspace" in abi.trimmoe_status_str(-6)
 
