@@ -53,6 +53,8 @@ def parse():
                     help="timed steps (default 20; the decode workload: its step count, 128)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="switch_base_8e")
+    ap.add_argument("--horizon", type=int, default=None,
+                    help="look-ahead horizon H of the decision (default: the workload's, 1)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -170,7 +172,10 @@ def cpu_baseline(inp, target_s, max_f64_bytes=24e9):
     cfg = inp["cfg"]
     N = cfg["n_layers"]
     n_l = min(N, max(1, int(max_f64_bytes // _f64_layer_bytes(cfg))))
-    models = {l: O.model_from_inputs(inp, layers=[l]) for l in range(n_l)}
+    H = int(inp["policy"].get("horizon", 1))
+    models = {l: O.model_from_inputs(inp, layers=[l],
+                                     decision_layers=range(l + 1, min(l + H, N)))
+              for l in range(n_l)}
     pol = {k: float(np.float32(v)) for k, v in inp["policy"].items()}
     h0 = inp["h0"].double().cpu().numpy()
     T = h0.shape[0]
@@ -254,6 +259,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     cfg = workload(args.workload)
+    if args.horizon is not None:
+        cfg["horizon"] = args.horizon
     decode = "decode_steps" in cfg
     K = args.steps if args.steps is not None else (cfg["decode_steps"] if decode else 20)
     W = args.warmup
@@ -364,6 +371,7 @@ def main():
                    "experts": cfg["n_experts"], "top_k": cfg["top_k"], "d_ff": cfg["d_ff"],
                    "d_ff_shared": cfg["d_ff_shared"], "vocab_exit": cfg["vocab_exit"],
                    "tokens_per_step": T, "fresh_batch_per_step": decode,
+                   "horizon": cfg["horizon"], "transition_row_entries": cfg["trans_support"],
                    "parallelism": "single-gpu"},
         "roofline": {
             "kernel": {"route": "k_route (route, substitution, skip)",

@@ -46,7 +46,7 @@
 extern "C" {
 #endif
 
-#define TRIMMOE_ABI_VERSION 2
+#define TRIMMOE_ABI_VERSION 3
 
 /* status codes */
 #define TRIMMOE_OK 0
@@ -70,6 +70,12 @@ extern "C" {
 /* limits checked by validation */
 #define TRIMMOE_MAX_EXPERTS 256
 #define TRIMMOE_MAX_TOPK 8
+/* look-ahead (policy.horizon > 1): H <= 4, top_k <= 4, 1 <= trans_b <= 8,
+ * (2^k + 1) * trans_b^k <= 1024 first-level branches per token, and
+ * (2^k + 1)^H * trans_b^(k (H - 1)) <= 2^21 cost evaluations per token */
+#define TRIMMOE_MAX_HORIZON 4
+#define TRIMMOE_MAX_LOOKAHEAD_TOPK 4
+#define TRIMMOE_MAX_TRANS_B 8
 
 /* actions recorded in the trace */
 #define TRIMMOE_ACT_INACTIVE 0
@@ -101,6 +107,13 @@ typedef struct trimmoe_layer {
   const float* sim;       /* [E, E] fp32 expert similarity Sim_l (Eq. (3))      */
   float theta;            /* importance threshold theta_l (Eq. (24), Sec. V-C)  */
   float skip_slope;       /* s_l of the skip degradation rho(I)=min(1,s_l I)    */
+  /* Expert transitions P_l from this layer to the next (Eq. (38)), read by
+   * the look-ahead only (policy.horizon > 1: the decision at layer l reads
+   * P_l .. P_{l+H-2}, never the last layer's, and those must be non-NULL):
+   * row e holds trans_b (target, probability) entries; target -1
+   * (probability 0) pads a row.  Device memory, caller-owned.             */
+  const int16_t* trans_to; /* [E, trans_b] next-layer expert or -1           */
+  const float* trans_p;    /* [E, trans_b] probabilities, each row sums to 1 */
 } trimmoe_layer;
 
 typedef struct trimmoe_model {
@@ -116,6 +129,7 @@ typedef struct trimmoe_model {
   int32_t conf_mode;      /* TRIMMOE_CONF_SOFTMAX | TRIMMOE_CONF_SIGMOID        */
   int32_t normalize_topk; /* 1: slot weight p_e / I, 0: p_e                     */
   const trimmoe_layer* layers; /* host array of N layers                        */
+  int32_t trans_b;        /* entries per transition row (0: no transitions)     */
 } trimmoe_model;
 
 /*
@@ -124,6 +138,15 @@ typedef struct trimmoe_model {
  * skip = (1 - omega_t) * Lambda / budget (Eq. (32)).  Q(e, j) =
  * min(1, phi_scale * (1 - Sim[e][j]) / 2) (Eq. (3)); a local expert j is a
  * feasible substitute of e when Sim[e][j] >= sim_min.
+ *
+ * With horizon H > 1 every candidate action also carries the cost-to-go
+ * Phi^(H-1) of Eq. (39) and the action minimising the sum is taken
+ * (Eq. (40)): the expected least cost of the next H - 1 layers, each slot's
+ * next target drawn from the transition row of the expert the slot runs
+ * (its routed target after a skip), starting from the budget the action
+ * leaves.  The token's importance at this layer stands in for later ones,
+ * exits are not predicted inside the recursion, and the token never moves
+ * (one GPU: the location in Eq. (39) is always this device).
  */
 typedef struct trimmoe_policy {
   float p_exit;      /* confidence requirement p_J (Eq. (8))               */
@@ -135,6 +158,8 @@ typedef struct trimmoe_policy {
   float sim_min;     /* similarity floor of feasible substitutes            */
   const float* p_exit_tok; /* [T] device, per-token p_J, or NULL            */
   const float* budget_tok; /* [T] device, per-token budget, or NULL         */
+  int32_t horizon;   /* look-ahead horizon H, 1..TRIMMOE_MAX_HORIZON (Sec. V-E,
+                        Eq. (39), (40)); 1 = the myopic rule                */
 } trimmoe_policy;
 
 /*

@@ -170,24 +170,25 @@ def route(z, k: int, normalize: bool):
 
 
 # ----------------------------------------------------------------------------
-# Algorithm 2 at H = 1 for one token at one layer
+# Algorithm 2 for one token at one layer
 # ----------------------------------------------------------------------------
-def decide(S, w, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol):
-    """Execute/skip decision and server-expert selection for one token.
+def step_options(S, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol,
+                 m_logit, m_budget):
+    """The feasible actions of one token at one layer and their per-step costs.
 
-    Implements Eq. (31), (32), (34), (35), the importance admission of
-    Sec. V-C and the argmin of Eq. (40) at H = 1 (readings A8-A18).
-    Returns a dict with the action, per-slot (target, exec, kind, weight),
-    the merged execute rows, the degradation charged, and the margins.
+    Eq. (31) execute costs over the substitution subsets A that Eq. (34)'s
+    budget filter admits, Eq. (35) transmission necessity, the importance
+    admission of Sec. V-C and the Eq. (32) skip cost (readings A8-A18).
+    Returns (execs, skip, gamma_pos, lam, kinds0): execs is a list of
+    (f, n_sub, mask, charge, x) with x the expert each slot would run (its
+    target, or the substitute on the bits of mask); skip is (f, charge, x)
+    with x the routed targets, or None.  Deciding margins are appended to
+    m_logit (importance against theta) and m_budget (budget comparisons).
     """
-    k = len(S)
     wt = pol["omega_t"]
     wd = 1.0 - wt
     t_loc, t_rem = pol["t_local"], pol["t_remote"]
-    margins = []
-
-    kinds0 = []
-    qs = []
+    kinds0, qs = [], []
     n_local = n_remote = 0
     rsub = []  # ranks of remote slots that have a local substitute
     for r, e in enumerate(S):
@@ -202,12 +203,10 @@ def decide(S, w, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol):
             if sub_c[e] >= 0:
                 rsub.append(r)
 
-    def quality(sq):
-        return wd * sq / budget if budget > 0 else 0.0
+    def quality(charge):
+        return wd * charge / budget if budget > 0 else 0.0
 
-    # enumerate execute assignments A (bitmask over slot ranks, bits only on
-    # substitutable remote slots); Eq. (34) budget filter, Eq. (31) cost
-    options = []
+    execs = []
     for sel in range(1 << len(rsub)):
         mask = 0
         sq = 0.0
@@ -217,32 +216,55 @@ def decide(S, w, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol):
                 sq += qs[r]
         n_sub = bin(mask).count("1")
         if mask:
-            margins.append(abs(budget - d_hat - sq))
+            m_budget.append(abs(budget - d_hat - sq))
         if d_hat + sq <= budget:
-            f = wt * ((n_local + n_sub) * t_loc + (n_remote - n_sub) * t_rem) \
-                + quality(sq)
-            options.append((f, n_sub, mask, sq))
-    options.sort()
-    best_f, best_nsub, best_mask, best_sq = options[0]
-    if len(options) > 1:
-        margins.append(options[1][0] - options[0][0])
+            f = wt * ((n_local + n_sub) * t_loc + (n_remote - n_sub) * t_rem) + quality(sq)
+            x = [sub_c[e] if mask >> r & 1 else e for r, e in enumerate(S)]
+            execs.append((f, n_sub, mask, sq, x))
 
     # Eq. (35): Gamma > 0 iff no feasible assignment leaves no remote slot
-    all_local_feasible = any(n_sub == n_remote for (_, n_sub, _, _) in options)
-    gamma_pos = not all_local_feasible
-
+    gamma_pos = not any(n_sub == n_remote for (_, n_sub, _, _, _) in execs)
     lam = min(1.0, slope * I)  # Eq. (5), reading A8
-    skip = False
+    skip = None
     if gamma_pos:
-        margins.append(abs(I - theta))
-        margins.append(abs(budget - d_hat - lam))
+        m_logit.append(abs(I - theta))
+        m_budget.append(abs(budget - d_hat - lam))
         if I <= theta and d_hat + lam <= budget:
-            f_skip = quality(lam)  # Eq. (32)
-            margins.append(abs(best_f - f_skip))
-            skip = f_skip < best_f  # tie goes to execute (A14)
+            skip = (quality(lam), lam, list(S))  # Eq. (32)
+    return execs, skip, gamma_pos, lam, kinds0
 
+
+def decide(S, w, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol, phi=None):
+    """Execute/skip decision and server-expert selection for one token.
+
+    Eq. (40): the action minimising the per-step cost plus the look-ahead
+    cost-to-go phi(x, D-hat after the action) (zero at H = 1, Sec. V-E);
+    ties as in A14.  Returns a dict with the action, per-slot (target, exec,
+    kind, weight), the merged execute rows, the degradation charged, and the
+    margins (all, importance/cost ones, budget ones).
+    """
+    k = len(S)
+    m_logit, m_budget = [], []
+    execs, skip_opt, gamma_pos, lam, kinds0 = step_options(
+        S, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol, m_logit, m_budget)
+
+    def total(f, charge, x):
+        return f + (phi(x, d_hat + charge) if phi is not None else 0.0)
+
+    options = sorted((total(f, sq, x), n_sub, mask, sq) for (f, n_sub, mask, sq, x) in execs)
+    best_t, best_nsub, best_mask, best_sq = options[0]
+    if len(options) > 1:
+        m_logit.append(options[1][0] - options[0][0])
+    skip = False
+    if skip_opt is not None:
+        t_skip = total(*skip_opt)
+        m_logit.append(abs(best_t - t_skip))
+        skip = t_skip < best_t  # tie goes to execute (A14)
+
+    margins = m_logit + m_budget
     out = dict(target=list(S), weight=list(w), importance=I, lam=lam,
-               gamma_pos=gamma_pos, margins=margins)
+               gamma_pos=gamma_pos, margins=margins, margins_logit=m_logit,
+               margins_budget=m_budget)
     if skip:
         out.update(action=ACT_SKIP, exec=[-1] * k, kind=[KIND_NONE] * k,
                    d_inc=lam, rows=[])
@@ -266,6 +288,73 @@ def decide(S, w, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol):
     out.update(action=ACT_EXEC, exec=exec_ids, kind=kinds, d_inc=best_sq,
                rows=rows)
     return out
+
+
+# ----------------------------------------------------------------------------
+# Look-ahead cost-to-go (Sec. V-E, Eq. (38)-(40)) for H > 1
+#
+# Readings: L1 one device, the token never moves (A10): the location in
+# Eq. (39) is always home, so the cost-to-go depends on an action only
+# through the experts it runs and the budget it leaves.  L2 P_l(x -> y) is an
+# input per layer (Eq. (38) counts come from a calibration pass), stored as
+# rows of at most B (target, probability) pairs.  The source of a slot is
+# the expert it runs (the substitute after a substitution, the routed target
+# when the slot runs exact or the layer is skipped).  L3 with top-k > 1 the
+# slots move independently: a next-layer target tuple has the product of
+# its slots' probabilities, and it is decided as a routed tuple (duplicates
+# included).  L4 future importance is the token's importance at the current
+# layer (skip admission and Lambda at later layers use it with their own
+# theta and slope).  L5 exits are not predicted inside the recursion (their
+# confidence is unknown; the calibration sets of Eq. (36) are not part of
+# the step), so the recursion ranges over execute and skip.  L6 the
+# recursion stops at the last layer.  L7 the decision at the current layer
+# keeps the tie order of A14 on the totals f + Phi.
+# ----------------------------------------------------------------------------
+def cost_to_go(model, tables, l: int, h: int, x, d_hat: float, I: float, budget: float, pol,
+               m_logit, m_budget, memo=None):
+    """Phi_l^(h)(x, D-hat): the expected least cost of the next h layers
+    (Eq. (39)) for a token leaving layer l having run experts x."""
+    N = model["n_layers"]
+    if h == 0 or l >= N - 1:
+        return 0.0
+    key = (l, h, tuple(x), d_hat)
+    if memo is not None and key in memo:
+        return memo[key]
+    rows = model["layers"][l]["trans"]
+    nxt = model["layers"][l + 1]
+    sub_c, sub_q, sub_m = tables[l + 1]
+    acc = 0.0
+    for combo in _tuples([rows[e] for e in x]):
+        prob = 1.0
+        for _, pr in combo:
+            prob *= pr
+        if prob == 0.0:
+            continue
+        tau = [t for t, _ in combo]
+        m_budget.extend(sub_m[e] for e in tau if not nxt["local_mask"][e])
+        execs, skip, _, _, _ = step_options(tau, I, nxt["local_mask"], sub_c, sub_q, d_hat,
+                                            budget, nxt["theta"], nxt["skip_slope"], pol,
+                                            m_logit, m_budget)
+        cands = [(f, sq, xo) for (f, _, _, sq, xo) in execs]
+        if skip is not None:
+            cands.append(skip)
+        best = min(f + cost_to_go(model, tables, l + 1, h - 1, xo, d_hat + charge, I, budget,
+                                  pol, m_logit, m_budget, memo)
+                   for f, charge, xo in cands)
+        acc += prob * best
+    if memo is not None:
+        memo[key] = acc
+    return acc
+
+
+def _tuples(rows):
+    """Every choice of one entry per row, the first row varying slowest."""
+    if not rows:
+        yield ()
+        return
+    for head in rows[0]:
+        for rest in _tuples(rows[1:]):
+            yield (head,) + rest
 
 
 # ----------------------------------------------------------------------------
@@ -332,6 +421,13 @@ def layer_step(model, l: int, pol, state, token_budget=None, token_p_exit=None):
     local = [bool(v) for v in L["local_mask"]]
     sub_c, sub_q, sub_m = substitutes(L["sim"], local, pol["phi_scale"],
                                       pol["sim_min"])
+    # look-ahead over the next H - 1 layers (Eq. (39)); H = 1 is the myopic rule
+    H = int(pol.get("horizon", 1))
+    tables = {}
+    for j in range(l + 1, min(l + H, N)):
+        Lj = model["layers"][j]
+        tables[j] = substitutes(Lj["sim"], [bool(v) for v in Lj["local_mask"]],
+                                pol["phi_scale"], pol["sim_min"])
 
     tr = dict(action=np.zeros(T, np.int8),
               target=np.full((T, k), -1, np.int16),
@@ -341,6 +437,7 @@ def layer_step(model, l: int, pol, state, token_budget=None, token_p_exit=None):
               importance=np.full(T, math.nan),
               xi=np.full(T, math.nan), d_acc=np.full(T, math.nan),
               margin=np.full(T, _INF), margin_pre=np.full(T, _INF),
+              margin_logit=np.full(T, _INF), margin_budget=np.full(T, _INF),
               margin_exit=np.full(T, _INF), rows={})
 
     act_list = list(state["active"])
@@ -354,12 +451,24 @@ def layer_step(model, l: int, pol, state, token_budget=None, token_p_exit=None):
     for i, q in enumerate(act_list):
         S, w, I, _, m_route = route(Z[i], k, bool(model["normalize_topk"]))
         budget = pol["budget"] if token_budget is None else float(token_budget[q])
+        la_logit, la_budget = [], []
+        phi = None
+        if H > 1 and l < N - 1:
+            memo = {}
+
+            def phi(x, d, I=I, budget=budget, memo=memo):
+                return cost_to_go(model, tables, l, H - 1, x, d, I, budget, pol, la_logit,
+                                  la_budget, memo)
         dec = decide(S, w, I, local, sub_c, sub_q, state["d_acc"][q], budget,
-                     L["theta"], L["skip_slope"], pol)
-        m = min([m_route] + dec["margins"]
-                + [sub_m[e] for e in S if not local[e]])
+                     L["theta"], L["skip_slope"], pol, phi)
+        m_logit = min([m_route] + dec["margins_logit"] + la_logit)
+        m_budget = min(dec["margins_budget"] + la_budget
+                       + [sub_m[e] for e in S if not local[e]], default=_INF)
+        m = min(m_logit, m_budget)
         tr["margin"][q] = m
         tr["margin_pre"][q] = m
+        tr["margin_logit"][q] = m_logit
+        tr["margin_budget"][q] = m_budget
         tr["action"][q] = dec["action"]
         tr["target"][q] = S
         tr["gate"][q] = w
@@ -431,8 +540,11 @@ def _f64(t):
     return t.detach().to("cpu").to(torch.float64).numpy()
 
 
-def model_from_inputs(inputs, layers=None):
-    """fp64 numpy copy of generated inputs (exact widening of stored values)."""
+def model_from_inputs(inputs, layers=None, decision_layers=()):
+    """fp64 numpy copy of generated inputs (exact widening of stored values).
+
+    ``decision_layers``: further layers of which only what a look-ahead
+    reads is copied (placement, similarity, theta, slope, transitions)."""
     cfg = inputs["cfg"]
     sel = range(cfg["n_layers"]) if layers is None else layers
     out = dict(n_layers=cfg["n_layers"], n_experts=cfg["n_experts"],
@@ -449,8 +561,25 @@ def model_from_inputs(inputs, layers=None):
             b_exit=_f64(L["b_exit"]),
             local_mask=[int(v) for v in L["local_mask"].cpu()],
             sim=_f64(L["sim"]), theta=float(L["theta"]),
-            skip_slope=float(L["skip_slope"]))
+            skip_slope=float(L["skip_slope"]), trans=_trans_rows(L))
+    for l in decision_layers:
+        L = inputs["layers"][l]
+        out["layers"][l] = dict(local_mask=[int(v) for v in L["local_mask"].cpu()],
+                                sim=_f64(L["sim"]), theta=float(L["theta"]),
+                                skip_slope=float(L["skip_slope"]), trans=_trans_rows(L))
     return out
+
+
+def _trans_rows(L):
+    """Rows of P_l (reading L2): per source expert, its (target, probability)
+    entries in stored order, padding (target -1) dropped; None if absent."""
+    to, pr = L.get("trans_to"), L.get("trans_p")
+    if to is None:
+        return None
+    to = to.cpu().numpy()
+    pr = _f64(pr)
+    return [[(int(t), float(v)) for t, v in zip(to[e], pr[e]) if t >= 0]
+            for e in range(to.shape[0])]
 
 
 # ----------------------------------------------------------------------------

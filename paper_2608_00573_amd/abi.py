@@ -16,7 +16,7 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libtrimmoe.so")
 
-ABI_VERSION = 2   # TRIMMOE_ABI_VERSION this binding is written for
+ABI_VERSION = 3   # TRIMMOE_ABI_VERSION this binding is written for
 N_COUNTERS = 16   # per-layer trace counters (row stride of trimmoe_trace.counters)
 TRIMMOE_OK = 0
 STATUS = {0: "OK", -1: "ERR_NULL", -2: "ERR_SHAPE", -3: "ERR_DTYPE", -4: "ERR_POLICY",
@@ -33,7 +33,8 @@ class Layer(C.Structure):
                 ("ws_up", C.c_void_p), ("ws_gate", C.c_void_p), ("ws_down", C.c_void_p),
                 ("w_exit", C.c_void_p), ("b_exit", C.c_void_p),
                 ("local_mask", C.c_void_p), ("sim", C.c_void_p),
-                ("theta", C.c_float), ("skip_slope", C.c_float)]
+                ("theta", C.c_float), ("skip_slope", C.c_float),
+                ("trans_to", C.c_void_p), ("trans_p", C.c_void_p)]
 
 
 class Model(C.Structure):
@@ -41,14 +42,14 @@ class Model(C.Structure):
                 ("top_k", C.c_int32), ("d_ff", C.c_int32), ("d_ff_shared", C.c_int32),
                 ("vocab_exit", C.c_int32), ("dtype", C.c_int32), ("act", C.c_int32),
                 ("conf_mode", C.c_int32), ("normalize_topk", C.c_int32),
-                ("layers", C.POINTER(Layer))]
+                ("layers", C.POINTER(Layer)), ("trans_b", C.c_int32)]
 
 
 class Policy(C.Structure):
     _fields_ = [("p_exit", C.c_float), ("budget", C.c_float), ("omega_t", C.c_float),
                 ("t_local", C.c_float), ("t_remote", C.c_float), ("phi_scale", C.c_float),
                 ("sim_min", C.c_float), ("p_exit_tok", C.c_void_p),
-                ("budget_tok", C.c_void_p)]
+                ("budget_tok", C.c_void_p), ("horizon", C.c_int32)]
 
 
 class State(C.Structure):
@@ -217,7 +218,8 @@ class ModelHandle:
         arr = (Layer * n_layers)()
         for i, L in enumerate(layers):
             for key in ("w_router", "b_router", "w_up", "w_gate", "w_down", "ws_up", "ws_gate",
-                        "ws_down", "w_exit", "b_exit", "local_mask", "sim"):
+                        "ws_down", "w_exit", "b_exit", "local_mask", "sim", "trans_to",
+                        "trans_p"):
                 t = L.get(key)
                 if t is not None:
                     if not t.is_contiguous():
@@ -227,16 +229,18 @@ class ModelHandle:
             arr[i].theta = float(L["theta"])
             arr[i].skip_slope = float(L["skip_slope"])
         self.layers = arr
+        trans_b = next((int(L["trans_to"].shape[1]) for L in layers
+                        if L.get("trans_to") is not None), 0)
         self.model = Model(n_layers, d_model, n_experts, top_k, d_ff, d_ff_shared, vocab_exit,
                            dtype, act, conf_mode, normalize_topk,
-                           C.cast(arr, C.POINTER(Layer)))
+                           C.cast(arr, C.POINTER(Layer)), trans_b)
 
 
 def make_policy(*, p_exit, budget, omega_t, t_local, t_remote, phi_scale, sim_min,
-                p_exit_tok=None, budget_tok=None) -> Policy:
+                p_exit_tok=None, budget_tok=None, horizon=1) -> Policy:
     return Policy(p_exit, budget, omega_t, t_local, t_remote, phi_scale, sim_min,
                   None if p_exit_tok is None else p_exit_tok.data_ptr(),
-                  None if budget_tok is None else budget_tok.data_ptr())
+                  None if budget_tok is None else budget_tok.data_ptr(), int(horizon))
 
 
 class StateBuffers:

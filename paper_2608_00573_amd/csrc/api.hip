@@ -68,6 +68,27 @@ int validate_policy(const trimmoe_policy* p) {
   if (!(p->t_local >= 0.f) || !(p->t_remote >= 0.f) || isinf(p->t_local) || isinf(p->t_remote))
     return TRIMMOE_ERR_POLICY;
   if (!(p->phi_scale >= 0.f) || isinf(p->phi_scale)) return TRIMMOE_ERR_POLICY;
+  if (p->horizon < 1 || p->horizon > TRIMMOE_MAX_HORIZON) return TRIMMOE_ERR_POLICY;
+  return TRIMMOE_OK;
+}
+
+// The look-ahead's limits (policy.horizon > 1): its work per token grows as
+// (2^k + 1)^H * B^(k (H - 1)) cost evaluations.  Layers first..last run;
+// layer l reads the transitions of layers l .. l + H - 2 (not past N - 2).
+int validate_lookahead(const trimmoe_model* m, const trimmoe_policy* p, int first, int last) {
+  // the horizon the first layer run sees (later layers see no more)
+  const int H = std::min(p->horizon, m->n_layers - first);
+  if (H <= 1) return TRIMMOE_OK;
+  const int k = m->top_k, B = m->trans_b;
+  if (k > TRIMMOE_MAX_LOOKAHEAD_TOPK || B < 1 || B > TRIMMOE_MAX_TRANS_B) return TRIMMOE_ERR_SHAPE;
+  double tuples = 1.0;
+  for (int s = 0; s < k; ++s) tuples *= B;
+  const double opts = (double)((1 << k) + 1);
+  if (opts * tuples > kMaxBranches) return TRIMMOE_ERR_SHAPE;
+  if (pow(opts, H) * pow(tuples, H - 1) > (double)(1 << 21)) return TRIMMOE_ERR_SHAPE;
+  const int end = std::min(last + H - 1, m->n_layers - 1);
+  for (int l = first; l < end; ++l)
+    if (!m->layers[l].trans_to || !m->layers[l].trans_p) return TRIMMOE_ERR_NULL;
   return TRIMMOE_OK;
 }
 
@@ -166,6 +187,18 @@ void fill_params(LayerParams& P, const trimmoe_model* m, int l, const trimmoe_po
   P.sim_min = pol->sim_min;
   P.p_exit_tok = pol->p_exit_tok;
   P.budget_tok = pol->budget_tok;
+  P.horizon = std::min(pol->horizon, m->n_layers - l);
+  P.trans_b = m->trans_b;
+  for (int j = 0; j < kMaxLookahead; ++j) {
+    const bool later = j + 1 < P.horizon;  // layer l + j + 1 is looked at
+    const trimmoe_layer* Lj = later ? &m->layers[l + j + 1] : nullptr;
+    P.la_mask[j] = Lj ? Lj->local_mask : nullptr;
+    P.la_sim[j] = Lj ? Lj->sim : nullptr;
+    P.la_theta[j] = Lj ? Lj->theta : 0.f;
+    P.la_slope[j] = Lj ? Lj->skip_slope : 0.f;
+    P.la_tto[j] = j + 1 < P.horizon ? m->layers[l + j].trans_to : nullptr;
+    P.la_tp[j] = j + 1 < P.horizon ? m->layers[l + j].trans_p : nullptr;
+  }
   P.T = T;
   P.h = s->h;
   P.d_acc = s->d_acc;
@@ -253,6 +286,7 @@ int stack(const trimmoe_model* m, const trimmoe_policy* p, trimmoe_state* s,
   int rc = validate_model(m);
   if (rc) return rc;
   if ((rc = validate_policy(p))) return rc;
+  if ((rc = validate_lookahead(m, p, 0, m->n_layers - 1))) return rc;
   if ((rc = validate_state(m, s))) return rc;
   if ((rc = check_workspace(m, s, workspace, workspace_bytes))) return rc;
   const int per = TRIMMOE_TIMED_CLASSES + 1;
@@ -322,8 +356,9 @@ int trimmoe_layer_step(const trimmoe_model* m, int32_t layer, const trimmoe_poli
   int rc = validate_model(m);
   if (rc) return rc;
   if ((rc = validate_policy(p))) return rc;
-  if ((rc = validate_state(m, s))) return rc;
   if (layer < 0 || layer >= m->n_layers) return TRIMMOE_ERR_LAYER;
+  if ((rc = validate_lookahead(m, p, layer, layer))) return rc;
+  if ((rc = validate_state(m, s))) return rc;
   if ((rc = check_workspace(m, s, workspace, workspace_bytes))) return rc;
   return run_layer(m, layer, p, s, trace, workspace, static_cast<hipStream_t>(stream), nullptr,
                    1);

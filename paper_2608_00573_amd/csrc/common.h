@@ -35,6 +35,10 @@ inline int exit_tile_rows(bool bf16, int T) {
 constexpr int kF32Tile = 16;
 // per-layer trace counters (row stride of trimmoe_trace.counters)
 constexpr int kCounters = 16;
+// look-ahead: later layers a decision looks at, and first-level branches
+// (candidate action, next-layer target tuple) per token
+constexpr int kMaxLookahead = TRIMMOE_MAX_HORIZON - 1;
+constexpr int kMaxBranches = 1024;
 
 // slots of the small device counter block in the workspace
 enum CountSlot {
@@ -88,6 +92,15 @@ struct LayerParams {
   float p_exit, budget, omega_t, t_local, t_remote, phi_scale, sim_min;
   const float* p_exit_tok;
   const float* budget_tok;
+  // look-ahead (Eq. (39)): la_*[j - 1] describe layer + j for j = 1 ..
+  // horizon - 1; la_tto/la_tp[j] the transitions from layer + j to the next
+  int horizon;  // effective horizon: min(policy horizon, N - layer)
+  int trans_b;
+  const uint8_t* la_mask[kMaxLookahead];
+  const float* la_sim[kMaxLookahead];
+  float la_theta[kMaxLookahead], la_slope[kMaxLookahead];
+  const int16_t* la_tto[kMaxLookahead];
+  const float* la_tp[kMaxLookahead];
   // state
   int T;
   void* h;

@@ -79,13 +79,200 @@ static __host__ __device__ inline int route_ks(int E, int d) {
   return ks;
 }
 
-// One block = RB active tokens.  Phase 0: the layer's substitute table.
+// Eq. (3): best local substitute c(e) = argmin over local j != e with
+// Sim[e][j] >= sim_min of Q(e, j) = min(1, phi_scale (1 - Sim[e][j]) / 2),
+// ties to the lower j (-1: none), and its Q
+__device__ inline void best_substitute(const float* sim, const uint8_t* local, int E, int e,
+                                       float phi_scale, float sim_min, int& c, float& q) {
+  int best = -1;
+  float bq = 0.f;
+  for (int j = 0; j < E; ++j) {
+    if (j == e || !local[j]) continue;
+    const float sv = sim[(size_t)e * E + j];
+    if (!(sv >= sim_min)) continue;
+    const float qj = fminf(1.f, phi_scale * (1.f - sv) * 0.5f);
+    if (best < 0 || qj < bq) {
+      best = j;
+      bq = qj;
+    }
+  }
+  c = best;
+  q = bq;
+}
+
+// ------------------------------------------------ look-ahead (Eq. (39)) --
+// Cost-to-go of a token over the later layers of the horizon.  The token
+// never moves (one GPU), so it depends on an action only through the
+// experts the slots run (sources of the next-layer transitions) and the
+// budget the action leaves.  Level j is layer + j; its placement and
+// substitute table are at [j - 1], the transitions out of level j at [j].
+// Every slot moves independently (a tuple's probability is the product of
+// its slots'); the token's current importance stands in for later ones;
+// exits are not predicted.  All arrays live in the route block's LDS.
+struct LaView {
+  int E, k, B, ntup;          // ntup = B^k next-layer tuples
+  const uint8_t* mask;        // [horizon - 1][E]
+  const int16_t* subc;        // [horizon - 1][E]
+  const float* subq;          // [horizon - 1][E]
+  const int16_t* tto;         // [horizon - 1][E * B], -1 = padding
+  const float* tp;            // [horizon - 1][E * B]
+  const float* theta;         // [horizon - 1]
+  const float* slope;         // [horizon - 1]
+  float wt, wd, tl, tr;
+};
+
+// next-layer tuple `it` of sources x out of level j: targets and probability
+// (slot 0 is the most significant digit; padding entries give 0)
+__device__ inline float la_tuple(const LaView& v, int j, const int* x, int it, int* tau) {
+  const int16_t* to = v.tto + (size_t)j * v.E * v.B;
+  const float* pr = v.tp + (size_t)j * v.E * v.B;
+  int div = v.ntup;
+  float prob = 1.f;
+  for (int s = 0; s < v.k; ++s) {
+    div /= v.B;
+    const int dgt = (it / div) % v.B;
+    const int t = to[x[s] * v.B + dgt];
+    tau[s] = t < 0 ? 0 : t;
+    prob = t < 0 ? 0.f : prob * pr[x[s] * v.B + dgt];
+  }
+  return prob;
+}
+
+template <int R>
+__device__ float la_phi(const LaView& v, int j, const int* x, float D, float I, float b);
+
+// least per-step cost plus cost-to-go (R more levels) of the options at
+// level j for routed targets tau with D-hat = D: the rule of Eq. (31),
+// (32), (34), (35) and the importance admission at layer + j
+template <int R>
+__device__ float la_inner(const LaView& v, int j, const int* tau, float D, float I, float b) {
+  const int lev = j - 1;
+  const uint8_t* mask = v.mask + (size_t)lev * v.E;
+  const int16_t* subc = v.subc + (size_t)lev * v.E;
+  const float* subq = v.subq + (size_t)lev * v.E;
+  int n_loc = 0, n_rem = 0, nsub = 0;
+  int rs[TRIMMOE_MAX_LOOKAHEAD_TOPK];
+  float q[TRIMMOE_MAX_LOOKAHEAD_TOPK];
+  for (int s = 0; s < v.k; ++s) {
+    const int e = tau[s];
+    if (mask[e]) {
+      ++n_loc;
+      q[s] = 0.f;
+    } else {
+      ++n_rem;
+      const int c = subc[e];
+      q[s] = c >= 0 ? subq[e] : 0.f;
+      if (c >= 0) rs[nsub++] = s;
+    }
+  }
+  float best = __builtin_inff();
+  bool all_local = false;
+  for (int sel = 0; sel < (1 << nsub); ++sel) {
+    float sq = 0.f;
+    int ns = 0;
+    int x[TRIMMOE_MAX_LOOKAHEAD_TOPK];
+    for (int s = 0; s < v.k; ++s) x[s] = tau[s];
+    for (int u = 0; u < nsub; ++u)
+      if ((sel >> u) & 1) {
+        sq += q[rs[u]];
+        ++ns;
+        x[rs[u]] = subc[tau[rs[u]]];
+      }
+    if (D + sq <= b) {
+      if (ns == n_rem) all_local = true;
+      float f = v.wt * ((float)(n_loc + ns) * v.tl + (float)(n_rem - ns) * v.tr) +
+                (b > 0.f ? v.wd * sq / b : 0.f);
+      if constexpr (R > 0) f += la_phi<R>(v, j, x, D + sq, I, b);
+      best = fminf(best, f);
+    }
+  }
+  if (!all_local) {
+    const float lam = fminf(1.f, v.slope[lev] * I);
+    if (I <= v.theta[lev] && D + lam <= b) {
+      float f = b > 0.f ? v.wd * lam / b : 0.f;
+      if constexpr (R > 0) f += la_phi<R>(v, j, tau, D + lam, I, b);
+      best = fminf(best, f);
+    }
+  }
+  return best;
+}
+
+// Phi^(R): expectation over the next layer's tuples of la_inner<R - 1>
+template <int R>
+__device__ float la_phi(const LaView& v, int j, const int* x, float D, float I, float b) {
+  float acc = 0.f;
+  for (int it = 0; it < v.ntup; ++it) {
+    int tau[TRIMMOE_MAX_LOOKAHEAD_TOPK];
+    const float prob = la_tuple(v, j, x, it, tau);
+    if (prob != 0.f) acc += prob * la_inner<R - 1>(v, j + 1, tau, D, I, b);
+  }
+  return acc;
+}
+
+// la_inner at level 1 with `rem` further levels (horizon - 2)
+__device__ inline float la_inner_top(const LaView& v, int rem, const int* tau, float D, float I,
+                                     float b) {
+  if (rem == 0) return la_inner<0>(v, 1, tau, D, I, b);
+  if (rem == 1) return la_inner<1>(v, 1, tau, D, I, b);
+  return la_inner<2>(v, 1, tau, D, I, b);
+}
+
+// A route block's look-ahead LDS, after the logits: 4-byte arrays first,
+// then 2-byte, then bytes.  base == NULL only measures.  Returns bytes.
+struct LaLds {
+  float *tp, *subq, *theta, *slope;  // later layers (see LaView)
+  float* branch;                      // [waves][(2^k + 1) B^k] first-level values
+  float* phi;                         // [RB][2^kmax + 1] cost-to-go per option
+  float *tokI, *tokD, *tokB;          // [RB] importance, D-hat, budget
+  int* nsub;                          // [RB] substitutable remote slots
+  int16_t *tto, *subc;
+  uint8_t *mask, *skipok;             // skipok: [RB] skip admitted at this layer
+};
+
+__host__ __device__ inline int la_ntup(int B, int k) {
+  int n = 1;
+  for (int s = 0; s < k; ++s) n *= B;
+  return n;
+}
+
+__host__ __device__ inline size_t la_carve(char* base, int E, int B, int k, int nlev,
+                                           LaLds* o) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> char* {
+    char* q = base ? base + off : nullptr;
+    off += (bytes + 3) & ~(size_t)3;
+    return q;
+  };
+  const size_t branches = (size_t)((1 << k) + 1) * la_ntup(B, k);
+  LaLds tmp;
+  LaLds& L = o ? *o : tmp;
+  L.tp = (float*)take((size_t)nlev * E * B * 4);
+  L.subq = (float*)take((size_t)nlev * E * 4);
+  L.theta = (float*)take((size_t)nlev * 4);
+  L.slope = (float*)take((size_t)nlev * 4);
+  L.branch = (float*)take((size_t)kRouteWaves * branches * 4);
+  L.phi = (float*)take((size_t)RB * ((1 << TRIMMOE_MAX_LOOKAHEAD_TOPK) + 1) * 4);
+  L.tokI = (float*)take((size_t)RB * 4);
+  L.tokD = (float*)take((size_t)RB * 4);
+  L.tokB = (float*)take((size_t)RB * 4);
+  L.nsub = (int*)take((size_t)RB * 4);
+  L.tto = (int16_t*)take((size_t)nlev * E * B * 2);
+  L.subc = (int16_t*)take((size_t)nlev * E * 2);
+  L.mask = (uint8_t*)take((size_t)nlev * E);
+  L.skipok = (uint8_t*)take((size_t)RB);
+  return off;
+}
+
+// One block = RB active tokens.  Phase 0: the layer's substitute table
+// (and, with look-ahead, the later layers' tables and transitions).
 // Phase 1: router logits into LDS (MFMA 16x16x32 bf16 tiles, or fp32 FMA).
-// Phase 2: one thread per token runs the decision.  Phase 3: per-block
-// expert histogram for the bucketing.
-template <bool BF16>
+// Phase 2: one thread per token runs the decision; with look-ahead (LA) the
+// block first evaluates the cost-to-go of every candidate action of its
+// tokens, one wavefront per token, its lanes over (action, next-layer tuple)
+// branches.  Phase 3: per-block expert histogram for the bucketing.
+template <bool BF16, bool LA>
 __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
-  extern __shared__ float zs[];  // [route_ks][RB][E] logits, K partial sums
+  extern __shared__ float zs[];  // [route_ks][RB][E] logits, K partial sums; then LaLds
   __shared__ int s_cnt[TRIMMOE_MAX_EXPERTS];
   __shared__ int s_subc[TRIMMOE_MAX_EXPERTS];
   __shared__ float s_subq[TRIMMOE_MAX_EXPERTS];
@@ -105,24 +292,46 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   for (int e = threadIdx.x; e < E; e += blockDim.x) s_cnt[e] = 0;
   if (threadIdx.x == 0) s_xcnt = 0;
 
-  // Eq. (3): best local substitute c(e) = argmin over local j != e with
-  // Sim[e][j] >= sim_min of Q(e, j) = min(1, phi_scale (1 - Sim[e][j]) / 2),
-  // ties to the lower j (-1: none); Q of it in s_subq
+  // Eq. (3): the layer's substitute table
   for (int e = threadIdx.x; e < E; e += blockDim.x) {
-    int best = -1;
-    float bq = 0.f;
-    for (int j = 0; j < E; ++j) {
-      if (j == e || !p.local_mask[j]) continue;
-      const float sv = p.sim[(size_t)e * E + j];
-      if (!(sv >= p.sim_min)) continue;
-      const float q = fminf(1.f, p.phi_scale * (1.f - sv) * 0.5f);
-      if (best < 0 || q < bq) {
-        best = j;
-        bq = q;
-      }
+    int c;
+    float q;
+    best_substitute(p.sim, p.local_mask, E, e, p.phi_scale, p.sim_min, c, q);
+    s_subc[e] = c;
+    s_subq[e] = q;
+  }
+
+  LaLds la;
+  LaView lv;
+  const int nlev = LA ? p.horizon - 1 : 0;
+  if constexpr (LA) {
+    const int B = p.trans_b;
+    const int ks = BF16 ? route_ks(E, d) : 1;
+    la_carve(reinterpret_cast<char*>(zs + (size_t)ks * RB * E), E, B, k, nlev, &la);
+    // later layers: placement, substitute tables, theta and slope; the
+    // transitions out of this layer and every later one but the last
+    for (int idx = threadIdx.x; idx < nlev * E; idx += blockDim.x) {
+      const int j = idx / E, e = idx % E;
+      int c;
+      float q;
+      best_substitute(p.la_sim[j], p.la_mask[j], E, e, p.phi_scale, p.sim_min, c, q);
+      la.mask[idx] = p.la_mask[j][e] ? 1 : 0;
+      la.subc[idx] = (int16_t)c;
+      la.subq[idx] = q;
     }
-    s_subc[e] = best;
-    s_subq[e] = bq;
+    for (int idx = threadIdx.x; idx < nlev * E * B; idx += blockDim.x) {
+      const int j = idx / (E * B), r = idx % (E * B);
+      const int t = p.la_tto[j][r];
+      const bool ok = t >= 0 && t < E;  // anything else is padding
+      la.tto[idx] = (int16_t)(ok ? t : -1);
+      la.tp[idx] = ok ? p.la_tp[j][r] : 0.f;
+    }
+    if (threadIdx.x < nlev) {
+      la.theta[threadIdx.x] = p.la_theta[threadIdx.x];
+      la.slope[threadIdx.x] = p.la_slope[threadIdx.x];
+    }
+    lv = LaView{E, k, B, la_ntup(B, k), la.mask, la.subc, la.subq, la.tto, la.tp,
+                la.theta, la.slope, p.omega_t, 1.f - p.omega_t, p.t_local, p.t_remote};
   }
 
   if constexpr (BF16) {
@@ -218,9 +427,11 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   __syncthreads();
 
   const int i = threadIdx.x;
+  int pos = 0, t = 0, n_loc = 0, n_rem = 0, nsub = 0;
+  float I = 0.f, budget = 0.f, D = 0.f;
   if (i < nt) {
-    const int pos = base + i;
-    const int t = p.active_idx[pos];
+    pos = base + i;
+    t = p.active_idx[pos];
     float* z = zs + i * E;
     const float ninf = -__builtin_inff();
     for (int e = 0; e < E; ++e) {
@@ -250,7 +461,6 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     const float zmax = z[sS[i][0]];
     float sum = 0.f;
     for (int e = 0; e < E; ++e) sum += expf(z[e] - zmax);
-    float I = 0.f;
     for (int r = 0; r < k; ++r) {
       const float pr = expf(z[sS[i][r]] - zmax) / sum;
       sW[i][r] = pr;
@@ -260,7 +470,6 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
       for (int r = 0; r < k; ++r) sW[i][r] = sW[i][r] / I;
 
     // resolve slots: local exact, or remote with/without a local substitute
-    int n_loc = 0, n_rem = 0, nsub = 0;
     for (int r = 0; r < k; ++r) {
       const int e = sS[i][r];
       if (p.local_mask[e]) {
@@ -273,9 +482,77 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
         if (c >= 0) sRsub[i][nsub++] = r;
       }
     }
-    const float budget = p.budget_tok ? p.budget_tok[t] : p.budget;
-    const float D = p.d_acc[t];
+    budget = p.budget_tok ? p.budget_tok[t] : p.budget;
+    D = p.d_acc[t];
+  }
+
+  if constexpr (LA) {
+    // Eq. (39)-(40): cost-to-go of every candidate action of the block's
+    // tokens.  Options 0 .. 2^nsub - 1 execute (bit u substitutes slot
+    // sRsub[u]); option 2^nsub skips.  Every branch (option, next-layer
+    // tuple) is one lane's work; a wavefront takes one token at a time and
+    // sums the branches of each option in tuple order.
+    if (i < nt) {
+      la.tokI[i] = I;
+      la.tokD[i] = D;
+      la.tokB[i] = budget;
+      la.nsub[i] = nsub;
+      // the skip is a candidate iff Gamma > 0 (no feasible all-local
+      // assignment, Eq. (35)), I <= theta and the budget admits Lambda
+      float sq_all = 0.f;
+      for (int u = 0; u < nsub; ++u) sq_all += sQ[i][sRsub[i][u]];
+      const bool all_local = nsub == n_rem && D + sq_all <= budget;
+      const float lam = fminf(1.f, p.skip_slope * I);
+      la.skipok[i] = !all_local && I <= p.theta && D + lam <= budget;
+    }
+    __syncthreads();
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int ntup = lv.ntup, rem = nlev - 1;
+    float* br = la.branch + (size_t)wave * ((1 << k) + 1) * ntup;
+    for (int r = 0; r < RB / kRouteWaves; ++r) {
+      const int ti = wave + kRouteWaves * r;
+      const int nopt = ti < nt ? (1 << la.nsub[ti]) + 1 : 0;
+      for (int it = lane; it < nopt * ntup; it += 64) {
+        const int o = it / ntup, tup = it % ntup;
+        const int ns = la.nsub[ti];
+        const float Dt = la.tokD[ti], bt = la.tokB[ti], It = la.tokI[ti];
+        int x[TRIMMOE_MAX_LOOKAHEAD_TOPK];
+        for (int s = 0; s < k; ++s) x[s] = sS[ti][s];
+        float charge = 0.f;
+        bool feasible;
+        if (o < (1 << ns)) {
+          for (int u = 0; u < ns; ++u)
+            if ((o >> u) & 1) {
+              const int s = sRsub[ti][u];
+              charge += sQ[ti][s];
+              x[s] = s_subc[sS[ti][s]];
+            }
+          feasible = Dt + charge <= bt;
+        } else {
+          charge = fminf(1.f, p.skip_slope * It);
+          feasible = la.skipok[ti] != 0;
+        }
+        float val = 0.f;
+        if (feasible) {
+          int tau[TRIMMOE_MAX_LOOKAHEAD_TOPK];
+          const float prob = la_tuple(lv, 0, x, tup, tau);
+          if (prob != 0.f) val = prob * la_inner_top(lv, rem, tau, Dt + charge, It, bt);
+        }
+        br[it] = val;
+      }
+      __syncthreads();
+      if (lane < nopt) {
+        float acc = 0.f;
+        for (int u = 0; u < ntup; ++u) acc += br[lane * ntup + u];
+        la.phi[ti * ((1 << TRIMMOE_MAX_LOOKAHEAD_TOPK) + 1) + lane] = acc;
+      }
+      __syncthreads();
+    }
+  }
+
+  if (i < nt) {
     const float wt = p.omega_t, wd = 1.f - p.omega_t;
+    const float* phi = LA ? la.phi + i * ((1 << TRIMMOE_MAX_LOOKAHEAD_TOPK) + 1) : nullptr;
     // Eq. (34) + Eq. (31): enumerate substitution subsets of remote slots
     bool have = false, all_local = false;
     float bf = 0.f, bsq = 0.f;
@@ -292,8 +569,9 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
       if (!(D + sq <= budget)) continue;
       const int ns = __popc(sel);
       if (ns == n_rem) all_local = true;
-      const float f = wt * ((float)(n_loc + ns) * p.t_local + (float)(n_rem - ns) * p.t_remote) +
-                      (budget > 0.f ? wd * sq / budget : 0.f);
+      float f = wt * ((float)(n_loc + ns) * p.t_local + (float)(n_rem - ns) * p.t_remote) +
+                (budget > 0.f ? wd * sq / budget : 0.f);
+      if constexpr (LA) f += phi[sel];  // Eq. (40): per-step cost + cost-to-go
       const bool better = !have || f < bf || (f == bf && (ns < bns || (ns == bns && mask < bmask)));
       if (better) {
         have = true;
@@ -307,7 +585,8 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     const float lam = fminf(1.f, p.skip_slope * I);
     bool skip = false;
     if (!all_local && I <= p.theta && D + lam <= budget) {
-      const float fs = budget > 0.f ? wd * lam / budget : 0.f;
+      float fs = budget > 0.f ? wd * lam / budget : 0.f;
+      if constexpr (LA) fs += phi[1 << nsub];
       skip = fs < bf;
     }
     if (!have) skip = false;  // unreachable: the empty assignment is feasible
@@ -668,11 +947,23 @@ hipError_t launch_trace_fill(const LayerParams& p, int n_layers, hipStream_t st)
 
 hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st) {
   const int nb = cdiv(p.T, RB);
-  const size_t lds = (size_t)(bf16 ? route_ks(p.E, p.d) : 1) * RB * p.E * sizeof(float);
-  if (bf16)
-    hipLaunchKernelGGL(k_route<true>, dim3(nb), dim3(64 * kRouteWaves), lds, st, p);
-  else
-    hipLaunchKernelGGL(k_route<false>, dim3(nb), dim3(64 * kRouteWaves), lds, st, p);
+  size_t lds = (size_t)(bf16 ? route_ks(p.E, p.d) : 1) * RB * p.E * sizeof(float);
+  const dim3 grid(nb), block(64 * kRouteWaves);
+  if (p.horizon > 1) {
+    lds += la_carve(nullptr, p.E, p.trans_b, p.k, p.horizon - 1, nullptr);
+    auto kern = bf16 ? k_route<true, true> : k_route<false, true>;
+    if (lds > 65536) {
+      const hipError_t e =
+          hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                              (int)lds);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, grid, block, lds, st, p);
+  } else if (bf16) {
+    hipLaunchKernelGGL((k_route<true, false>), grid, block, lds, st, p);
+  } else {
+    hipLaunchKernelGGL((k_route<false, false>), grid, block, lds, st, p);
+  }
   return hipGetLastError();
 }
 

@@ -26,7 +26,13 @@ Recipe (all draws from ``synthgen.rng``; ``sigma`` = 0.02 unless noted):
 * importance thresholds theta_l ~ U(0,1) (sorted ascending over depth when
   ``theta_sorted``); skip-degradation slopes s_l = (budget/2)/max(theta_l,
   0.05), i.e. a linear degradation curve whose tolerance is the budget
-  spread over two expected skips.
+  spread over two expected skips;
+* expert transitions P_l (l < N-1, used by the look-ahead): for each source
+  expert e a support of ``trans_support`` = B distinct next-layer experts
+  (the first B of a seeded permutation) with probabilities proportional to
+  u^3, u ~ U(0,1) per entry (peaked rows, as calibration counts of a
+  routing with layer-to-layer correlation would give), stored as fp32 and
+  used as stored.
 
 Everything is returned in the storage dtype (bf16 or fp32) on ``device``.
 """
@@ -43,6 +49,7 @@ SIGMA = 0.02
 # tensor ids: per-layer ids are (layer + 1) << 16 | kind << 10 | expert
 _K_UP, _K_GATE, _K_DOWN, _K_SUP, _K_SGATE, _K_SDOWN = 1, 2, 3, 4, 5, 6
 _K_ROUTER, _K_ZIPF_PERM, _K_LOCAL_PERM, _K_ALPHA = 7, 8, 9, 10
+_K_TRANS_PERM, _K_TRANS_P = 11, 12
 _ID_WLM = 1 << 40
 _ID_THETA = (1 << 40) + 1
 _ID_H0 = (1 << 40) + 16
@@ -169,11 +176,31 @@ def make_layer(cfg, layer: int, w_lm: torch.Tensor, device="cpu") -> dict:
     theta = float(torch.tensor(theta_all[layer].item(), dtype=torch.float32))
     slope = float(torch.tensor((cfg["budget"] / 2.0) / max(theta, 0.05),
                                dtype=torch.float32))
+    trans_to, trans_p = transitions(cfg, layer)
     return dict(w_router=w_router, b_router=b_router, w_up=w_up, w_gate=w_gate,
                 w_down=w_down, ws_up=ws_up, ws_gate=ws_gate, ws_down=ws_down,
                 w_exit=w_exit, b_exit=None, local_mask=mask.to(device),
                 sim=sim.to(device), theta=theta, skip_slope=slope,
+                trans_to=None if trans_to is None else trans_to.to(device),
+                trans_p=None if trans_p is None else trans_p.to(device),
                 twin=twin, alpha=alpha, gamma=g32)
+
+
+def transitions(cfg, layer: int):
+    """P_layer as (targets int16 [E, B], probabilities fp32 [E, B]); (None,
+    None) for the last layer."""
+    E, N = cfg["n_experts"], cfg["n_layers"]
+    if layer >= N - 1:
+        return None, None
+    B = min(int(cfg.get("trans_support", 4)), E)
+    to = torch.empty(E, B, dtype=torch.int16)
+    pr = torch.empty(E, B, dtype=torch.float32)
+    for e in range(E):
+        perm = permutation(cfg["seed"], _lid(layer, _K_TRANS_PERM, e), E)
+        u = uniform_f64(cfg["seed"], _lid(layer, _K_TRANS_P, e), B) ** 3
+        to[e] = perm[:B].to(torch.int16)
+        pr[e] = (u / u.sum()).to(torch.float32)
+    return to, pr
 
 
 def exit_lm(cfg, device="cpu") -> torch.Tensor:
@@ -224,6 +251,7 @@ def make_inputs(cfg, device="cpu", token_seed: int | None = None,
     policy = {k: cfg[k] for k in ("budget", "omega_t", "t_local", "t_remote",
                                   "phi_scale", "sim_min")}
     policy["p_exit"] = cfg["p_exit"]
+    policy["horizon"] = int(cfg.get("horizon", 1))
     return dict(cfg=cfg, layers=layers, h0=h0, policy=policy)
 
 

@@ -105,9 +105,14 @@ XI_RTOL_FORCED_BF16 = 2e-3
 
 
 def compare_stack(cfg, ref_state, ref_traces, gst, gtr, band=BAND, tol=None, layer0=0,
-                  excluded=None, ftol=None, band_exit=None):
+                  excluded=None, ftol=None, band_exit=None, band_budget=None):
     """Compare a GPU stack (or a suffix of it starting at layer0) with the oracle.
 
+    band_budget: when given, the oracle's budget comparisons (D-hat plus a
+    charge against the budget, substitute-table ties: quantities the GPU
+    computes from the same stored Sim values, so to within fp32 rounding)
+    get this band and only the importance, logit and cost margins get
+    `band`; otherwise every pre-FFN margin gets `band`.
     Returns a dict of statistics; raises AssertionError on any mismatch.
     """
     tol = TOL[cfg["dtype"]] if tol is None else tol
@@ -121,7 +126,11 @@ def compare_stack(cfg, ref_state, ref_traces, gst, gtr, band=BAND, tol=None, lay
         act_r = rtr["action"]
         live = act_r != O.ACT_INACTIVE
         bx = band if band_exit is None else band_exit
-        inband = live & ((rtr["margin_pre"] <= band) | (rtr["margin_exit"] <= bx))
+        if band_budget is None:
+            pre = rtr["margin_pre"] <= band
+        else:
+            pre = (rtr["margin_logit"] <= band) | (rtr["margin_budget"] <= band_budget)
+        inband = live & (pre | (rtr["margin_exit"] <= bx))
         excl |= inband
         cmp = live & ~excl
         stats["compared"] += int(cmp.sum())

@@ -174,3 +174,56 @@ def test_layer_step_rejects_bad_layer_workspace_and_state():
     assert rc == -1
     assert torch.count_nonzero(keep) == 0
     assert torch.count_nonzero(ws) == 0
+
+
+def _la_layers(n, E, B, with_trans=True):
+    layers = _fake_layers(n, E)
+    to = torch.zeros(E, B, dtype=torch.int16)
+    pr = torch.zeros(E, B, dtype=torch.float32)
+    for i, L in enumerate(layers):
+        L["trans_to"] = to if with_trans and i < n - 1 else None
+        L["trans_p"] = pr if with_trans and i < n - 1 else None
+    return layers
+
+
+@pytest.mark.parametrize("over,B,horizon,code", [
+    (dict(), 4, 5, -4),                      # horizon above the maximum
+    (dict(), 4, 0, -4),                      # horizon below 1
+    (dict(n_experts=16, top_k=5), 2, 2, -2),  # look-ahead needs top-k <= 4
+    (dict(), 9, 2, -2),                      # rows of more than 8 entries
+    (dict(n_experts=16, top_k=4), 3, 2, -2),  # 17 * 81 first-level branches > 1024
+    (dict(n_layers=4, top_k=2), 8, 4, -2),   # 5^4 * 64^3 evaluations > 2^21
+])
+def test_look_ahead_limits_rejected_before_launch(over, B, horizon, code):
+    dims = dict(DIMS, **over)
+    mh = abi.model_handle(dims, _la_layers(dims["n_layers"], dims["n_experts"], B))
+    st, keep = _state_stub()
+    pol = abi.make_policy(**POL, horizon=horizon)
+    rc = abi.lib().trimmoe_stack_forward(C.byref(mh.model), C.byref(pol), C.byref(st), None,
+                                         None, 0, None)
+    assert rc == code
+    assert torch.count_nonzero(keep) == 0
+
+
+def test_look_ahead_needs_the_transitions_a_decision_reads():
+    dims = dict(DIMS, n_layers=3)
+    mh = abi.model_handle(dims, _la_layers(3, 8, 4, with_trans=False))
+    st, _ = _state_stub()
+    st.xi = None  # a call that passes the look-ahead checks stops at the state
+    pol = abi.make_policy(**POL, horizon=2)
+    L = abi.lib()
+    assert L.trimmoe_stack_forward(C.byref(mh.model), C.byref(pol), C.byref(st), None, None, 0,
+                                   None) == -2   # trans_b = 0
+    mh = abi.model_handle(dims, _la_layers(3, 8, 4))
+    mh.layers[1].trans_to = None
+    assert L.trimmoe_stack_forward(C.byref(mh.model), C.byref(pol), C.byref(st), None, None, 0,
+                                   None) == -1   # layer 1's decision reads P_1
+    # layer 0 at H = 2 reads only P_0; the last layer reads nothing
+    for layer in (0, 2):
+        assert L.trimmoe_layer_step(C.byref(mh.model), layer, C.byref(pol), C.byref(st), None,
+                                    None, 0, None) == -1   # the NULL state member
+    assert L.trimmoe_layer_step(C.byref(mh.model), 1, C.byref(pol), C.byref(st), None, None, 0,
+                                None) == -1
+    pol3 = abi.make_policy(**POL, horizon=3)
+    assert L.trimmoe_layer_step(C.byref(mh.model), 0, C.byref(pol3), C.byref(st), None, None, 0,
+                                None) == -1

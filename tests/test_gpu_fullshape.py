@@ -25,13 +25,16 @@ pytestmark = pytest.mark.gpu
 
 def _full_layer(name, layer, n_sample, seed, **over):
     cfg = workload(name, **over)
-    N, T, k = cfg["n_layers"], cfg["n_tokens"], cfg["top_k"]
+    N, T, k, H = cfg["n_layers"], cfg["n_tokens"], cfg["top_k"], cfg["horizon"]
     dev = torch.device("cuda:0")
-    log(f"[fullshape] {name} layer {layer} T={T}: generating inputs on the GPU")
-    inp = make_inputs(cfg, device=dev, layers=[layer])
+    ahead = list(range(layer + 1, min(layer + H, N)))  # layers the look-ahead reads
+    log(f"[fullshape] {name} layer {layer} T={T} H={H}: generating inputs on the GPU")
+    inp = make_inputs(cfg, device=dev, layers=[layer] + ahead)
     L = inp["layers"][layer]
-    # only slot `layer` of the model is read by trimmoe_layer_step
-    mh = abi.model_handle(cfg, [L] * N)
+    # trimmoe_layer_step reads slot `layer` (and, looking ahead, the
+    # decision inputs of the next H - 1 slots); the others repeat it
+    mh = abi.model_handle(cfg, [inp["layers"][j] if inp["layers"][j] is not None else L
+                                for j in range(N)])
     ws = abi.alloc_workspace(mh.model, T, dev)
     policy = abi.make_policy(**inp["policy"])
 
@@ -68,7 +71,7 @@ def _full_layer(name, layer, n_sample, seed, **over):
                active=[i for i, t in enumerate(idx) if t in aset],
                exit_layer=before["exit_layer"][idx].copy(), xi=before["xi"][idx].copy())
     log(f"[fullshape] {name} layer {layer}: oracle on {len(idx)} sampled tokens")
-    model = O.model_from_inputs(inp, layers=[layer])
+    model = O.model_from_inputs(inp, layers=[layer], decision_layers=ahead)
     pol = policy32(inp["policy"])
     rtr = O.layer_step(model, layer, pol, sub)
     g_sub = {key: v[:, idx] for key, v in gtr.items() if key != "counters"}
@@ -158,3 +161,12 @@ def test_mixtral_decode_full_layer_every_token():
     # 32 tokens: the oracle checks all of them
     stats, _, _ = _full_layer("mixtral_8x7b_decode", 16, n_sample=32, seed=34)
     assert stats["sampled"] == 32
+
+
+@pytest.mark.parametrize("layer", [16, 30, 31])
+def test_mixtral_decode_full_layer_look_ahead(layer):
+    # H = 3 over 8 experts top-2 with 4-entry transition rows (16 tuples per
+    # level); at layer 30 the horizon is cut to 2, at the last layer to 1
+    stats, _, _ = _full_layer("mixtral_8x7b_decode", layer, n_sample=32, seed=35 + layer,
+                              horizon=3)
+    assert stats["sampled"] == 32 and stats["compared"] >= 16

@@ -1,0 +1,112 @@
+"""GPU parity of the look-ahead decision (Sec. V-E, Eq. (38)-(40), H > 1).
+
+Whole stacks through trimmoe_stack_forward against the oracle, on a recipe
+where the look-ahead changes decisions (remote slots cost 2 local ones and
+the delay weight is 0.2, so spending budget now competes with saving it for
+later layers).  fp32 stacks use a 1e-5 band for importance and cost margins
+and 1e-7 for budget comparisons (both sides compute D-hat from the same
+stored Sim values); bf16 stacks keep the 1e-3 band and 1e-4 for budgets.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from paper_2608_00573_amd import abi
+from synthgen import make_inputs, workload
+
+from gpu_harness import (GpuRun, check_invariants_gpu, compare_stack, gpu_state_np,
+                         gpu_trace_np, log, oracle_run, policy32)
+
+pytestmark = pytest.mark.gpu
+
+RECIPE = dict(t_remote=2.0, omega_t=0.2)
+
+
+def _stack(cfg, band, band_budget):
+    inp = make_inputs(cfg)
+    log(f"[lookahead] {cfg['dtype']} T={cfg['n_tokens']} N={cfg['n_layers']} "
+        f"k={cfg['top_k']} B={cfg['trans_support']} H={cfg['horizon']}")
+    g = GpuRun(inp)
+    st, tr = g.stack()
+    gst, gtr = gpu_state_np(st), gpu_trace_np(tr)
+    ref_state, ref_traces = oracle_run(inp)
+    stats = compare_stack(cfg, ref_state, ref_traces, gst, gtr, band=band,
+                          band_budget=band_budget)
+    check_invariants_gpu(cfg, policy32(inp["policy"]), gst, gtr)
+    log(f"[lookahead] ok {stats}")
+    return inp, g, gtr, stats
+
+
+def _decisions_differ(g, gtr, inp):
+    """(token, layer) decisions of the GPU at H = 1 that differ from gtr's."""
+    st1, tr1 = g.stack(pol=dict(inp["policy"], horizon=1))
+    t1 = gpu_trace_np(tr1)
+    return int(((t1["action"] != gtr["action"]) | np.any(t1["exec"] != gtr["exec"], axis=2)).sum())
+
+
+def test_top1_horizon3():
+    cfg = workload("tiny_fp32", n_layers=4, horizon=3, **RECIPE)
+    inp, g, gtr, stats = _stack(cfg, 1e-5, 1e-7)
+    assert stats["excluded_tokens"] <= 4
+    assert _decisions_differ(g, gtr, inp) >= 5
+
+
+def test_top2_horizon3():
+    cfg = workload("tiny_fp32", n_layers=4, top_k=2, normalize_topk=1, horizon=3, **RECIPE)
+    inp, g, gtr, stats = _stack(cfg, 1e-5, 1e-7)
+    assert stats["excluded_tokens"] <= 6
+    assert _decisions_differ(g, gtr, inp) >= 5
+
+
+def test_horizon4_full_transition_rows():
+    # H = 4 (three later layers) and 8-entry rows over 8 experts
+    cfg = workload("tiny_fp32", n_layers=5, horizon=4, trans_support=8, **RECIPE)
+    _, _, _, stats = _stack(cfg, 1e-5, 1e-7)
+    assert stats["excluded_tokens"] <= 4 and stats["compared"] > 150
+
+
+def test_ragged_tokens_horizon2():
+    # 333 tokens: eleven route blocks, the last one ragged
+    cfg = workload("tiny_fp32", n_layers=3, n_tokens=333, top_k=2, normalize_topk=1, horizon=2,
+                   **RECIPE)
+    _, _, _, stats = _stack(cfg, 1e-5, 1e-7)
+    assert stats["compared"] > 600
+
+
+@pytest.mark.parametrize("H", [2, 3])
+def test_bf16_swiglu_top2_shared(H):
+    cfg = workload("tiny_fp32", dtype="bf16", act="swiglu", top_k=2, normalize_topk=1,
+                   n_layers=4, n_tokens=512, d_model=128, d_ff=256, d_ff_shared=128,
+                   horizon=H, **RECIPE)
+    _, _, _, stats = _stack(cfg, 1e-3, 1e-4)
+    assert stats["compared"] >= 0.8 * 512
+
+
+def test_top4_sixty_experts_two_entry_rows():
+    # Qwen-like routing: 60 experts top-4 (17 candidate actions, 16 tuples
+    # per level with 2-entry rows), horizon 2
+    cfg = workload("tiny_fp32", n_layers=3, n_experts=60, n_local=20, top_k=4, horizon=2,
+                   trans_support=2, n_tokens=128, **RECIPE)
+    _, _, _, stats = _stack(cfg, 1e-5, 1e-7)
+    assert stats["compared"] > 200
+
+
+def test_validation_of_look_ahead_limits():
+    cfg = workload("tiny_fp32", n_layers=3, horizon=2)
+    inp = make_inputs(cfg)
+    g = GpuRun(inp)
+    st = abi.StateBuffers(inp["h0"].to(g.dev).clone())
+    for pol, err in ((dict(inp["policy"], horizon=5), abi.TrimmoeError),
+                     (dict(inp["policy"], horizon=0), abi.TrimmoeError)):
+        with pytest.raises(err):
+            abi.trimmoe_stack_forward(g.mh.model, g.policy(pol), st.state, None, g.ws)
+    # transitions missing on a layer the decision reads
+    layers = [dict(L) for L in g.layers]
+    layers[0]["trans_to"] = None
+    mh = abi.model_handle(cfg, layers)
+    with pytest.raises(abi.TrimmoeError):
+        abi.trimmoe_stack_forward(mh.model, g.policy(), st.state, None, g.ws)
+    # ...but layer 1 alone at H = 2 reads only P_1
+    abi.trimmoe_layer_step(mh.model, 1, g.policy(), st.state, None, g.ws)
+    torch.cuda.synchronize()
