@@ -65,6 +65,10 @@ def parse():
     ap.add_argument("--kappa", type=float, default=0.2,
                     help="step size of the delay/quality weight update")
     ap.add_argument("--p-floor", type=float, default=0.1, help="lower bound of p_J")
+    ap.add_argument("--offline", action="store_true",
+                    help="also time the offline stage (calibration pass on the GPU, "
+                         "statistics, transition rows, placement over 10 servers) and the "
+                         "oracle's placement")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (to scale HBM byte "
                          "counters) and exit")
@@ -236,6 +240,40 @@ def feedback_loop(abi, cfg, mh, pol0, batches, K, window, ws, eta, kappa, p_floo
     e1.record(stream)
     torch.cuda.synchronize()
     return e0.elapsed_time(e1), traj
+
+
+def offline_stage(abi, cfg, mh, inp, h0, ws):
+    """Table I on this workload: the calibration pass over the batch, the
+    Sec. IV-C statistics and Eq. (38) rows (4 entries), and the Eq. (28)
+    greedy replication over 10 synthetic servers with memory ratio 2, each
+    timed; the oracle's placement of the same instance timed beside it."""
+    import numpy as np
+    import torch
+
+    from oracle import placement as P
+    from paper_2608_00573_amd import offline
+    from synthgen.servers import make_servers
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    rec = offline.calibration_pass(mh.model, inp["policy"], h0, ws)
+    t1 = time.perf_counter()
+    theta = [L["theta"] for L in inp["layers"]]
+    tab = offline.offline_tables(rec, inp["policy"]["p_exit"], theta, cfg["n_experts"],
+                                 min(4, cfg["n_experts"]))
+    t2 = time.perf_counter()
+    srv = make_servers(cfg, n_servers=10, memory_ratio=2.0)
+    x, added = offline.place(tab, srv)
+    t3 = time.perf_counter()
+    wx, placed = P.place_replicas(tab["lam"], srv["rho"], srv["z"], srv["nbytes"],
+                                  srv["capacity"], srv["bandwidth"], srv["latency"], srv["x0"])
+    t4 = time.perf_counter()
+    return {"calibration_tokens": int(h0.shape[0]), "servers": 10, "memory_ratio": 2.0,
+            "calibration_pass_s": t1 - t0, "statistics_and_transitions_s": t2 - t1,
+            "placement_s": t3 - t2, "replicas_added": added,
+            "oracle_placement_s": t4 - t3, "placement_matches_oracle": bool(np.array_equal(x, wx)),
+            "pi": [round(float(v), 4) for v in tab["pi"]],
+            "home_experts_per_layer": x[srv["home"]].sum(axis=1).tolist()}
 
 
 def main():
@@ -419,6 +457,8 @@ def main():
             "observation_cost_frac": ms_obs / ms_total - 1.0,
             "p_exit_start": inp["policy"]["p_exit"], "omega_t_start": inp["policy"]["omega_t"],
             "windows": traj}
+    if args.offline:
+        out["offline"] = offline_stage(abi, cfg, mh, inp, batches[0], ws)
     if not args.no_cpu_baseline:
         inp["h0"] = batches[0]
         out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)

@@ -311,6 +311,70 @@ int trimmoe_window_stats(const trimmoe_model* m, const trimmoe_policy* p,
 int trimmoe_feedback_update(trimmoe_policy* p, const double* stats, double eta,
                             double kappa, double p_floor);
 
+/*
+ * Offline statistics and replica placement (Table I), host-only functions:
+ * all pointers are host memory owned by the caller; arguments are checked
+ * before anything is written.
+ *
+ * A calibration record is what a full-depth exact pass of the stack writes
+ * into its trace (budget 0 and a confidence requirement above 1, so that
+ * nothing is skipped, substituted or exited): trace->target [N, Q, k],
+ * trace->importance [N, Q], trace->xi [N, Q] (NaN where not evaluated).
+ *
+ * trimmoe_calib_exit_layers: per calibration token, the first layer l < N - 1
+ * whose confidence xi[l][q] >= p_exit (0-based), else N: the layer after
+ * which the exit gate of Eq. (8) would let it leave.
+ */
+int trimmoe_calib_exit_layers(int32_t n_layers, int32_t n_tokens, const float* xi, float p_exit,
+                              int32_t* exit_layer);
+
+/*
+ * Execution-frequency statistics of Sec. IV-C: pi[l] (Eq. (26)) the
+ * fraction of tokens active entering layer l (exit_layer[q] >= l);
+ * act[l][e] the fraction of those whose routed set contains e; sigma[l][e]
+ * (Eq. (27)) the fraction of the latter whose importance exceeds theta[l]
+ * (0 when none); lambda = pi * sigma * act.  target [N, Q, k] int16 in
+ * [0, E); outputs fp64, [N] and [N, E].
+ */
+int trimmoe_calib_stats(int32_t n_layers, int32_t n_tokens, int32_t n_experts, int32_t top_k,
+                        const int16_t* target, const float* importance,
+                        const int32_t* exit_layer, const float* theta, double* pi, double* act,
+                        double* sigma, double* lambda);
+
+/*
+ * Expert transition statistics P_l (Eq. (38)) for l < N - 1 from a
+ * calibration record, in the layout the look-ahead reads: row e of layer l
+ * holds the trans_b most frequent next-layer experts (ties to the lower
+ * id), probabilities renormalised over them, padded with (-1, 0).  With
+ * top-k every (routed at l, routed at l + 1) pair of a token active at both
+ * layers counts once.  trans_to / trans_p: [N - 1, E, trans_b];
+ * 1 <= trans_b <= E.
+ */
+int trimmoe_calib_transitions(int32_t n_layers, int32_t n_tokens, int32_t n_experts,
+                              int32_t top_k, const int16_t* target, const int32_t* exit_layer,
+                              int32_t trans_b, int16_t* trans_to, float* trans_p);
+
+/*
+ * Communication-aware greedy replication (Table I, lines 9-13): starting
+ * from the baseline deployment x [M, N, E] (1 = expert (l, e) on server m),
+ * which must satisfy (c.1)-(c.3), repeatedly place the replica of largest
+ * redundancy benefit B = lambda[l][e] * rho[m][l] * (z[l] / mean bandwidth
+ * + mean latency) (Eq. (28); means over the servers hosting the expert,
+ * from bandwidth / latency [M, M]) among the pairs not yet placed that fit
+ * the server's residual memory (capacity [M], nbytes [N, E]); ties to the
+ * lower layer, expert, server; stop when no positive benefit fits.  x is
+ * updated in place; *n_placed = replicas added.  By Property 1 the result
+ * satisfies (c.1)-(c.3).  A baseline that violates them: TRIMMOE_ERR_SHAPE;
+ * negative, NaN or infinite inputs (bandwidth must be > 0):
+ * TRIMMOE_ERR_POLICY.  Row x[m] of the result is the local_mask of every
+ * layer for a device playing server m.
+ */
+int trimmoe_place_replicas(int32_t n_servers, int32_t n_layers, int32_t n_experts,
+                           const double* lambda, const double* rho, const double* z,
+                           const double* nbytes, const double* capacity,
+                           const double* bandwidth, const double* latency, uint8_t* x,
+                           int32_t* n_placed);
+
 #ifdef __cplusplus
 }
 #endif

@@ -11,6 +11,8 @@ from __future__ import annotations
 import ctypes as C
 import os
 
+import numpy as np
+
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -66,7 +68,9 @@ class Trace(C.Structure):
 
 EXPORTS = ["trimmoe_abi_version", "trimmoe_status_str", "trimmoe_workspace_size",
            "trimmoe_state_reset", "trimmoe_layer_step", "trimmoe_stack_forward",
-           "trimmoe_stack_forward_timed", "trimmoe_window_stats", "trimmoe_feedback_update"]
+           "trimmoe_stack_forward_timed", "trimmoe_window_stats", "trimmoe_feedback_update",
+           "trimmoe_calib_exit_layers", "trimmoe_calib_stats", "trimmoe_calib_transitions",
+           "trimmoe_place_replicas"]
 TIMED_CLASSES = ["route", "bucket", "up", "down", "shared", "combine", "exit", "gate"]
 
 _lib = None
@@ -107,6 +111,16 @@ def lib():
         L.trimmoe_feedback_update.restype = C.c_int
         L.trimmoe_feedback_update.argtypes = [C.POINTER(Policy), C.POINTER(C.c_double),
                                               C.c_double, C.c_double, C.c_double]
+        i32, f32, p = C.c_int32, C.c_float, C.c_void_p
+        L.trimmoe_calib_exit_layers.restype = C.c_int
+        L.trimmoe_calib_exit_layers.argtypes = [i32, i32, p, f32, p]
+        L.trimmoe_calib_stats.restype = C.c_int
+        L.trimmoe_calib_stats.argtypes = [i32, i32, i32, i32, p, p, p, p, p, p, p, p]
+        L.trimmoe_calib_transitions.restype = C.c_int
+        L.trimmoe_calib_transitions.argtypes = [i32, i32, i32, i32, p, p, i32, p, p]
+        L.trimmoe_place_replicas.restype = C.c_int
+        L.trimmoe_place_replicas.argtypes = [i32, i32, i32, p, p, p, p, p, p, p, p,
+                                             C.POINTER(C.c_int32)]
         if L.trimmoe_abi_version() != ABI_VERSION:
             raise RuntimeError(f"{LIB_PATH} has ABI version {L.trimmoe_abi_version()}, the "
                                f"binding expects {ABI_VERSION}: rebuild it")
@@ -201,6 +215,71 @@ def trimmoe_feedback_update(policy: Policy, stats, eta: float, kappa: float, p_f
     arr = (C.c_double * 6)(*[float(v) for v in stats])
     _check("trimmoe_feedback_update",
            lib().trimmoe_feedback_update(C.byref(policy), arr, eta, kappa, p_floor))
+
+
+# ------------------------------------- offline statistics and placement ----
+def _host(a, dtype):
+    """A C-contiguous numpy copy (or view) of a host array in `dtype`."""
+    if isinstance(a, torch.Tensor):
+        a = a.detach().cpu().numpy()
+    return np.ascontiguousarray(np.asarray(a, dtype=dtype))
+
+
+def _np_ptr(a: np.ndarray):
+    return C.c_void_p(a.ctypes.data)
+
+
+def trimmoe_calib_exit_layers(xi, p_exit: float) -> np.ndarray:
+    """Exit layer of every calibration token from per-layer confidences [N, Q]."""
+    xi = _host(xi, np.float32)
+    N, Q = xi.shape
+    out = np.zeros(Q, dtype=np.int32)
+    _check("trimmoe_calib_exit_layers",
+           lib().trimmoe_calib_exit_layers(N, Q, _np_ptr(xi), float(p_exit), _np_ptr(out)))
+    return out
+
+
+def trimmoe_calib_stats(target, importance, exit_layer, theta, n_experts: int):
+    """(pi [N], act [N, E], sigma [N, E], lambda [N, E]) of a calibration record."""
+    target = _host(target, np.int16)
+    importance = _host(importance, np.float32)
+    exit_layer = _host(exit_layer, np.int32)
+    theta = _host(theta, np.float32)
+    N, Q, k = target.shape
+    E = int(n_experts)
+    pi = np.zeros(N)
+    act, sigma, lam = np.zeros((N, E)), np.zeros((N, E)), np.zeros((N, E))
+    _check("trimmoe_calib_stats",
+           lib().trimmoe_calib_stats(N, Q, E, k, _np_ptr(target), _np_ptr(importance),
+                                     _np_ptr(exit_layer), _np_ptr(theta), _np_ptr(pi),
+                                     _np_ptr(act), _np_ptr(sigma), _np_ptr(lam)))
+    return pi, act, sigma, lam
+
+
+def trimmoe_calib_transitions(target, exit_layer, n_experts: int, trans_b: int):
+    """Transition rows (to int16 [N-1, E, B], p float32 [N-1, E, B])."""
+    target = _host(target, np.int16)
+    exit_layer = _host(exit_layer, np.int32)
+    N, Q, k = target.shape
+    E, B = int(n_experts), int(trans_b)
+    to = np.zeros((max(N - 1, 0), E, B), dtype=np.int16)
+    pr = np.zeros((max(N - 1, 0), E, B), dtype=np.float32)
+    _check("trimmoe_calib_transitions",
+           lib().trimmoe_calib_transitions(N, Q, E, k, _np_ptr(target), _np_ptr(exit_layer), B,
+                                           _np_ptr(to), _np_ptr(pr)))
+    return to, pr
+
+
+def trimmoe_place_replicas(lam, rho, z, nbytes, capacity, bandwidth, latency, x0):
+    """Greedy replication from a baseline x0 [M, N, E]; returns (x, n_placed)."""
+    x = _host(x0, np.uint8).copy()
+    M, N, E = x.shape
+    args = [_host(v, np.float64) for v in (lam, rho, z, nbytes, capacity, bandwidth, latency)]
+    n = C.c_int32(0)
+    _check("trimmoe_place_replicas",
+           lib().trimmoe_place_replicas(M, N, E, *[_np_ptr(v) for v in args], _np_ptr(x),
+                                        C.byref(n)))
+    return x, int(n.value)
 
 
 # ------------------------------------------------ struct construction ------
