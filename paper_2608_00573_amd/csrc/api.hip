@@ -109,7 +109,7 @@ size_t carve(const trimmoe_model* m, int T, char* base, LayerParams* p) {
   const size_t es = bf16 ? 2 : 4;
   const int Tm = T > 0 ? T : 1;
   const size_t R = (size_t)Tm * k;
-  const int nblk = cdiv(Tm, kRouteTokens);
+  const int nblk = route_blocks_max(Tm);
   const int max_tiles = (int)cdiv((int)R, kGemmBM) + E;
   const int n_vtiles = cdiv(m->vocab_exit, exit_tile_rows(bf16, Tm));
   size_t off = 0;
@@ -189,6 +189,7 @@ void fill_params(LayerParams& P, const trimmoe_model* m, int l, const trimmoe_po
   P.budget_tok = pol->budget_tok;
   P.horizon = std::min(pol->horizon, m->n_layers - l);
   P.trans_b = m->trans_b;
+  P.rb = route_block_tokens(T, P.horizon > 1);
   for (int j = 0; j < kMaxLookahead; ++j) {
     const bool later = j + 1 < P.horizon;  // layer l + j + 1 is looked at
     const trimmoe_layer* Lj = later ? &m->layers[l + j + 1] : nullptr;

@@ -12,12 +12,30 @@ namespace trimmoe {
 typedef uint16_t bf16_t;
 
 // ---------------------------------------------------------------- tiling --
-// tokens handled by one block of the route and permute kernels
+// tokens handled by one block of the route and permute kernels (at most;
+// with look-ahead a small batch uses fewer per block: route_block_tokens)
 constexpr int kRouteTokens = 32;
+// route blocks the look-ahead aims for: one per CU
+constexpr int kLookaheadBlocks = 256;
+
+// tokens per route block for a batch of T tokens: kRouteTokens, or with
+// look-ahead the power of two that gives about kLookaheadBlocks blocks
+inline int route_block_tokens(int T, bool lookahead) {
+  if (!lookahead) return kRouteTokens;
+  int rb = 1;
+  while (rb < kRouteTokens && 2 * rb * kLookaheadBlocks <= T) rb *= 2;
+  return rb;
+}
+// route blocks the workspace provides for batches of up to T tokens
+inline int route_blocks_max(int T) {
+  const int full = (T + kRouteTokens - 1) / kRouteTokens;
+  const int la = T < 2 * kLookaheadBlocks ? T : 2 * kLookaheadBlocks;
+  return full > la ? full : la;
+}
 // rows of an expert group covered by one grouped-GEMM tile
 constexpr int kGemmBM = 128;
 // batches of this many tokens or more use the 256-token exit-head tile
-constexpr int kWideTokens = 6144;
+constexpr int kWideTokens = 4096;
 constexpr int kGemmBN = 128;
 constexpr int kGemmBK = 64;
 // vocabulary rows of one exit-head tile (bf16 MFMA path / fp32 path); bf16
@@ -96,6 +114,7 @@ struct LayerParams {
   // horizon - 1; la_tto/la_tp[j] the transitions from layer + j to the next
   int horizon;  // effective horizon: min(policy horizon, N - layer)
   int trans_b;
+  int rb;       // tokens per route block (route, scan and bucket agree on it)
   const uint8_t* la_mask[kMaxLookahead];
   const float* la_sim[kMaxLookahead];
   float la_theta[kMaxLookahead], la_slope[kMaxLookahead];

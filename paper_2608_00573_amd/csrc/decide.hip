@@ -285,9 +285,9 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   __shared__ float sRw[RB][KMAX];   // merged rows: summed weight
 
   const int n_a = *p.n_active;
-  const int base = blockIdx.x * RB;
+  const int base = blockIdx.x * p.rb;
   if (base >= n_a) return;
-  const int nt = min(RB, n_a - base);
+  const int nt = min(p.rb, n_a - base);
   const int E = p.E, d = p.d, k = p.k;
   for (int e = threadIdx.x; e < E; e += blockDim.x) s_cnt[e] = 0;
   if (threadIdx.x == 0) s_xcnt = 0;
@@ -506,13 +506,17 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
       la.skipok[i] = !all_local && I <= p.theta && D + lam <= budget;
     }
     __syncthreads();
+    // tokens in flight per round and wavefronts per token (a block of few
+    // tokens gives each token several wavefronts)
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int tpr = min(p.rb, kRouteWaves), wpt = kRouteWaves / tpr;
+    const int slot = wave / wpt, wsub = wave % wpt;
     const int ntup = lv.ntup, rem = nlev - 1;
-    float* br = la.branch + (size_t)wave * ((1 << k) + 1) * ntup;
-    for (int r = 0; r < RB / kRouteWaves; ++r) {
-      const int ti = wave + kRouteWaves * r;
+    float* br = la.branch + (size_t)slot * ((1 << k) + 1) * ntup;
+    for (int r = 0; r * tpr < p.rb; ++r) {
+      const int ti = slot + tpr * r;
       const int nopt = ti < nt ? (1 << la.nsub[ti]) + 1 : 0;
-      for (int it = lane; it < nopt * ntup; it += 64) {
+      for (int it = wsub * 64 + lane; it < nopt * ntup; it += wpt * 64) {
         const int o = it / ntup, tup = it % ntup;
         const int ns = la.nsub[ti];
         const float Dt = la.tokD[ti], bt = la.tokB[ti], It = la.tokI[ti];
@@ -541,7 +545,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
         br[it] = val;
       }
       __syncthreads();
-      if (lane < nopt) {
+      if (wsub == 0 && lane < nopt) {
         float acc = 0.f;
         for (int u = 0; u < ntup; ++u) acc += br[lane * ntup + u];
         la.phi[ti * ((1 << TRIMMOE_MAX_LOOKAHEAD_TOPK) + 1) + lane] = acc;
@@ -691,7 +695,7 @@ __global__ __launch_bounds__(1024) void k_scan(LayerParams p) {
   __shared__ int s_off[TRIMMOE_MAX_EXPERTS];
   __shared__ int s_toff[TRIMMOE_MAX_EXPERTS];
   const int n_a = *p.n_active;
-  const int nb = (n_a + RB - 1) / RB;
+  const int nb = (n_a + p.rb - 1) / p.rb;
   const int E = p.E;
   int ep = 1;
   while (ep < E) ep <<= 1;
@@ -765,9 +769,9 @@ __global__ __launch_bounds__(256) void k_bucket(LayerParams p) {
   __shared__ int s_exec[RB * KMAX];
   __shared__ int s_act[RB];
   const int n_a = *p.n_active;
-  const int base = blockIdx.x * RB;
+  const int base = blockIdx.x * p.rb;
   if (base >= n_a) return;
-  const int nt = min(RB, n_a - base);
+  const int nt = min(p.rb, n_a - base);
   const int k = p.k, E = p.E;
   const int i = threadIdx.x;
   if (i < nt) {
@@ -946,7 +950,7 @@ hipError_t launch_trace_fill(const LayerParams& p, int n_layers, hipStream_t st)
 }
 
 hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st) {
-  const int nb = cdiv(p.T, RB);
+  const int nb = cdiv(p.T, p.rb);
   size_t lds = (size_t)(bf16 ? route_ks(p.E, p.d) : 1) * RB * p.E * sizeof(float);
   const dim3 grid(nb), block(64 * kRouteWaves);
   if (p.horizon > 1) {
@@ -973,7 +977,7 @@ hipError_t launch_scan(const LayerParams& p, hipStream_t st) {
 }
 
 hipError_t launch_bucket(const LayerParams& p, hipStream_t st) {
-  hipLaunchKernelGGL(k_bucket, dim3(cdiv(p.T, RB)), dim3(256), 0, st, p);
+  hipLaunchKernelGGL(k_bucket, dim3(cdiv(p.T, p.rb)), dim3(256), 0, st, p);
   return hipGetLastError();
 }
 

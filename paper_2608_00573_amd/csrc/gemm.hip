@@ -512,9 +512,12 @@ struct ExitArgs {
 };
 
 using ExitTile = Tile<kExitTileBF16, 128, 1, 4, 2>;
-// 256 tokens per tile for large batches: 2/3 of the DMA bytes per MFMA of the
-// 128-token tile, in a two-stage ring (the 128-token tile keeps three stages,
-// and its finer token tiles balance the persistent grid better at small n_x)
+// 256 tokens per tile for large batches: 64 x 128 wavefront tiles read 3/4 of
+// the LDS bytes per MFMA of the 64 x 64 ones and the DMA writes 2/3, which
+// brings a k-step's LDS traffic (~125 B/clk at the MFMA peak) under the LDS
+// bandwidth (128 B/clk; the 128-token tile needs ~172).  It runs a two-stage
+// ring (the 128-token tile keeps three stages, and its finer token tiles
+// balance the persistent grid better at small n_x)
 using ExitWide = Tile<kExitTileBF16, 256, 1, 4, 2>;
 // decode-sized batches (kExitSmallTokens or fewer): 32 token columns, 128
 // vocabulary rows, so the tiles cover the CUs and the MFMA work is not 4x
