@@ -375,6 +375,50 @@ int trimmoe_place_replicas(int32_t n_servers, int32_t n_layers, int32_t n_expert
                            const double* bandwidth, const double* latency, uint8_t* x,
                            int32_t* n_placed);
 
+/*
+ * Exit-head training (Sec. IV-A) on cached hidden states.  Device memory,
+ * caller-owned; work is enqueued on `stream`; arguments are checked before
+ * anything is enqueued.
+ *
+ * trimmoe_head_argmax: argmax[q] = argmax_v (w_head[v] . h[q] + b_head[v])
+ * over the V rows of an output head w_head [V, d] (ties to the lower v): the
+ * prediction of a representation, from which the consistency labels of
+ * Eq. (22) follow.  h [n_rows, d] and w_head in `dtype` (bf16: d a multiple
+ * of 64, both 16-byte aligned); b_head fp32 [V] or NULL; argmax int32
+ * [n_rows].  Needs a 256-byte aligned workspace of
+ * trimmoe_head_argmax_workspace_size(dtype, V, n_rows) bytes.
+ */
+int trimmoe_head_argmax_workspace_size(int32_t dtype, int32_t vocab, int32_t n_rows,
+                                       size_t* bytes);
+int trimmoe_head_argmax(int32_t dtype, int32_t vocab, int32_t d_model, int32_t n_rows,
+                        const void* w_head, const float* b_head, const void* h, int32_t* argmax,
+                        void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * trimmoe_consistency_labels: Eq. (22), labels[q] = (pred[q] == ref[q]) for
+ * the predictions of one layer and of full depth (int32 [n_rows] each, from
+ * trimmoe_head_argmax); labels uint8 [n_rows].
+ */
+int trimmoe_consistency_labels(int32_t n_rows, const int32_t* pred, const int32_t* ref,
+                               uint8_t* labels, void* stream);
+
+/*
+ * trimmoe_train_exit_head: `epochs` steps of full-batch gradient descent of
+ * the exit head xi = sigmoid(w . h + c) on the binary cross-entropy of
+ * Eq. (23) against labels[q] in {0, 1} (uint8 [n_rows]):
+ * w -= lr * mean_q (xi_q - y_q) h_q and c -= lr * mean_q (xi_q - y_q).
+ * w (fp32 [d]) and c (fp32 [1]) hold the start on entry and the trained head
+ * on return; loss (fp32 [epochs], or NULL) receives Eq. (23) at the weights
+ * each epoch starts from.  h [n_rows, d] in `dtype` (bf16: d a multiple of
+ * 64).  Sums run in a fixed order in fp64: repeated runs give identical
+ * weights.  Needs a 256-byte aligned workspace of
+ * trimmoe_train_exit_head_workspace_size(n_rows) bytes.
+ */
+int trimmoe_train_exit_head_workspace_size(int32_t n_rows, size_t* bytes);
+int trimmoe_train_exit_head(int32_t dtype, int32_t d_model, int32_t n_rows, const void* h,
+                            const uint8_t* labels, int32_t epochs, float lr, float* w, float* c,
+                            float* loss, void* workspace, size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

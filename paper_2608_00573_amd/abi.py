@@ -70,7 +70,10 @@ EXPORTS = ["trimmoe_abi_version", "trimmoe_status_str", "trimmoe_workspace_size"
            "trimmoe_state_reset", "trimmoe_layer_step", "trimmoe_stack_forward",
            "trimmoe_stack_forward_timed", "trimmoe_window_stats", "trimmoe_feedback_update",
            "trimmoe_calib_exit_layers", "trimmoe_calib_stats", "trimmoe_calib_transitions",
-           "trimmoe_place_replicas"]
+           "trimmoe_place_replicas", "trimmoe_head_argmax_workspace_size",
+           "trimmoe_head_argmax", "trimmoe_consistency_labels",
+           "trimmoe_train_exit_head_workspace_size",
+           "trimmoe_train_exit_head"]
 TIMED_CLASSES = ["route", "bucket", "up", "down", "shared", "combine", "exit", "gate"]
 
 _lib = None
@@ -121,6 +124,17 @@ def lib():
         L.trimmoe_place_replicas.restype = C.c_int
         L.trimmoe_place_replicas.argtypes = [i32, i32, i32, p, p, p, p, p, p, p, p,
                                              C.POINTER(C.c_int32)]
+        L.trimmoe_head_argmax_workspace_size.restype = C.c_int
+        L.trimmoe_head_argmax_workspace_size.argtypes = [i32, i32, i32, C.POINTER(C.c_size_t)]
+        L.trimmoe_head_argmax.restype = C.c_int
+        L.trimmoe_head_argmax.argtypes = [i32, i32, i32, i32, p, p, p, p, p, C.c_size_t, p]
+        L.trimmoe_consistency_labels.restype = C.c_int
+        L.trimmoe_consistency_labels.argtypes = [i32, p, p, p, p]
+        L.trimmoe_train_exit_head_workspace_size.restype = C.c_int
+        L.trimmoe_train_exit_head_workspace_size.argtypes = [i32, C.POINTER(C.c_size_t)]
+        L.trimmoe_train_exit_head.restype = C.c_int
+        L.trimmoe_train_exit_head.argtypes = [i32, i32, i32, p, p, i32, f32, p, p, p, p,
+                                              C.c_size_t, p]
         if L.trimmoe_abi_version() != ABI_VERSION:
             raise RuntimeError(f"{LIB_PATH} has ABI version {L.trimmoe_abi_version()}, the "
                                f"binding expects {ABI_VERSION}: rebuild it")
@@ -280,6 +294,66 @@ def trimmoe_place_replicas(lam, rho, z, nbytes, capacity, bandwidth, latency, x0
            lib().trimmoe_place_replicas(M, N, E, *[_np_ptr(v) for v in args], _np_ptr(x),
                                         C.byref(n)))
     return x, int(n.value)
+
+
+# ------------------------------------------------- exit-head training ------
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError(f"hidden states must be bf16 or fp32, not {t.dtype}")
+
+
+def _aligned_ws(nbytes: int, device) -> torch.Tensor:
+    ws = torch.empty(nbytes + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + nbytes]
+
+
+def trimmoe_head_argmax(w_head: torch.Tensor, h: torch.Tensor, b_head=None,
+                        stream=None) -> torch.Tensor:
+    """argmax over the rows of an output head [V, d] for each row of h [Q, d]
+    (both on one GPU, same dtype); returns int32 [Q] on the GPU."""
+    assert w_head.dtype == h.dtype and w_head.is_contiguous() and h.is_contiguous()
+    V, d = w_head.shape
+    Q = h.shape[0]
+    dt = _dtype_code(h)
+    n = C.c_size_t(0)
+    _check("trimmoe_head_argmax_workspace_size",
+           lib().trimmoe_head_argmax_workspace_size(dt, V, Q, C.byref(n)))
+    ws = _aligned_ws(n.value, h.device)
+    out = torch.empty(Q, dtype=torch.int32, device=h.device)
+    _check("trimmoe_head_argmax",
+           lib().trimmoe_head_argmax(dt, V, d, Q, _ptr(w_head), _ptr(b_head), _ptr(h), _ptr(out),
+                                     _ptr(ws), ws.numel(), _stream_handle(stream)))
+    return out
+
+
+def trimmoe_consistency_labels(pred: torch.Tensor, ref: torch.Tensor, stream=None):
+    """Eq. (22) on the GPU: uint8 [Q], 1 where pred == ref (int32 [Q] each)."""
+    assert pred.dtype == torch.int32 and ref.dtype == torch.int32 and pred.shape == ref.shape
+    out = torch.empty(pred.shape[0], dtype=torch.uint8, device=pred.device)
+    _check("trimmoe_consistency_labels",
+           lib().trimmoe_consistency_labels(pred.shape[0], _ptr(pred), _ptr(ref), _ptr(out),
+                                            _stream_handle(stream)))
+    return out
+
+
+def trimmoe_train_exit_head(h: torch.Tensor, labels: torch.Tensor, epochs: int, lr: float,
+                            w: torch.Tensor, c: torch.Tensor, loss=None, stream=None):
+    """Gradient descent of the sigmoid exit head on BCE; w (fp32 [d]) and c
+    (fp32 [1]) are updated in place; loss (fp32 [epochs]) if given."""
+    assert w.dtype == torch.float32 and c.dtype == torch.float32 and labels.dtype == torch.uint8
+    Q, d = h.shape
+    n = C.c_size_t(0)
+    _check("trimmoe_train_exit_head_workspace_size",
+           lib().trimmoe_train_exit_head_workspace_size(Q, C.byref(n)))
+    ws = _aligned_ws(n.value, h.device)
+    _check("trimmoe_train_exit_head",
+           lib().trimmoe_train_exit_head(_dtype_code(h), d, Q, _ptr(h), _ptr(labels), int(epochs),
+                                         float(lr), _ptr(w), _ptr(c), _ptr(loss), _ptr(ws),
+                                         ws.numel(), _stream_handle(stream)))
 
 
 # ------------------------------------------------ struct construction ------

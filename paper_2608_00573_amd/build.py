@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libtrimmoe.so")
-SOURCES = ["api.hip", "decide.hip", "gemm.hip"]
+SOURCES = ["api.hip", "decide.hip", "gemm.hip", "head.hip"]
 HOST_SOURCES = ["placement.cpp"]  # host-only C++ (offline statistics and placement)
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 CXX = os.environ.get("CXX", "g++")

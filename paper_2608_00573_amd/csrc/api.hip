@@ -418,4 +418,95 @@ int trimmoe_feedback_update(trimmoe_policy* p, const double* stats, double eta, 
   return TRIMMOE_OK;
 }
 
+// ----------------------------------------- exit-head training (Sec. IV-A) --
+namespace {
+size_t argmax_ws(bool bf16, int V, int n_rows, int* n_vtiles) {
+  const int rows = n_rows > 0 ? n_rows : 1;
+  const int nvt = cdiv(V, bf16 ? exit_tile_rows(true, rows) : kExitTileF32);
+  if (n_vtiles) *n_vtiles = nvt;
+  return 256 + align256((size_t)rows * nvt * sizeof(float2));
+}
+size_t train_ws(int n_rows) {
+  const int rows = n_rows > 0 ? n_rows : 1;
+  return align256((size_t)rows * 4) + align256((size_t)rows * 8);
+}
+bool head_dims_ok(int dtype, int d) {
+  if (dtype == TRIMMOE_BF16) return d >= 64 && d % 64 == 0;
+  return dtype == TRIMMOE_F32 && d >= 1;
+}
+}  // namespace
+
+int trimmoe_head_argmax_workspace_size(int32_t dtype, int32_t vocab, int32_t n_rows,
+                                       size_t* bytes) {
+  if (!bytes) return TRIMMOE_ERR_NULL;
+  if (dtype != TRIMMOE_F32 && dtype != TRIMMOE_BF16) return TRIMMOE_ERR_DTYPE;
+  if (vocab < 1 || n_rows < 0) return TRIMMOE_ERR_SHAPE;
+  *bytes = argmax_ws(dtype == TRIMMOE_BF16, vocab, n_rows, nullptr);
+  return TRIMMOE_OK;
+}
+
+int trimmoe_head_argmax(int32_t dtype, int32_t vocab, int32_t d_model, int32_t n_rows,
+                        const void* w_head, const float* b_head, const void* h, int32_t* argmax,
+                        void* workspace, size_t workspace_bytes, void* stream) {
+  if (!w_head || !h || !argmax || !workspace) return TRIMMOE_ERR_NULL;
+  if (dtype != TRIMMOE_F32 && dtype != TRIMMOE_BF16) return TRIMMOE_ERR_DTYPE;
+  if (vocab < 1 || n_rows < 0 || !head_dims_ok(dtype, d_model)) return TRIMMOE_ERR_SHAPE;
+  const bool bf16 = dtype == TRIMMOE_BF16;
+  if (bf16 && (!aligned16(w_head) || !aligned16(h))) return TRIMMOE_ERR_SHAPE;
+  int nvt = 0;
+  if (reinterpret_cast<uintptr_t>(workspace) & 255) return TRIMMOE_ERR_WORKSPACE;
+  if (workspace_bytes < argmax_ws(bf16, vocab, n_rows, &nvt)) return TRIMMOE_ERR_WORKSPACE;
+  if (n_rows == 0) return TRIMMOE_OK;
+  int dev = 0, ncu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return TRIMMOE_ERR_HIP;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t* n_dev = static_cast<int32_t*>(workspace);
+  float2* partials = reinterpret_cast<float2*>(static_cast<char*>(workspace) + 256);
+  if (launch_set_int(n_dev, n_rows, st) != hipSuccess ||
+      launch_head_argmax_partials(bf16, w_head, b_head, h, n_dev, n_rows, vocab, d_model, nvt,
+                                  partials, ncu, st) != hipSuccess ||
+      launch_argmax_reduce(partials, nvt, n_rows, argmax, st) != hipSuccess)
+    return TRIMMOE_ERR_HIP;
+  return TRIMMOE_OK;
+}
+
+int trimmoe_consistency_labels(int32_t n_rows, const int32_t* pred, const int32_t* ref,
+                               uint8_t* labels, void* stream) {
+  if (!pred || !ref || !labels) return TRIMMOE_ERR_NULL;
+  if (n_rows < 0) return TRIMMOE_ERR_SHAPE;
+  if (launch_consistency(pred, ref, n_rows, labels, static_cast<hipStream_t>(stream)) !=
+      hipSuccess)
+    return TRIMMOE_ERR_HIP;
+  return TRIMMOE_OK;
+}
+
+int trimmoe_train_exit_head_workspace_size(int32_t n_rows, size_t* bytes) {
+  if (!bytes) return TRIMMOE_ERR_NULL;
+  if (n_rows < 0) return TRIMMOE_ERR_SHAPE;
+  *bytes = train_ws(n_rows);
+  return TRIMMOE_OK;
+}
+
+int trimmoe_train_exit_head(int32_t dtype, int32_t d_model, int32_t n_rows, const void* h,
+                            const uint8_t* labels, int32_t epochs, float lr, float* w, float* c,
+                            float* loss, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!h || !labels || !w || !c || !workspace) return TRIMMOE_ERR_NULL;
+  if (dtype != TRIMMOE_F32 && dtype != TRIMMOE_BF16) return TRIMMOE_ERR_DTYPE;
+  if (n_rows < 1 || epochs < 0 || !head_dims_ok(dtype, d_model)) return TRIMMOE_ERR_SHAPE;
+  if (!(lr >= 0.f) || isinf(lr)) return TRIMMOE_ERR_POLICY;
+  if (reinterpret_cast<uintptr_t>(workspace) & 255) return TRIMMOE_ERR_WORKSPACE;
+  if (workspace_bytes < train_ws(n_rows)) return TRIMMOE_ERR_WORKSPACE;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  float* r = static_cast<float*>(workspace);
+  double* row_loss = reinterpret_cast<double*>(static_cast<char*>(workspace) +
+                                               align256((size_t)n_rows * 4));
+  for (int e = 0; e < epochs; ++e)
+    if (launch_bce_step(dtype == TRIMMOE_BF16, h, labels, n_rows, d_model, lr, w, c, r, row_loss,
+                        loss ? loss + e : nullptr, st) != hipSuccess)
+      return TRIMMOE_ERR_HIP;
+  return TRIMMOE_OK;
+}
+
 }  // extern "C"

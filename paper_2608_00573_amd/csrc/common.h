@@ -191,6 +191,22 @@ hipError_t launch_bucket(const LayerParams& p, hipStream_t st);
 hipError_t launch_combine(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_exit_reduce(const LayerParams& p, hipStream_t st);
 hipError_t launch_compact(const LayerParams& p, hipStream_t st);
+// exit-head training (Sec. IV-A): per-tile (max logit, row) partials of an
+// output head over rows of hidden states (head.hip reduces them to argmax)
+hipError_t launch_head_argmax_partials(bool bf16, const void* W, const float* bias, const void* H,
+                                       const int* n_rows_dev, int n_rows, int V, int K,
+                                       int n_vtiles, float2* partials, int n_cu, hipStream_t st);
+hipError_t launch_argmax_reduce(const float2* partials, int n_vtiles, int n_rows, int32_t* out,
+                                hipStream_t st);
+hipError_t launch_consistency(const int32_t* pred, const int32_t* ref, int n_rows,
+                              uint8_t* labels, hipStream_t st);
+// *p = v on the stream (a kernel, so that the call can be captured)
+hipError_t launch_set_int(int32_t* p, int v, hipStream_t st);
+// one full-batch descent step of the sigmoid exit head on BCE (Eq. (23)):
+// residuals r = sigmoid(w . h + c) - y and per-row losses, then the update
+hipError_t launch_bce_step(bool bf16, const void* H, const uint8_t* y, int n_rows, int d,
+                           float lr, float* w, float* c, float* r, double* row_loss,
+                           float* loss_out, hipStream_t st);
 hipError_t launch_window_stats(const WindowArgs& w, hipStream_t st);
 
 // launchers (gemm.hip)

@@ -524,7 +524,7 @@ using ExitWide = Tile<kExitTileBF16, 256, 1, 4, 2>;
 // padding; W_exit streaming (HBM) bounds it
 using ExitSmall = Tile<kExitTileBF16Small, 32, 1, 4, 1>;
 
-template <class T>
+template <class T, bool ARGMAX = false>
 struct ExitSrc {
   struct Desc {
     int mt, nt;
@@ -553,6 +553,61 @@ struct ExitSrc {
     make_dptrs<T>(q, a.W, src, a.H, nullptr, j0, min(T::BN, n_x - j0), a.K, 0);
   }
   __device__ __forceinline__ void epilogue(const Desc& d, Acc<T>& acc) const {
+    if constexpr (ARGMAX)
+      epilogue_argmax(d, acc);
+    else
+      epilogue_softmax(d, acc);
+  }
+  // per (token, vocabulary tile): the largest logit and its vocabulary row
+  // (ties to the lower row), the row stored as the float's bit pattern
+  __device__ __forceinline__ void epilogue_argmax(const Desc& d, Acc<T>& acc) const {
+    const int v0 = d.mt * T::BM, j0 = d.nt * T::BN;
+    const int a_valid = min(T::BM, a.V - v0);
+    const int b_valid = min(T::BN, n_x - j0);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave / T::GN, wn = wave % T::GN;
+#pragma unroll
+    for (int jj = 0; jj < T::TN; ++jj) {
+      float m = -__builtin_inff();
+      int mi = 0x7fffffff;
+#pragma unroll
+      for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = acc_row<T>(wm, i, r, lane);
+          float y = acc[i][jj][r];
+          if (a.bias) y += a.bias[v0 + min(row, a_valid - 1)];
+          if (row < a_valid && (y > m || (y == m && row < mi))) {
+            m = y;
+            mi = row;
+          }
+        }
+      const float m2 = __shfl_xor(m, 32);
+      const int mi2 = __shfl_xor(mi, 32);
+      if (m2 > m || (m2 == m && mi2 < mi)) {
+        m = m2;
+        mi = mi2;
+      }
+      if (lane < 32) s_part[wm][acc_col<T>(wn, jj, lane)] = make_float2(m, __int_as_float(mi));
+    }
+    lds_barrier();
+    const int c = threadIdx.x;
+    if (c < b_valid) {
+      float M = s_part[0][c].x;
+      int R = __float_as_int(s_part[0][c].y);
+#pragma unroll
+      for (int g = 1; g < T::GM; ++g) {
+        const float2 v = s_part[g][c];
+        const int rv = __float_as_int(v.y);
+        if (v.x > M || (v.x == M && rv < R)) {
+          M = v.x;
+          R = rv;
+        }
+      }
+      a.partials[(size_t)(j0 + c) * a.n_vtiles + d.mt] = make_float2(M, __int_as_float(v0 + R));
+    }
+  }
+  __device__ __forceinline__ void epilogue_softmax(const Desc& d, Acc<T>& acc) const {
     const int v0 = d.mt * T::BM, j0 = d.nt * T::BN;
     const int a_valid = min(T::BM, a.V - v0);
     const int b_valid = min(T::BN, n_x - j0);
@@ -616,7 +671,7 @@ struct ExitSrc {
   }
 };
 
-template <class T>
+template <class T, bool ARGMAX = false>
 __global__ __launch_bounds__(T::THREADS) void k_exit_mma(ExitArgs a) {
   __shared__ __align__(16) char lds[DmaTile<T>::LDS];
   __shared__ float2 s_part[T::GM][T::BN];  // per wavefront row: (max, sum) per token column
@@ -624,7 +679,7 @@ __global__ __launch_bounds__(T::THREADS) void k_exit_mma(ExitArgs a) {
   TileSched S;
   int ntiles;
   if (!S.init(a.n_vtiles, (n_x + T::BN - 1) / T::BN, 1, ntiles)) return;
-  const ExitSrc<T> src{a, S, n_x, s_part};
+  const ExitSrc<T, ARGMAX> src{a, S, n_x, s_part};
   dma_gemm_stream<T>(lds, ntiles, a.K / BK, src);
 }
 
@@ -674,6 +729,7 @@ __global__ __launch_bounds__(256) void k_ffn_f32(const float* X, const int* x_id
 }
 
 // exit head, fp32: block = 16 vocabulary rows x 16 tokens
+template <bool ARGMAX = false>
 __global__ __launch_bounds__(256) void k_exit_f32(const float* W, const float* H, const int* tok,
                                                   const float* bias, const int* n_exec, int V,
                                                   int K, int n_vtiles, float2* partials) {
@@ -686,7 +742,7 @@ __global__ __launch_bounds__(256) void k_exit_f32(const float* W, const float* H
   float z = -__builtin_inff();
   if (v < V && j < n_x) {
     const float* w = W + (size_t)v * K;
-    const float* h = H + (size_t)tok[j] * K;
+    const float* h = H + (size_t)(tok ? tok[j] : j) * K;
     float acc = 0.f;
     for (int c = 0; c < K; ++c) acc = fmaf(w[c], h[c], acc);
     z = acc + (bias ? bias[v] : 0.f);
@@ -695,7 +751,17 @@ __global__ __launch_bounds__(256) void k_exit_f32(const float* W, const float* H
   __syncthreads();
   if (threadIdx.x < FT) {
     const int jj = jt * FT + threadIdx.x;
-    if (jj < n_x) {
+    if (jj < n_x && ARGMAX) {
+      // the largest logit of the tile and its row (ties to the lower row)
+      float m = -__builtin_inff();
+      int mi = vt * FT;
+      for (int u = 0; u < FT && vt * FT + u < V; ++u)
+        if (s_z[u][threadIdx.x] > m) {
+          m = s_z[u][threadIdx.x];
+          mi = vt * FT + u;
+        }
+      partials[(size_t)jj * n_vtiles + vt] = make_float2(m, __int_as_float(mi));
+    } else if (jj < n_x) {
       float m = -__builtin_inff();
       for (int u = 0; u < FT; ++u) m = fmaxf(m, s_z[u][threadIdx.x]);
       float s = 0.f;
@@ -807,9 +873,35 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
     }
   } else {
     const dim3 grid(p.n_vtiles * cdiv(p.T, FT));
-    hipLaunchKernelGGL(k_exit_f32, grid, dim3(256), 0, st, static_cast<const float*>(p.w_exit),
+    hipLaunchKernelGGL(k_exit_f32<false>, grid, dim3(256), 0, st, static_cast<const float*>(p.w_exit),
                        static_cast<const float*>(p.h), p.exec_list, p.b_exit, &p.counts[kCntExec],
                        p.V, p.d, p.n_vtiles, p.partials);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_head_argmax_partials(bool bf16, const void* W, const float* bias, const void* H,
+                                       const int* n_rows_dev, int n_rows, int V, int K,
+                                       int n_vtiles, float2* partials, int n_cu, hipStream_t st) {
+  if (n_rows <= 0) return hipSuccess;
+  if (bf16) {
+    ExitArgs a{static_cast<const bf16_t*>(W), static_cast<const bf16_t*>(H), bias, n_rows_dev, V,
+               K, n_vtiles, partials};
+    if (n_rows <= kExitSmallTokens) {
+      const dim3 grid(min(n_vtiles * cdiv(n_rows, ExitSmall::BN), n_cu));
+      hipLaunchKernelGGL((k_exit_mma<ExitSmall, true>), grid, dim3(ExitSmall::THREADS), 0, st, a);
+    } else if (n_rows >= kWideTokens) {
+      const dim3 grid(min(n_vtiles * cdiv(n_rows, ExitWide::BN), n_cu));
+      hipLaunchKernelGGL((k_exit_mma<ExitWide, true>), grid, dim3(ExitWide::THREADS), 0, st, a);
+    } else {
+      const dim3 grid(min(n_vtiles * cdiv(n_rows, ExitTile::BN), n_cu));
+      hipLaunchKernelGGL((k_exit_mma<ExitTile, true>), grid, dim3(ExitTile::THREADS), 0, st, a);
+    }
+  } else {
+    const dim3 grid(n_vtiles * cdiv(n_rows, FT));
+    hipLaunchKernelGGL(k_exit_f32<true>, grid, dim3(256), 0, st, static_cast<const float*>(W),
+                       static_cast<const float*>(H), nullptr, bias, n_rows_dev, V, K, n_vtiles,
+                       partials);
   }
   return hipGetLastError();
 }

@@ -43,3 +43,41 @@ def place(tables: dict, servers: dict):
     return abi.trimmoe_place_replicas(tables["lam"], servers["rho"], servers["z"],
                                       servers["nbytes"], servers["capacity"],
                                       servers["bandwidth"], servers["latency"], servers["x0"])
+
+
+def calibration_hidden_states(model: abi.Model, policy: dict, h0: torch.Tensor,
+                              workspace: torch.Tensor):
+    """Table I, line 1, keeping the representation after every layer: the
+    full-depth exact pass one layer at a time; returns [h after layer l] for
+    l = 0 .. N - 1 (on the GPU, the model's dtype)."""
+    cal = abi.make_policy(**dict(policy, budget=0.0, p_exit=_NEVER, horizon=1))
+    st = abi.StateBuffers(h0.clone())
+    abi.trimmoe_state_reset(model, st.state)
+    hs = []
+    for l in range(model.n_layers):
+        abi.trimmoe_layer_step(model, l, cal, st.state, None, workspace)
+        hs.append(st.h.clone())
+    torch.cuda.synchronize()
+    return hs
+
+
+def consistency_labels(hs, w_head: torch.Tensor):
+    """Eq. (22) for layers 0 .. N - 2: 1 where the output head's prediction
+    of the layer's representation equals its prediction at full depth."""
+    final = abi.trimmoe_head_argmax(w_head, hs[-1])
+    return [abi.trimmoe_consistency_labels(abi.trimmoe_head_argmax(w_head, h), final)
+            for h in hs[:-1]]
+
+
+def train_sigmoid_heads(hs, labels, epochs: int, lr: float):
+    """Table I, lines 3-4: one sigmoid exit head per layer 0 .. N - 2 trained
+    on BCE (Eq. (23)) from zero; returns [(w fp32 [d], c fp32 [1], losses)]."""
+    out = []
+    for h, y in zip(hs, labels):
+        w = torch.zeros(h.shape[1], dtype=torch.float32, device=h.device)
+        c = torch.zeros(1, dtype=torch.float32, device=h.device)
+        loss = torch.zeros(max(epochs, 1), dtype=torch.float32, device=h.device)
+        abi.trimmoe_train_exit_head(h, y, epochs, lr, w, c, loss)
+        out.append((w, c, loss[:epochs]))
+    torch.cuda.synchronize()
+    return out
