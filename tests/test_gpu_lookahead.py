@@ -110,3 +110,13 @@ def test_validation_of_look_ahead_limits():
     # ...but layer 1 alone at H = 2 reads only P_1
     abi.trimmoe_layer_step(mh.model, 1, g.policy(), st.state, None, g.ws)
     torch.cuda.synchronize()
+
+
+def test_256_experts_look_ahead_tables_beyond_64k_lds():
+    # 256 experts top-2 with 8-entry rows and two later layers: the route
+    # block's look-ahead tables and logits need ~74 KB of LDS (the launch
+    # raises the kernel's dynamic-LDS limit)
+    cfg = workload("tiny_fp32", n_layers=3, n_experts=256, n_local=128, top_k=2,
+                   normalize_topk=1, horizon=3, trans_support=8, n_tokens=32, **RECIPE)
+    _, _, _, stats = _stack(cfg, 1e-5, 1e-7)
+    assert stats["compared"] >= 40
