@@ -134,12 +134,13 @@ def test_library_update_rejects_bad_arguments():
 KEYS = ("tokens", "exits", "xi_exit", "util", "delay", "delay_ref")
 
 
-def _recount(cfg, pol, masks, gst, gtr):
+def _recount(cfg, pol, masks, gst, gtr, budget_tok=None):
     """The six sums recomputed in fp64 from the GPU's own state and trace
     (masks: the local-expert mask of each layer)."""
     N, k = cfg["n_layers"], cfg["top_k"]
     ex = gst["exit_layer"] < N
-    b = np.float64(np.float32(pol["budget"]))
+    b = np.float64(np.float32(pol["budget"])) if budget_tok is None \
+        else np.asarray(budget_tok, np.float64)
     run = gtr["action"] == O.ACT_EXEC
     remote = ((gtr["kind"] == O.KIND_REMOTE) & run[:, :, None]).sum()
     slots = run.sum() * k
@@ -153,45 +154,54 @@ def _recount(cfg, pol, masks, gst, gtr):
         means.append(d.mean() if d.size else None)
     pooled = np.concatenate(all_d).mean()
     ref = sum(T * k * (pooled if m is None else m) for m in means)
-    return np.array([T, ex.sum(), gst["xi"][ex].sum(), (gst["d_acc"] / b).sum(),
+    util = np.where(b > 0, gst["d_acc"] / np.where(b > 0, b, 1.0), 0.0)
+    return np.array([T, ex.sum(), gst["xi"][ex].sum(), util.sum(),
                      (slots - remote) * tl + remote * tr, ref])
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("over", [dict(n_tokens=200, n_layers=3),
-                                  dict(dtype="bf16", act="swiglu", top_k=2, normalize_topk=1,
-                                       n_layers=3, n_tokens=300, d_ff_shared=128)],
-                         ids=["f32_top1", "bf16_top2_shared"])
-def test_window_stats_match_oracle(over):
+@pytest.mark.parametrize("over,per_token", [(dict(n_tokens=200, n_layers=3), False),
+                                            (dict(dtype="bf16", act="swiglu", top_k=2,
+                                                  normalize_topk=1, n_layers=3, n_tokens=300,
+                                                  d_ff_shared=128), False),
+                                            (dict(n_tokens=200, n_layers=3), True)],
+                         ids=["f32_top1", "bf16_top2_shared", "f32_per_token_budget"])
+def test_window_stats_match_oracle(over, per_token):
     from synthgen import make_inputs, workload
     from tests.gpu_harness import GpuRun, FTOL, compare_stack, gpu_state_np, gpu_trace_np, \
         log, oracle_run, policy32
 
     cfg = workload("tiny_fp32", **over)
-    log(f"[feedback] window stats {cfg['dtype']} T={cfg['n_tokens']} k={cfg['top_k']}")
+    log(f"[feedback] window stats {cfg['dtype']} T={cfg['n_tokens']} k={cfg['top_k']} "
+        f"per-token budget {per_token}")
     inp = make_inputs(cfg)
     pol = policy32(inp["policy"])
+    T = cfg["n_tokens"]
+    btok = np.choose(np.arange(T) % 3, [0.0, 0.01, 0.04]).astype(np.float32) \
+        if per_token else None
     g = GpuRun(inp)
-    st, tr = g.stack()
+    st, tr = g.stack(budget_tok=btok)
     gst, gtr = gpu_state_np(st), gpu_trace_np(tr)
+    bt_dev = None if btok is None else torch.from_numpy(btok).to(g.dev)
+    cpol = g.policy(budget_tok=bt_dev)
     # a second pass that records only the counters; the sums of a window add up
     st2 = abi.StateBuffers(inp["h0"].to(g.dev).clone())
     ct = abi.CounterTrace(cfg["n_layers"], g.dev)
-    abi.trimmoe_stack_forward(g.mh.model, g.policy(), st2.state, ct.trace, g.ws)
+    abi.trimmoe_stack_forward(g.mh.model, cpol, st2.state, ct.trace, g.ws)
     stats = torch.zeros(6, dtype=torch.float64, device=g.dev)
-    abi.trimmoe_window_stats(g.mh.model, g.policy(), st.state, tr.trace, stats)
-    abi.trimmoe_window_stats(g.mh.model, g.policy(), st2.state, ct.trace, stats)
+    abi.trimmoe_window_stats(g.mh.model, cpol, st.state, tr.trace, stats)
+    abi.trimmoe_window_stats(g.mh.model, cpol, st2.state, ct.trace, stats)
     torch.cuda.synchronize()
     assert torch.equal(ct.counters.cpu(), tr.counters.cpu())
     got = stats.cpu().numpy() / 2
     # against the GPU's own per-token record: only summation order differs
     masks = [L["local_mask"].cpu().numpy().astype(bool) for L in inp["layers"]]
-    own = _recount(cfg, pol, masks, gst, gtr)
+    own = _recount(cfg, pol, masks, gst, gtr, btok)
     assert np.allclose(got, own, rtol=1e-12, atol=1e-12), (got, own)
 
-    ref_state, ref_traces = oracle_run(inp)
+    ref_state, ref_traces = oracle_run(inp, token_budget=btok)
     cmp = compare_stack(cfg, ref_state, ref_traces, gst, gtr)
-    ref = O.window_stats(O.model_from_inputs(inp), pol, ref_state, ref_traces)
+    ref = O.window_stats(O.model_from_inputs(inp), pol, ref_state, ref_traces, btok)
     ref = np.array([ref[k] for k in KEYS])
     # a token excluded by the margin band may differ in every decision: one
     # exit, a confidence of at most 1, a utilisation of at most 1 and N k
@@ -203,7 +213,8 @@ def test_window_stats_match_oracle(over):
     xrel = max(frel, 1e-4)
     # The reference moves with the routes of excluded tokens: at most N k
     # slots change price, each re-weighted T / (active tokens) at its layer.
-    slack = np.array([0.0, n, n + xrel * ref[2], n + T * dabs / pol["budget"],
+    bmin = pol["budget"] if btok is None else float(btok[btok > 0].min())
+    slack = np.array([0.0, n, n + xrel * ref[2], n + T * dabs / bmin,
                       n * N * k * pol["t_remote"], n * N * k * pol["t_remote"] * T]) \
         + 1e-9 * np.abs(ref)
     log(f"[feedback] gpu {got.tolist()} oracle {ref.tolist()} excluded {n}")

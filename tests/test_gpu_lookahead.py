@@ -23,17 +23,17 @@ pytestmark = pytest.mark.gpu
 RECIPE = dict(t_remote=2.0, omega_t=0.2)
 
 
-def _stack(cfg, band, band_budget):
+def _stack(cfg, band, band_budget, budget_tok=None, p_exit_tok=None):
     inp = make_inputs(cfg)
     log(f"[lookahead] {cfg['dtype']} T={cfg['n_tokens']} N={cfg['n_layers']} "
         f"k={cfg['top_k']} B={cfg['trans_support']} H={cfg['horizon']}")
     g = GpuRun(inp)
-    st, tr = g.stack()
+    st, tr = g.stack(budget_tok=budget_tok, p_exit_tok=p_exit_tok)
     gst, gtr = gpu_state_np(st), gpu_trace_np(tr)
-    ref_state, ref_traces = oracle_run(inp)
+    ref_state, ref_traces = oracle_run(inp, token_budget=budget_tok, token_p_exit=p_exit_tok)
     stats = compare_stack(cfg, ref_state, ref_traces, gst, gtr, band=band,
                           band_budget=band_budget)
-    check_invariants_gpu(cfg, policy32(inp["policy"]), gst, gtr)
+    check_invariants_gpu(cfg, policy32(inp["policy"]), gst, gtr, budget_tok, p_exit_tok)
     log(f"[lookahead] ok {stats}")
     return inp, g, gtr, stats
 
@@ -120,3 +120,15 @@ def test_256_experts_look_ahead_tables_beyond_64k_lds():
                    normalize_topk=1, horizon=3, trans_support=8, n_tokens=32, **RECIPE)
     _, _, _, stats = _stack(cfg, 1e-5, 1e-7)
     assert stats["compared"] >= 40
+
+
+def test_per_token_budgets_and_requirements_horizon3():
+    # the recursion spends each token's own budget: zero for every third
+    # token (exact execution only), generous for others
+    cfg = workload("tiny_fp32", n_layers=4, top_k=2, normalize_topk=1, horizon=3, **RECIPE)
+    T = cfg["n_tokens"]
+    budget_tok = np.choose(np.arange(T) % 3, [0.0, 0.02, 0.05]).astype(np.float32)
+    p_exit_tok = np.where(np.arange(T) % 4 == 0, 2.0, 0.5).astype(np.float32)
+    _, _, gtr, stats = _stack(cfg, 1e-5, 1e-7, budget_tok, p_exit_tok)
+    assert stats["excluded_tokens"] <= 6
+    assert np.all(gtr["kind"][:, np.arange(T) % 3 == 0] != O.KIND_SUB)
