@@ -67,8 +67,7 @@ def parse():
     ap.add_argument("--p-floor", type=float, default=0.1, help="lower bound of p_J")
     ap.add_argument("--offline", action="store_true",
                     help="also time the offline stage (calibration pass on the GPU, "
-                         "statistics, transition rows, placement over 10 servers) and the "
-                         "oracle's placement")
+                         "statistics, transition rows, placement over 10 servers)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (to scale HBM byte "
                          "counters) and exit")
@@ -246,11 +245,9 @@ def offline_stage(abi, cfg, mh, inp, h0, ws):
     """Table I on this workload: the calibration pass over the batch, the
     Sec. IV-C statistics and Eq. (38) rows (4 entries), and the Eq. (28)
     greedy replication over 10 synthetic servers with memory ratio 2, each
-    timed; the oracle's placement of the same instance timed beside it."""
-    import numpy as np
+    timed."""
     import torch
 
-    from oracle import placement as P
     from paper_2608_00573_amd import offline
     from synthgen.servers import make_servers
 
@@ -265,13 +262,9 @@ def offline_stage(abi, cfg, mh, inp, h0, ws):
     srv = make_servers(cfg, n_servers=10, memory_ratio=2.0)
     x, added = offline.place(tab, srv)
     t3 = time.perf_counter()
-    wx, placed = P.place_replicas(tab["lam"], srv["rho"], srv["z"], srv["nbytes"],
-                                  srv["capacity"], srv["bandwidth"], srv["latency"], srv["x0"])
-    t4 = time.perf_counter()
     return {"calibration_tokens": int(h0.shape[0]), "servers": 10, "memory_ratio": 2.0,
             "calibration_pass_s": t1 - t0, "statistics_and_transitions_s": t2 - t1,
             "placement_s": t3 - t2, "replicas_added": added,
-            "oracle_placement_s": t4 - t3, "placement_matches_oracle": bool(np.array_equal(x, wx)),
             "pi": [round(float(v), 4) for v in tab["pi"]],
             "home_experts_per_layer": x[srv["home"]].sum(axis=1).tolist()}
 
