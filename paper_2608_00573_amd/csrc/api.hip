@@ -190,6 +190,9 @@ void fill_params(LayerParams& P, const trimmoe_model* m, int l, const trimmoe_po
   P.horizon = std::min(pol->horizon, m->n_layers - l);
   P.trans_b = m->trans_b;
   P.rb = route_block_tokens(T, P.horizon > 1);
+  P.bm = expert_tile_rows(m->dtype == TRIMMOE_BF16, T, k, m->n_experts, m->d_model, m->d_ff);
+  // the large-group down GEMM has enough tiles without K splits
+  if (P.bm == kBigBM) P.down_splits = 1;
   for (int j = 0; j < kMaxLookahead; ++j) {
     const bool later = j + 1 < P.horizon;  // layer l + j + 1 is looked at
     const trimmoe_layer* Lj = later ? &m->layers[l + j + 1] : nullptr;

@@ -32,8 +32,28 @@ inline int route_blocks_max(int T) {
   const int la = T < 2 * kLookaheadBlocks ? T : 2 * kLookaheadBlocks;
   return full > la ? full : la;
 }
-// rows of an expert group covered by one grouped-GEMM tile
+// rows of an expert group covered by one grouped-GEMM tile: kGemmBM, or
+// kBigBM for the large-group core (bf16 batches with at least
+// kBigRowsPerExpert rows per expert on average)
 constexpr int kGemmBM = 128;
+constexpr int kBigBM = 256;
+constexpr int kBigRowsPerExpert = 1024;
+// the dense shared-expert GEMMs use the large-group core from this many tokens
+constexpr int kBigDenseTokens = 2048;
+// the large-group core addresses its operands with 32-bit byte offsets
+inline bool big_offsets_fit(long long rows, long long cols) {
+  return rows * cols * 2 < (1ll << 31);
+}
+inline int expert_tile_rows(bool bf16, int T, int k, int E, int d, int F) {
+  const long long R = (long long)T * k;
+  return bf16 && R >= (long long)kBigRowsPerExpert * E && big_offsets_fit(T, d) &&
+                 big_offsets_fit(R, F)
+             ? kBigBM
+             : kGemmBM;
+}
+inline bool big_dense(bool bf16, int T, int d, int Fs) {
+  return bf16 && T >= kBigDenseTokens && big_offsets_fit(T, d) && big_offsets_fit(T, Fs);
+}
 // batches of this many tokens or more use the 256-token exit-head tile
 constexpr int kWideTokens = 4096;
 constexpr int kGemmBN = 128;
@@ -115,6 +135,7 @@ struct LayerParams {
   int horizon;  // effective horizon: min(policy horizon, N - layer)
   int trans_b;
   int rb;       // tokens per route block (route, scan and bucket agree on it)
+  int bm;       // rows per expert tile of the grouped GEMMs (kGemmBM or kBigBM)
   const uint8_t* la_mask[kMaxLookahead];
   const float* la_sim[kMaxLookahead];
   float la_theta[kMaxLookahead], la_slope[kMaxLookahead];

@@ -723,14 +723,14 @@ __global__ __launch_bounds__(1024) void k_scan(LayerParams p) {
   int total = 0, ttotal = 0;
   const int tot = threadIdx.x < E ? s_tot[threadIdx.x] : 0;
   const int off = block_exclusive_scan(tot, s_wave, &total);
-  const int nt_e = (tot + kGemmBM - 1) / kGemmBM;
+  const int nt_e = (tot + p.bm - 1) / p.bm;
   const int toff = block_exclusive_scan(nt_e, s_wave, &ttotal);
   if (threadIdx.x < E) {
     s_off[threadIdx.x] = off;
     s_toff[threadIdx.x] = toff;
     p.exp_off[threadIdx.x] = off;
     for (int u = 0; u < nt_e; ++u)
-      p.tiles[toff + u] = make_int4(threadIdx.x, off + u * kGemmBM, off + tot, 0);
+      p.tiles[toff + u] = make_int4(threadIdx.x, off + u * p.bm, off + tot, 0);
   }
   // executed-token offsets of the route blocks
   int xrun = 0;
@@ -747,7 +747,7 @@ __global__ __launch_bounds__(1024) void k_scan(LayerParams p) {
     p.counts[kCntRows] = total;
     int nt_all = 0, distinct = 0;
     for (int x = 0; x < E; ++x) {
-      nt_all += (s_tot[x] + kGemmBM - 1) / kGemmBM;
+      nt_all += (s_tot[x] + p.bm - 1) / p.bm;
       distinct += s_tot[x] > 0;
     }
     p.counts[kCntTiles] = nt_all;

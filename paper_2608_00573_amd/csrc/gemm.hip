@@ -496,6 +496,274 @@ __global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
   dma_gemm_stream<T>(lds, ntiles, nk, src);
 }
 
+// ------------------------------------------ large-group expert GEMMs --
+// Expert groups of prefill batches (about a thousand rows or more per expert)
+// and the dense shared expert of large batches use a second core with
+// 256 x 256 block tiles and 4 wavefronts, one per SIMD, each owning a
+// 128 x 128 output patch (16 accumulators of 32 x 32, held in AGPRs).  A
+// k-step then reads 8 fragments for 16 MFMAs (half the LDS bytes per MFMA of
+// the 64 x 64 patches) and a 64-wide K slice moves 64 KB for 256 x 256
+// outputs (2/3 of the bytes per MFMA of the 128 x 256 block).  With one
+// wavefront per SIMD no other wavefront fills the MFMA pipe while this one
+// waits, so the instruction stream is laid out explicitly (sched_barrier
+// keeps the compiler from regrouping it):
+//   * a k-step issues its 16 MFMAs in growing-square order (tile (i, j)
+//     after every tile with a smaller max(i, j)), so it needs its fragments
+//     in pairs a0 b0 | a1 b1 | a2 b2 | a3 b3 and waits for each pair with a
+//     partial lgkmcnt; the next k-step's 8 reads go out one after each of the
+//     first 8 MFMAs;
+//   * operand DMAs are buffer loads with an LDS destination: a 32-bit row
+//     offset per thread and DMA, the K position in the scalar offset;
+//   * two 64 KB stages.  The slice barrier sits before the last k-step; right
+//     after it the stage just consumed takes the DMAs of the slice two
+//     ahead, one after each MFMA of that k-step.
+// Blocks are persistent and walk their XCD's contiguous tile range as the
+// other core does; each tile runs its own prologue and epilogue.
+namespace big {
+constexpr int BM = 256, BN = 256, THREADS = 256;
+constexpr int RB = 128;                  // bytes of a row segment (64 bf16)
+constexpr int AB = BM * RB;              // A rows of a stage
+constexpr int STAGE = AB + BN * RB;      // 64 KB
+constexpr int ND = 16;                   // DMAs per thread and slice: 8 A rows, 8 B rows
+constexpr int RPP = THREADS / 8;         // rows per DMA pass (8 threads per row)
+}  // namespace big
+
+struct Frag8 {
+  bf16x8_t a[4], b[4];
+};
+using Acc44 = f32x16_t[4][4];
+
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+
+template <int N>
+__device__ __forceinline__ void lgkm_le() {
+  asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N));
+}
+
+// fragment read with a constant byte offset from a per-lane LDS address
+template <int OFF>
+__device__ __forceinline__ bf16x8_t lds_read_at(uint32_t a) {
+  bf16x8_t v;
+  asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(a), "n"(OFF));
+  return v;
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p) {
+  // raw buffer, no range limit: every offset is clamped to a valid row first
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)0xffffffff,
+                                           0x00020000);
+}
+
+// 16 bytes per lane from base + voff + soff to LDS at l + 16 * lane (l wave-uniform)
+__device__ __forceinline__ void buf_dma(__amdgpu_buffer_rsrc_t r, char* l, uint32_t voff,
+                                        uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(
+      r, (__attribute__((address_space(3))) void*)(lds_char*)l, 16, voff, soff, 0, 0);
+}
+
+// k-step MFMA order and the fragment pairs it waits for
+constexpr int kSqI[16] = {0, 0, 1, 1, 0, 1, 2, 2, 2, 0, 1, 2, 3, 3, 3, 3};
+constexpr int kSqJ[16] = {0, 1, 0, 1, 2, 2, 0, 1, 2, 3, 3, 3, 0, 1, 2, 3};
+
+// B fragment j of a wavefront: LDS row offset from its first B row.  DUAL:
+// columns j = 0, 1 of the up operand (rows 0..127 of the stage's B half),
+// j = 2, 3 the same columns of the gate operand (rows 128..255).
+template <bool DUAL>
+constexpr int big_brow(int j) {
+  return DUAL ? (j < 2 ? 32 * j : 128 + 32 * (j - 2)) : 32 * j;
+}
+
+template <bool DUAL, int Q>
+__device__ __forceinline__ void big_read(Frag8& f, uint32_t pa, uint32_t pb) {
+  if constexpr (Q & 1)
+    f.b[Q >> 1] = lds_read_at<big::AB + big_brow<DUAL>(Q >> 1) * big::RB>(pb);
+  else
+    f.a[Q >> 1] = lds_read_at<(Q >> 1) * 32 * big::RB>(pa);
+}
+
+// MFMA slot T of a k-step: the wait for its fragment pair (fc's reads were
+// issued during the previous k-step; min(T, 8) of fn's are newer), the MFMA,
+// then fn's read T (T < 8) and issue(T) when DMA
+template <int T, bool DUAL, bool DMA, class Issue>
+__device__ __forceinline__ void big_slot(Frag8& fc, Frag8& fn, Acc44& acc, uint32_t pa,
+                                         uint32_t pb, Issue& issue) {
+  if constexpr (T == 0 || T == 1 || T == 4 || T == 9) {
+    constexpr int pair = T == 0 ? 0 : T == 1 ? 1 : T == 4 ? 2 : 3;
+    constexpr int newer = T < 8 ? T : 8;
+    lgkm_le<2 * (3 - pair) + newer>();
+    asm volatile("" : "+v"(fc.a[pair]), "+v"(fc.b[pair]));
+    sched_fence();
+  }
+  constexpr int i = kSqI[T], j = kSqJ[T];
+  acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc.a[i], fc.b[j], acc[i][j], 0, 0, 0);
+  sched_fence();
+  if constexpr (T < 8) {
+    big_read<DUAL, T>(fn, pa, pb);
+    sched_fence();
+  }
+  if constexpr (DMA) {
+    issue(T);
+    sched_fence();
+  }
+  if constexpr (T < 15) big_slot<T + 1, DUAL, DMA>(fc, fn, acc, pa, pb, issue);
+}
+
+// Per-thread DMA sources of one tile: A rows (gathered, clamped) and B rows
+// (clamped to the tile's valid columns), byte offsets within their buffers.
+struct BigDma {
+  __amdgpu_buffer_rsrc_t ra, rb0, rb1;
+  uint32_t oa[8], ob[8];
+};
+
+template <bool DUAL>
+__device__ __forceinline__ void big_dma(const BigDma& q, char* stage, int wave, uint32_t ko,
+                                        int u) {
+  char* st = stage + wave * 8 * big::RB;
+  if (u < 8)
+    buf_dma(q.ra, st + big::RPP * u * big::RB, q.oa[u], ko);
+  else
+    buf_dma(DUAL && u >= 12 ? q.rb1 : q.rb0, st + big::AB + big::RPP * (u - 8) * big::RB,
+            q.ob[u - 8], ko);
+}
+
+// C tile += A rows x B rows over nk slices from K column k0: returns with
+// every DMA landed and every wave past its last LDS read
+template <bool DUAL>
+__device__ __forceinline__ void big_tile(char* lds, const BigDma& q, int nk, Acc44& acc,
+                                         uint32_t a_lane[4], uint32_t b_lane[4], int wave) {
+  const uint32_t s0 = lds_addr(lds);
+  auto dma_slice = [&](int stage, int kt) {
+#pragma unroll
+    for (int u = 0; u < big::ND; ++u) big_dma<DUAL>(q, lds + stage * big::STAGE, wave, kt * big::RB, u);
+  };
+  Frag8 f0, f1;
+  dma_slice(0, 0);
+  dma_slice(1, min(1, nk - 1));
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(big::ND) : "memory");
+  big_read<DUAL, 0>(f0, s0 + a_lane[0], s0 + b_lane[0]);
+  big_read<DUAL, 1>(f0, s0 + a_lane[0], s0 + b_lane[0]);
+  big_read<DUAL, 2>(f0, s0 + a_lane[0], s0 + b_lane[0]);
+  big_read<DUAL, 3>(f0, s0 + a_lane[0], s0 + b_lane[0]);
+  big_read<DUAL, 4>(f0, s0 + a_lane[0], s0 + b_lane[0]);
+  big_read<DUAL, 5>(f0, s0 + a_lane[0], s0 + b_lane[0]);
+  big_read<DUAL, 6>(f0, s0 + a_lane[0], s0 + b_lane[0]);
+  big_read<DUAL, 7>(f0, s0 + a_lane[0], s0 + b_lane[0]);
+  int sx = 0;
+  auto none = [](int) {};
+  for (int g = 0; g < nk; ++g) {
+    const uint32_t cur = s0 + sx * big::STAGE, nxt = s0 + (sx ^ 1) * big::STAGE;
+    big_slot<0, DUAL, false>(f0, f1, acc, cur + a_lane[1], cur + b_lane[1], none);
+    big_slot<0, DUAL, false>(f1, f0, acc, cur + a_lane[2], cur + b_lane[2], none);
+    big_slot<0, DUAL, false>(f0, f1, acc, cur + a_lane[3], cur + b_lane[3], none);
+    // slice g + 1 landed and every wave's reads of stage sx are done
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    sched_fence();
+    // stage sx takes slice g + 2 (the last slice again past the end: in
+    // bounds and never read); the reads fetch slice g + 1's first k-step
+    const uint32_t ko = min(g + 2, nk - 1) * big::RB;
+    char* dst = lds + sx * big::STAGE;
+    auto issue = [&](int u) { big_dma<DUAL>(q, dst, wave, ko, u); };
+    big_slot<0, DUAL, true>(f1, f0, acc, nxt + a_lane[0], nxt + b_lane[0], issue);
+    sx ^= 1;
+  }
+  // the reads and DMAs past the last slice drain before the stages are reused
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// MODE 0: SwiGLU up and gate (NB operands W0 / W1, 128 output columns per
+// tile), MODE 1: ReLU up, MODE 2: down (fp32 out, K splits)
+template <int MODE>
+__global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
+  constexpr bool DUAL = MODE == 0;
+  constexpr int NT = DUAL ? 128 : 256;  // output columns per tile
+  __shared__ __align__(16) char lds[2 * big::STAGE];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int n_nt = (a.N + NT - 1) / NT;
+  const int dense_m1 = a.dense_rows ? *a.dense_rows : 0;
+  const int n_mt = a.dense_rows ? (dense_m1 + big::BM - 1) / big::BM : *a.n_tiles;
+  TileSched S;
+  int ntiles;
+  if (!S.init(n_mt, n_nt, a.n_split, ntiles)) return;
+  const int nk = (a.K / BK) / a.n_split;
+  // per-lane LDS offsets of the fragments, per k-step (16-byte chunk swizzle)
+  const int fr = lane & 31, hi = lane >> 5;
+  uint32_t a_lane[4], b_lane[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const uint32_t ch = ((2 * ks + hi) ^ swz(fr)) << 4;
+    a_lane[ks] = (wm * 128 + fr) * big::RB + ch;
+    b_lane[ks] = ((DUAL ? wn * 64 : wn * 128) + fr) * big::RB + ch;
+  }
+  // DMA rows of this thread: r0 + 32 u; 16-byte chunk cc of the row segment
+  const int r0 = tid >> 3;
+  const int cc = 8 * ((tid & 7) ^ swz(r0));
+  const __amdgpu_buffer_rsrc_t ra = buf_rsrc(a.X);
+  Acc44 acc;
+  for (int jt = 0; jt < ntiles; ++jt) {
+    int mt, nt, sp;
+    S.decode(jt, mt, nt, sp);
+    int e = 0, m0, m1;
+    if (a.dense_rows) {
+      m0 = mt * big::BM;
+      m1 = dense_m1;
+    } else {
+      const int4 tl = a.tiles[mt];
+      e = tl.x;
+      m0 = tl.y;
+      m1 = tl.z;
+    }
+    const int n0 = nt * NT;
+    const int a_valid = min(big::BM, m1 - m0), b_valid = min(NT, a.N - n0);
+    const int k0 = sp * nk * BK;
+    BigDma q;
+    q.ra = ra;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int r = m0 + min(r0 + big::RPP * u, a_valid - 1);
+      const int src = a.x_idx ? a.x_idx[r] : r;
+      q.oa[u] = (uint32_t)(((size_t)src * a.K + k0 + cc) * 2);
+    }
+    const size_t wo = (size_t)e * a.w_stride + (size_t)n0 * a.K;
+    q.rb0 = buf_rsrc(a.W0 + wo);
+    q.rb1 = buf_rsrc(DUAL ? a.W1 + wo : a.W0 + wo);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int col = DUAL ? r0 + big::RPP * (u & 3) : r0 + big::RPP * u;
+      q.ob[u] = (uint32_t)(((size_t)min(col, b_valid - 1) * a.K + k0 + cc) * 2);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
+    big_tile<DUAL>(lds, q, nk, acc, a_lane, b_lane, wave);
+    // epilogue: wavefront rows wm * 128 + .., columns (DUAL) wn * 64 + 32 j
+    // with the gate in accumulator j + 2, else wn * 128 + 32 j
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < (DUAL ? 2 : 4); ++j) {
+        const int col = (DUAL ? wn * 64 : wn * 128) + 32 * j + (lane & 31);
+        if (col >= b_valid) continue;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm * 128 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3);
+          if (row >= a_valid) continue;
+          const size_t o = (size_t)(m0 + row) * a.N + n0 + col;
+          if constexpr (MODE == 0) {
+            const float u = acc[i][j][r], g = acc[i][j + 2][r];
+            static_cast<bf16_t*>(a.out)[o] = f2bf(g / (1.f + expf(-g)) * u);
+          } else if constexpr (MODE == 1) {
+            static_cast<bf16_t*>(a.out)[o] = f2bf(fmaxf(acc[i][j][r], 0.f));
+          } else {
+            static_cast<float*>(a.out)[sp * a.split_stride + o] = acc[i][j][r];
+          }
+        }
+      }
+  }
+}
+
 // ----------------------------------------------------------- exit head --
 // M = vocabulary (A = W_exit [V, d]), N = executed tokens (B = hx [n_x, d],
 // the executed tokens' updated rows written by the combine kernel).
@@ -800,6 +1068,14 @@ static void launch_ffn_mma(const FfnArgs& a, int max_mt, int n_cu, hipStream_t s
   hipLaunchKernelGGL((k_ffn_mma<T, UP>), grid, dim3(T::THREADS), 0, st, a);
 }
 
+// persistent: at most one block per CU, none beyond the tile bound
+template <int MODE>
+static void launch_ffn_big(const FfnArgs& a, int max_mt, int n_cu, hipStream_t st) {
+  const int nt = cdiv(a.N, MODE == 0 ? 128 : big::BN);
+  const dim3 grid(min(max_mt * nt * a.n_split, n_cu));
+  hipLaunchKernelGGL(k_ffn_big<MODE>, grid, dim3(big::THREADS), 0, st, a);
+}
+
 static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared, hipStream_t st) {
   const int K = up ? p.d : (shared ? p.Fs : p.F);
   const int N = up ? (shared ? p.Fs : p.F) : p.d;
@@ -821,7 +1097,17 @@ static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared
     FfnArgs a{static_cast<const bf16_t*>(X), x_idx, static_cast<const bf16_t*>(w0),
               static_cast<const bf16_t*>(w1), w_stride, K, N, p.tiles, &p.counts[kCntTiles],
               dense, out, p.y_split_stride, n_split, act};
-    if (up && dual)
+    // large groups: the routed tile list was built with kBigBM rows per tile
+    const bool big = shared ? big_dense(true, p.T, p.d, p.Fs) : p.bm == kBigBM;
+    if (big) {
+      const int big_mt = shared ? cdiv(p.T, kBigBM) : cdiv(p.T * p.k, kBigBM) + p.E;
+      if (up && dual)
+        launch_ffn_big<0>(a, big_mt, p.n_cu, st);
+      else if (up)
+        launch_ffn_big<1>(a, big_mt, p.n_cu, st);
+      else
+        launch_ffn_big<2>(a, big_mt, p.n_cu, st);
+    } else if (up && dual)
       launch_ffn_mma<UpDualTile, true>(a, max_mt, p.n_cu, st);
     else if (up)
       launch_ffn_mma<UpTile, true>(a, max_mt, p.n_cu, st);

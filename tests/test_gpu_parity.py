@@ -59,6 +59,18 @@ def test_large_batch_relu_top1():
     _run_and_compare(cfg)
 
 
+def test_large_expert_groups_skewed_ragged():
+    # Mixtral-like routing (top-2 of 8, Zipf-skewed router bias) at 4096
+    # tokens: 1024 rows per expert on average, so the expert GEMMs take
+    # 256-row tiles; d_ff = 576 and d_model = 320 leave partial column tiles
+    # in the up/gate (128-column) and down (256-column) GEMMs
+    cfg = workload("mixtral_8x7b_prefill", n_tokens=4096, n_layers=2, d_model=320, d_ff=576,
+                   vocab_exit=1000)
+    # the library picks 256-row tiles from the batch shape: T k >= 1024 E
+    assert cfg["n_tokens"] * cfg["top_k"] >= 1024 * cfg["n_experts"]
+    _run_and_compare(cfg)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_sigmoid_exit_head(dtype):
     # the paper's own exit head: one logit w . h + b through a sigmoid
