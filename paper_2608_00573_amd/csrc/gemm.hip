@@ -512,11 +512,17 @@ __global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
 //     in pairs a0 b0 | a1 b1 | a2 b2 | a3 b3 and waits for each pair with a
 //     partial lgkmcnt; the next k-step's 8 reads go out one after each of the
 //     first 8 MFMAs;
-//   * operand DMAs are buffer loads with an LDS destination: a 32-bit row
-//     offset per thread and DMA, the K position in the scalar offset;
-//   * two 64 KB stages.  The slice barrier sits before the last k-step; right
-//     after it the stage just consumed takes the DMAs of the slice two
-//     ahead, one after each MFMA of that k-step.
+//   * operands are staged through registers two slices ahead: during
+//     slice g each thread's 16 buffer loads (8 A rows, 8 B rows of 16 bytes;
+//     32-bit row offsets, the K position in the scalar offset) fetch slice
+//     g + 2, one after every other MFMA of the second half of each k-step,
+//     and its 16 ds_writes put slice g + 1 (fetched during slice g - 1) into
+//     the other LDS stage.  The global fetch is thereby spread evenly over
+//     the slice: an LDS-destination DMA of a whole 64 KB slice right after
+//     the barrier asks the texture path for about 128 B/clk per CU against
+//     the ~50 B/clk it sustains, and its stalls land on the MFMA issue;
+//   * two 64 KB stages and one barrier per slice, before the last k-step: it
+//     waits for LDS work only (this slice's reads, the next slice's writes).
 // Blocks are persistent and walk their XCD's contiguous tile range as the
 // other core does; each tile runs its own prologue and epilogue.
 namespace big {
@@ -554,11 +560,22 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* p) {
                                            0x00020000);
 }
 
-// 16 bytes per lane from base + voff + soff to LDS at l + 16 * lane (l wave-uniform)
-__device__ __forceinline__ void buf_dma(__amdgpu_buffer_rsrc_t r, char* l, uint32_t voff,
-                                        uint32_t soff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(
-      r, (__attribute__((address_space(3))) void*)(lds_char*)l, 16, voff, soff, 0, 0);
+// a buffer of no records: every load from it returns zeros
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc_empty(const void* p) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, 0, 0x00020000);
+}
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// 16 bytes per lane from a buffer at voff + soff into registers
+__device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+}
+
+// 16 bytes per lane to LDS at a + OFF
+template <int OFF>
+__device__ __forceinline__ void lds_write_at(uint32_t a, const u32x4_t& v) {
+  asm volatile("ds_write_b128 %0, %1 offset:%2" ::"v"(a), "v"(v), "n"(OFF));
 }
 
 // k-step MFMA order and the fragment pairs it waits for
@@ -581,15 +598,78 @@ __device__ __forceinline__ void big_read(Frag8& f, uint32_t pa, uint32_t pb) {
     f.a[Q >> 1] = lds_read_at<(Q >> 1) * 32 * big::RB>(pa);
 }
 
+// Per-thread operand rows of one tile: row u < 8 is A row r0 + 32 u (gathered,
+// clamped), u >= 8 B row r0 + 32 (u - 8) (clamped to the valid columns); byte
+// offsets of the thread's 16-byte chunk within their buffers at K = k0
+struct BigRows {
+  __amdgpu_buffer_rsrc_t ra, rb0, rb1, none;
+  uint32_t off[16];
+};
+
+// the buffers one slice is fetched from: a slice past the last one reads the
+// empty buffer, so it lands as zeros and adds nothing
+struct BigSrc {
+  __amdgpu_buffer_rsrc_t ra, rb0, rb1;
+  uint32_t ko;
+  __device__ __forceinline__ BigSrc(const BigRows& q, int kt, int nk) {
+    const bool live = kt < nk;
+    ra = live ? q.ra : q.none;
+    rb0 = live ? q.rb0 : q.none;
+    rb1 = live ? q.rb1 : q.none;
+    ko = live ? kt * big::RB : 0;
+  }
+};
+
+// registers holding one slice of a thread's 16 rows
+struct BigStage {
+  u32x4_t r[16];
+};
+
+template <bool DUAL>
+__device__ __forceinline__ void big_fetch(BigStage& R, const BigRows& q, const BigSrc& b, int u) {
+  const __amdgpu_buffer_rsrc_t& rs = u < 8 ? b.ra : (DUAL && u >= 12 ? b.rb1 : b.rb0);
+  R.r[u] = buf_load16(rs, q.off[u], b.ko);
+}
+
+// row u of the thread into its stage: A rows at u * 32 rows, B rows after
+// the A half (the thread's LDS address wa carries its row r0 and chunk slot)
+template <int U>
+__device__ __forceinline__ void big_put(uint32_t wa, const BigStage& R) {
+  lds_write_at<(U < 8 ? U * big::RPP * big::RB : big::AB + (U - 8) * big::RPP * big::RB)>(wa, R.r[U]);
+}
+
+__device__ __forceinline__ void big_put_rt(uint32_t wa, const BigStage& R, int u) {
+  switch (u) {
+    case 0: big_put<0>(wa, R); break;
+    case 1: big_put<1>(wa, R); break;
+    case 2: big_put<2>(wa, R); break;
+    case 3: big_put<3>(wa, R); break;
+    case 4: big_put<4>(wa, R); break;
+    case 5: big_put<5>(wa, R); break;
+    case 6: big_put<6>(wa, R); break;
+    case 7: big_put<7>(wa, R); break;
+    case 8: big_put<8>(wa, R); break;
+    case 9: big_put<9>(wa, R); break;
+    case 10: big_put<10>(wa, R); break;
+    case 11: big_put<11>(wa, R); break;
+    case 12: big_put<12>(wa, R); break;
+    case 13: big_put<13>(wa, R); break;
+    case 14: big_put<14>(wa, R); break;
+    default: big_put<15>(wa, R); break;
+  }
+}
+
 // MFMA slot T of a k-step: the wait for its fragment pair (fc's reads were
-// issued during the previous k-step; min(T, 8) of fn's are newer), the MFMA,
-// then fn's read T (T < 8) and issue(T) when DMA
-template <int T, bool DUAL, bool DMA, class Issue>
+// issued during the previous k-step; newer LDS operations are the NWP writes
+// that followed them there and the min(T, 8) reads of fn issued here), the
+// MFMA, then fn's read T (T < 8), fetch(l0 + ..) after MFMAs 8, 10, 12, 14
+// and put(w0 + ..) after MFMAs 9, 11, 13, 15 (NW of them)
+template <int T, bool DUAL, int NWP, int NW, class Fetch, class Put>
 __device__ __forceinline__ void big_slot(Frag8& fc, Frag8& fn, Acc44& acc, uint32_t pa,
-                                         uint32_t pb, Issue& issue) {
+                                         uint32_t pb, Fetch& fetch, int l0, Put& put, int w0) {
   if constexpr (T == 0 || T == 1 || T == 4 || T == 9) {
     constexpr int pair = T == 0 ? 0 : T == 1 ? 1 : T == 4 ? 2 : 3;
-    constexpr int newer = T < 8 ? T : 8;
+    constexpr int newer = NWP + (T < 8 ? T : 8);
     lgkm_le<2 * (3 - pair) + newer>();
     asm volatile("" : "+v"(fc.a[pair]), "+v"(fc.b[pair]));
     sched_fence();
@@ -601,45 +681,61 @@ __device__ __forceinline__ void big_slot(Frag8& fc, Frag8& fn, Acc44& acc, uint3
     big_read<DUAL, T>(fn, pa, pb);
     sched_fence();
   }
-  if constexpr (DMA) {
-    issue(T);
+  if constexpr (T >= 8 && (T & 1) == 0) {
+    fetch(l0 + (T - 8) / 2);
     sched_fence();
   }
-  if constexpr (T < 15) big_slot<T + 1, DUAL, DMA>(fc, fn, acc, pa, pb, issue);
+  if constexpr (T >= 9 && (T & 1) == 1 && (T - 9) / 2 < NW) {
+    put(w0 + (T - 9) / 2);
+    sched_fence();
+  }
+  if constexpr (T < 15) big_slot<T + 1, DUAL, NWP, NW>(fc, fn, acc, pa, pb, fetch, l0, put, w0);
 }
 
-// Per-thread DMA sources of one tile: A rows (gathered, clamped) and B rows
-// (clamped to the tile's valid columns), byte offsets within their buffers.
-struct BigDma {
-  __amdgpu_buffer_rsrc_t ra, rb0, rb1;
-  uint32_t oa[8], ob[8];
-};
-
-template <bool DUAL>
-__device__ __forceinline__ void big_dma(const BigDma& q, char* stage, int wave, uint32_t ko,
-                                        int u) {
-  char* st = stage + wave * 8 * big::RB;
-  if (u < 8)
-    buf_dma(q.ra, st + big::RPP * u * big::RB, q.oa[u], ko);
-  else
-    buf_dma(DUAL && u >= 12 ? q.rb1 : q.rb0, st + big::AB + big::RPP * (u - 8) * big::RB,
-            q.ob[u - 8], ko);
+// Slice g from stage H (H = g % 2): Rf receives slice g + 2, Rp holds slice
+// g + 1, which goes to the other stage
+template <bool DUAL, int H>
+__device__ __forceinline__ void big_half(uint32_t s0, const BigRows& q, int nk, int g, Acc44& acc,
+                                         const uint32_t (&a_lane)[4], const uint32_t (&b_lane)[4],
+                                         uint32_t w_lane, Frag8& f0, Frag8& f1, BigStage& Rf,
+                                         BigStage& Rp) {
+  const uint32_t cur = s0 + H * big::STAGE, nxt = s0 + (H ^ 1) * big::STAGE;
+  const BigSrc src(q, g + 2, nk);
+  auto fetch = [&](int u) { big_fetch<DUAL>(Rf, q, src, u); };
+  auto put = [&](int u) { big_put_rt(nxt + w_lane, Rp, u); };
+  big_slot<0, DUAL, 0, 4>(f0, f1, acc, cur + a_lane[1], cur + b_lane[1], fetch, 0, put, 0);
+  big_slot<0, DUAL, 4, 4>(f1, f0, acc, cur + a_lane[2], cur + b_lane[2], fetch, 4, put, 4);
+  big_slot<0, DUAL, 4, 4>(f0, f1, acc, cur + a_lane[3], cur + b_lane[3], fetch, 8, put, 8);
+  big_put<12>(nxt + w_lane, Rp);
+  big_put<13>(nxt + w_lane, Rp);
+  big_put<14>(nxt + w_lane, Rp);
+  big_put<15>(nxt + w_lane, Rp);
+  // the next slice is in its stage and every wave's reads of this one are done
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  sched_fence();
+  big_slot<0, DUAL, 0, 0>(f1, f0, acc, nxt + a_lane[0], nxt + b_lane[0], fetch, 12, put, 0);
 }
 
-// C tile += A rows x B rows over nk slices from K column k0: returns with
-// every DMA landed and every wave past its last LDS read
+// C tile += A rows x B rows over nk slices from the rows' K origin; returns
+// with every load landed and every wave past its last LDS access
 template <bool DUAL>
-__device__ __forceinline__ void big_tile(char* lds, const BigDma& q, int nk, Acc44& acc,
-                                         uint32_t a_lane[4], uint32_t b_lane[4], int wave) {
+__device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Acc44& acc,
+                                         const uint32_t (&a_lane)[4], const uint32_t (&b_lane)[4],
+                                         uint32_t w_lane) {
   const uint32_t s0 = lds_addr(lds);
-  auto dma_slice = [&](int stage, int kt) {
+  BigStage R0, R1;
+  auto fetch_all = [&](BigStage& R, int kt) {
+    const BigSrc src(q, kt, nk);
 #pragma unroll
-    for (int u = 0; u < big::ND; ++u) big_dma<DUAL>(q, lds + stage * big::STAGE, wave, kt * big::RB, u);
+    for (int u = 0; u < 16; ++u) big_fetch<DUAL>(R, q, src, u);
   };
+  // prologue: slice 0 through R0 into stage 0; slice 1 into R1
+  fetch_all(R0, 0);
+  fetch_all(R1, 1);
+#pragma unroll
+  for (int u = 0; u < 16; ++u) big_put_rt(s0 + w_lane, R0, u);
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   Frag8 f0, f1;
-  dma_slice(0, 0);
-  dma_slice(1, min(1, nk - 1));
-  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(big::ND) : "memory");
   big_read<DUAL, 0>(f0, s0 + a_lane[0], s0 + b_lane[0]);
   big_read<DUAL, 1>(f0, s0 + a_lane[0], s0 + b_lane[0]);
   big_read<DUAL, 2>(f0, s0 + a_lane[0], s0 + b_lane[0]);
@@ -648,25 +744,14 @@ __device__ __forceinline__ void big_tile(char* lds, const BigDma& q, int nk, Acc
   big_read<DUAL, 5>(f0, s0 + a_lane[0], s0 + b_lane[0]);
   big_read<DUAL, 6>(f0, s0 + a_lane[0], s0 + b_lane[0]);
   big_read<DUAL, 7>(f0, s0 + a_lane[0], s0 + b_lane[0]);
-  int sx = 0;
-  auto none = [](int) {};
-  for (int g = 0; g < nk; ++g) {
-    const uint32_t cur = s0 + sx * big::STAGE, nxt = s0 + (sx ^ 1) * big::STAGE;
-    big_slot<0, DUAL, false>(f0, f1, acc, cur + a_lane[1], cur + b_lane[1], none);
-    big_slot<0, DUAL, false>(f1, f0, acc, cur + a_lane[2], cur + b_lane[2], none);
-    big_slot<0, DUAL, false>(f0, f1, acc, cur + a_lane[3], cur + b_lane[3], none);
-    // slice g + 1 landed and every wave's reads of stage sx are done
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-    sched_fence();
-    // stage sx takes slice g + 2 (the last slice again past the end: in
-    // bounds and never read); the reads fetch slice g + 1's first k-step
-    const uint32_t ko = min(g + 2, nk - 1) * big::RB;
-    char* dst = lds + sx * big::STAGE;
-    auto issue = [&](int u) { big_dma<DUAL>(q, dst, wave, ko, u); };
-    big_slot<0, DUAL, true>(f1, f0, acc, nxt + a_lane[0], nxt + b_lane[0], issue);
-    sx ^= 1;
+  // two slices per trip (R0 and R1 swap roles with the stages); for an odd
+  // count the last trip's second slice is the zero slice past the end
+  for (int g = 0; g < nk; g += 2) {
+    big_half<DUAL, 0>(s0, q, nk, g, acc, a_lane, b_lane, w_lane, f0, f1, R0, R1);
+    big_half<DUAL, 1>(s0, q, nk, g + 1, acc, a_lane, b_lane, w_lane, f0, f1, R1, R0);
   }
-  // the reads and DMAs past the last slice drain before the stages are reused
+  // the zero slices fetched past the end drain before the registers and
+  // stages are reused
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
@@ -696,9 +781,12 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
     a_lane[ks] = (wm * 128 + fr) * big::RB + ch;
     b_lane[ks] = ((DUAL ? wn * 64 : wn * 128) + fr) * big::RB + ch;
   }
-  // DMA rows of this thread: r0 + 32 u; 16-byte chunk cc of the row segment
+  // operand rows of this thread: r0 + 32 u; it fetches the 16-byte chunk cc
+  // of each row segment and writes it to chunk slot tid & 7 of the LDS row,
+  // so the stage holds the swizzled layout the fragment reads expect
   const int r0 = tid >> 3;
   const int cc = 8 * ((tid & 7) ^ swz(r0));
+  const uint32_t w_lane = r0 * big::RB + (tid & 7) * 16;
   const __amdgpu_buffer_rsrc_t ra = buf_rsrc(a.X);
   Acc44 acc;
   for (int jt = 0; jt < ntiles; ++jt) {
@@ -717,13 +805,14 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
     const int n0 = nt * NT;
     const int a_valid = min(big::BM, m1 - m0), b_valid = min(NT, a.N - n0);
     const int k0 = sp * nk * BK;
-    BigDma q;
+    BigRows q;
     q.ra = ra;
+    q.none = buf_rsrc_empty(a.X);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int r = m0 + min(r0 + big::RPP * u, a_valid - 1);
       const int src = a.x_idx ? a.x_idx[r] : r;
-      q.oa[u] = (uint32_t)(((size_t)src * a.K + k0 + cc) * 2);
+      q.off[u] = (uint32_t)(((size_t)src * a.K + k0 + cc) * 2);
     }
     const size_t wo = (size_t)e * a.w_stride + (size_t)n0 * a.K;
     q.rb0 = buf_rsrc(a.W0 + wo);
@@ -731,13 +820,13 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int col = DUAL ? r0 + big::RPP * (u & 3) : r0 + big::RPP * u;
-      q.ob[u] = (uint32_t)(((size_t)min(col, b_valid - 1) * a.K + k0 + cc) * 2);
+      q.off[8 + u] = (uint32_t)(((size_t)min(col, b_valid - 1) * a.K + k0 + cc) * 2);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
-    big_tile<DUAL>(lds, q, nk, acc, a_lane, b_lane, wave);
+    big_tile<DUAL>(lds, q, nk, acc, a_lane, b_lane, w_lane);
     // epilogue: wavefront rows wm * 128 + .., columns (DUAL) wn * 64 + 32 j
     // with the gate in accumulator j + 2, else wn * 128 + 32 j
 #pragma unroll
