@@ -54,6 +54,14 @@ inline int expert_tile_rows(bool bf16, int T, int k, int E, int d, int F) {
 inline bool big_dense(bool bf16, int T, int d, int Fs) {
   return bf16 && T >= kBigDenseTokens && big_offsets_fit(T, d) && big_offsets_fit(T, Fs);
 }
+// the exit head uses the large-group core for wide models and large batches
+// (its 256-row vocabulary tiles match kExitTileBF16)
+constexpr int kBigExitTokens = 1024;
+constexpr int kBigExitDModel = 2048;
+inline bool big_exit(bool bf16, int T, int V, int d) {
+  return bf16 && T >= kBigExitTokens && d >= kBigExitDModel && big_offsets_fit(V, d) &&
+         big_offsets_fit(T, d);
+}
 // batches of this many tokens or more use the 256-token exit-head tile
 constexpr int kWideTokens = 4096;
 constexpr int kGemmBN = 128;

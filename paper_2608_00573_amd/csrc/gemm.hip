@@ -1040,6 +1040,118 @@ __global__ __launch_bounds__(T::THREADS) void k_exit_mma(ExitArgs a) {
   dma_gemm_stream<T>(lds, ntiles, a.K / BK, src);
 }
 
+// Exit head on the large-group core (large d): 256 vocabulary rows x 256
+// executed tokens per tile, the same softmax partials as the epilogue above.
+// A wavefront reduces its 128 rows of a token column (64 per lane, then the
+// other half-wavefront); the two row halves meet in LDS.
+__global__ __launch_bounds__(big::THREADS) void k_exit_big(ExitArgs a) {
+  __shared__ __align__(16) char lds[2 * big::STAGE];
+  __shared__ float2 s_part[2][big::BN];  // per row half: (max y, sum) per token column
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int n_x = *a.n_exec;
+  TileSched S;
+  int ntiles;
+  if (!S.init(a.n_vtiles, (n_x + big::BN - 1) / big::BN, 1, ntiles)) return;
+  const int nk = a.K / BK;
+  const int fr = lane & 31, hi = lane >> 5;
+  uint32_t a_lane[4], b_lane[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const uint32_t ch = ((2 * ks + hi) ^ swz(fr)) << 4;
+    a_lane[ks] = (wm * 128 + fr) * big::RB + ch;
+    b_lane[ks] = (wn * 128 + fr) * big::RB + ch;
+  }
+  const int r0 = tid >> 3;
+  const int cc = 8 * ((tid & 7) ^ swz(r0));
+  const uint32_t w_lane = r0 * big::RB + (tid & 7) * 16;
+  const float ninf = -__builtin_inff();
+  const float kLog2e = 1.4426950408889634f;
+  Acc44 acc;
+  for (int jt = 0; jt < ntiles; ++jt) {
+    int vt, tt, sp;
+    S.decode(jt, vt, tt, sp);
+    const int v0 = vt * big::BM, c0 = tt * big::BN;
+    const int a_valid = min(big::BM, a.V - v0), b_valid = min(big::BN, n_x - c0);
+    BigRows q;
+    q.ra = buf_rsrc(a.W);
+    q.rb0 = buf_rsrc(a.H + (size_t)c0 * a.K);
+    q.rb1 = q.rb0;
+    q.none = buf_rsrc_empty(a.W);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      q.off[u] = (uint32_t)(((size_t)(v0 + min(r0 + big::RPP * u, a_valid - 1)) * a.K + cc) * 2);
+      q.off[8 + u] = (uint32_t)(((size_t)min(r0 + big::RPP * u, b_valid - 1) * a.K + cc) * 2);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
+    big_tile<false>(lds, q, nk, acc, a_lane, b_lane, w_lane);
+    // partials in base 2 (y = z log2 e): per token column the largest y and
+    // the sum of 2^(y - max y) over the tile's vocabulary rows.  Two passes
+    // over the accumulators (the logit z is recomputed, nothing written back):
+    // the largest z, then sum 2^(z log2 e - max y), one FMA and one
+    // v_exp_f32 per logit.  Partial tiles (last vocabulary tile, or a bias)
+    // take the bias and row mask in both passes.
+    const bool full = a_valid == big::BM && !a.bias;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float mz = ninf;
+      if (full) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mz = fmaxf(mz, acc[i][j][r]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = wm * 128 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3);
+            const float b = a.bias ? a.bias[v0 + min(row, a_valid - 1)] : 0.f;
+            if (row < a_valid) mz = fmaxf(mz, acc[i][j][r] + b);
+          }
+      }
+      mz = fmaxf(mz, __shfl_xor(mz, 32));
+      const float m = mz * kLog2e;
+      float sum = 0.f;
+      if (mz != ninf) {
+        if (full) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -m));
+        } else {
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int row = wm * 128 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3);
+              const float b = a.bias ? a.bias[v0 + min(row, a_valid - 1)] : 0.f;
+              if (row < a_valid) sum += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r] + b, kLog2e, -m));
+            }
+        }
+      }
+      sum += __shfl_xor(sum, 32);
+      if (lane < 32) s_part[wm][wn * 128 + 32 * j + lane] = make_float2(m, sum);
+    }
+    __syncthreads();
+    const int c = tid;
+    if (c < b_valid) {
+      const float2 p0 = s_part[0][c], p1 = s_part[1][c];
+      const float M = fmaxf(p0.x, p1.x);
+      float S2 = 0.f;
+      if (p0.y > 0.f) S2 += p0.y * __builtin_amdgcn_exp2f(p0.x - M);
+      if (p1.y > 0.f) S2 += p1.y * __builtin_amdgcn_exp2f(p1.x - M);
+      a.partials[(size_t)(c0 + c) * a.n_vtiles + vt] = make_float2(M, S2);
+    }
+    // s_part is rewritten by the next tile's epilogue only after its main
+    // loop's barriers
+  }
+}
+
 // ------------------------------------------------------------- fp32 path --
 constexpr int FT = kF32Tile;
 
@@ -1236,7 +1348,10 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
     ExitArgs a{static_cast<const bf16_t*>(p.w_exit), static_cast<const bf16_t*>(p.hx), p.b_exit,
                &p.counts[kCntExec], p.V, p.d, p.n_vtiles, p.partials};
     // persistent: at most one block per CU, none beyond the tile bound
-    if (p.T <= kExitSmallTokens) {
+    if (big_exit(true, p.T, p.V, p.d)) {
+      const dim3 grid(min(p.n_vtiles * cdiv(p.T, big::BN), p.n_cu));
+      hipLaunchKernelGGL(k_exit_big, grid, dim3(big::THREADS), 0, st, a);
+    } else if (p.T <= kExitSmallTokens) {
       const dim3 grid(min(p.n_vtiles * cdiv(p.T, ExitSmall::BN), p.n_cu));
       hipLaunchKernelGGL(k_exit_mma<ExitSmall>, grid, dim3(ExitSmall::THREADS), 0, st, a);
     } else if (p.T >= kWideTokens) {

@@ -71,6 +71,15 @@ def test_large_expert_groups_skewed_ragged():
     _run_and_compare(cfg)
 
 
+def test_wide_model_exit_head_ragged():
+    # d_model 2048 at 1100 tokens: the exit head takes 256 x 256 tiles with
+    # 4 wavefronts; 1100 tokens and 1000 vocabulary rows leave partial token
+    # and vocabulary tiles
+    cfg = workload("tiny_fp32", dtype="bf16", n_tokens=1100, d_model=2048, d_ff=256,
+                   n_experts=4, n_local=2, vocab_exit=1000, n_layers=2)
+    _run_and_compare(cfg)
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_sigmoid_exit_head(dtype):
     # the paper's own exit head: one logit w . h + b through a sigmoid
