@@ -846,13 +846,28 @@ __global__ __launch_bounds__(256) void k_combine(LayerParams p) {
       acc[0] += a0.x; acc[1] += a0.y; acc[2] += a0.z; acc[3] += a0.w;
       acc[4] += a1.x; acc[5] += a1.y; acc[6] += a1.z; acc[7] += a1.w;
     }
+    // 8 elements = 16 bytes (bf16) or 32 bytes (fp32) per row access: rows
+    // start at multiples of d (a multiple of 8) in 16-byte aligned buffers
     ST* hr = h + (size_t)t * p.d + c;
     ST* xr = static_cast<ST*>(p.hx) + (size_t)j * p.d + c;
+    if constexpr (sizeof(ST) == 2) {
+      union {
+        uint4 v;
+        ST e[8];
+      } in, out;
+      in.v = *reinterpret_cast<const uint4*>(hr);
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const ST o = from_f32<ST>(to_f32<ST>(hr[u]) + acc[u]);
-      hr[u] = o;
-      xr[u] = o;
+      for (int u = 0; u < 8; ++u) out.e[u] = from_f32<ST>(to_f32<ST>(in.e[u]) + acc[u]);
+      *reinterpret_cast<uint4*>(hr) = out.v;
+      *reinterpret_cast<uint4*>(xr) = out.v;
+    } else {
+      float4* h4 = reinterpret_cast<float4*>(hr);
+      float4* x4 = reinterpret_cast<float4*>(xr);
+      float4 a0 = h4[0], a1 = h4[1];
+      a0.x += acc[0]; a0.y += acc[1]; a0.z += acc[2]; a0.w += acc[3];
+      a1.x += acc[4]; a1.y += acc[5]; a1.z += acc[6]; a1.w += acc[7];
+      h4[0] = a0; h4[1] = a1;
+      x4[0] = a0; x4[1] = a1;
     }
   }
 }
