@@ -692,15 +692,14 @@ __device__ __forceinline__ void big_slot(Frag8& fc, Frag8& fn, Acc44& acc, uint3
   if constexpr (T < 15) big_slot<T + 1, DUAL, NWP, NW>(fc, fn, acc, pa, pb, fetch, l0, put, w0);
 }
 
-// Slice g from stage H (H = g % 2): Rf receives slice g + 2, Rp holds slice
-// g + 1, which goes to the other stage
+// One slice from stage H: Rf receives the slice two ahead (rows q, buffers
+// and K position src), Rp holds the next slice, which goes to the other stage
 template <bool DUAL, int H>
-__device__ __forceinline__ void big_half(uint32_t s0, const BigRows& q, int nk, int g, Acc44& acc,
-                                         const uint32_t (&a_lane)[4], const uint32_t (&b_lane)[4],
-                                         uint32_t w_lane, Frag8& f0, Frag8& f1, BigStage& Rf,
-                                         BigStage& Rp) {
+__device__ __forceinline__ void big_half(uint32_t s0, const BigRows& q, const BigSrc& src,
+                                         Acc44& acc, const uint32_t (&a_lane)[4],
+                                         const uint32_t (&b_lane)[4], uint32_t w_lane, Frag8& f0,
+                                         Frag8& f1, BigStage& Rf, BigStage& Rp) {
   const uint32_t cur = s0 + H * big::STAGE, nxt = s0 + (H ^ 1) * big::STAGE;
-  const BigSrc src(q, g + 2, nk);
   auto fetch = [&](int u) { big_fetch<DUAL>(Rf, q, src, u); };
   auto put = [&](int u) { big_put_rt(nxt + w_lane, Rp, u); };
   big_slot<0, DUAL, 0, 4>(f0, f1, acc, cur + a_lane[1], cur + b_lane[1], fetch, 0, put, 0);
@@ -747,8 +746,8 @@ __device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Ac
   // two slices per trip (R0 and R1 swap roles with the stages); for an odd
   // count the last trip's second slice is the zero slice past the end
   for (int g = 0; g < nk; g += 2) {
-    big_half<DUAL, 0>(s0, q, nk, g, acc, a_lane, b_lane, w_lane, f0, f1, R0, R1);
-    big_half<DUAL, 1>(s0, q, nk, g + 1, acc, a_lane, b_lane, w_lane, f0, f1, R1, R0);
+    big_half<DUAL, 0>(s0, q, BigSrc(q, g + 2, nk), acc, a_lane, b_lane, w_lane, f0, f1, R0, R1);
+    big_half<DUAL, 1>(s0, q, BigSrc(q, g + 3, nk), acc, a_lane, b_lane, w_lane, f0, f1, R1, R0);
   }
   // the zero slices fetched past the end drain before the registers and
   // stages are reused
@@ -1044,6 +1043,103 @@ __global__ __launch_bounds__(T::THREADS) void k_exit_mma(ExitArgs a) {
 // executed tokens per tile, the same softmax partials as the epilogue above.
 // A wavefront reduces its 128 rows of a token column (64 per lane, then the
 // other half-wavefront); the two row halves meet in LDS.
+
+// operand rows of tile j: vocabulary rows (A) and executed-token rows (B),
+// clamped to the valid ones
+__device__ __forceinline__ void exit_big_rows(BigRows& q, const ExitArgs& a, const TileSched& S,
+                                              int n_x, int j, int r0, int cc) {
+  int vt, tt, sp;
+  S.decode(j, vt, tt, sp);
+  const int v0 = vt * big::BM, c0 = tt * big::BN;
+  const int a_valid = min(big::BM, a.V - v0), b_valid = min(big::BN, n_x - c0);
+  q.rb0 = buf_rsrc(a.H + (size_t)c0 * a.K);
+  q.rb1 = q.rb0;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    q.off[u] = (uint32_t)(((size_t)(v0 + min(r0 + big::RPP * u, a_valid - 1)) * a.K + cc) * 2);
+    q.off[8 + u] = (uint32_t)(((size_t)min(r0 + big::RPP * u, b_valid - 1) * a.K + cc) * 2);
+  }
+}
+
+// partials in base 2 (y = z log2 e) of tile j: per token column the largest y
+// and the sum of 2^(y - max y) over the tile's vocabulary rows.  Two passes
+// over the accumulators (the logit z is recomputed, nothing written back):
+// the largest z, then sum 2^(z log2 e - max y), one FMA and one v_exp_f32
+// per logit.  Partial tiles (last vocabulary tile, or a bias) take the bias
+// and row mask in both passes.  The LDS exchange waits for LDS work only, so
+// the next tile's fetches stay in flight.
+__device__ __forceinline__ void exit_big_epilogue(const ExitArgs& a, const TileSched& S, int n_x,
+                                                  int jt, const Acc44& acc,
+                                                  float2 (*s_part)[big::BN], int wm, int wn,
+                                                  int lane) {
+  int vt, tt, sp;
+  S.decode(jt, vt, tt, sp);
+  const int v0 = vt * big::BM, c0 = tt * big::BN;
+  const int a_valid = min(big::BM, a.V - v0), b_valid = min(big::BN, n_x - c0);
+  const int hi = lane >> 5;
+  const float ninf = -__builtin_inff();
+  const float kLog2e = 1.4426950408889634f;
+  const bool full = a_valid == big::BM && !a.bias;
+  // this lane's rows are wm * 128 + 4 hi + o, o = 32 i + 8 (r / 4) + r % 4;
+  // row o is valid for o < lim, and bias row min(o, lim - 1) stays in range
+  const int lim = a_valid - (wm * 128 + 4 * hi);
+  const float* bias = a.bias ? a.bias + v0 + wm * 128 + 4 * hi : nullptr;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float mz = ninf;
+    if (full) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mz = fmaxf(mz, acc[i][j][r]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int o = 32 * i + 8 * (r >> 2) + (r & 3);
+          const float b = bias ? bias[min(o, lim - 1)] : 0.f;
+          mz = fmaxf(mz, o < lim ? acc[i][j][r] + b : ninf);
+        }
+    }
+    mz = fmaxf(mz, __shfl_xor(mz, 32));
+    const float m = mz * kLog2e;
+    float sum = 0.f;
+    if (mz != ninf) {
+      if (full) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -m));
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int o = 32 * i + 8 * (r >> 2) + (r & 3);
+            const float b = bias ? bias[min(o, lim - 1)] : 0.f;
+            const float e = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r] + b, kLog2e, -m));
+            sum += o < lim ? e : 0.f;
+          }
+      }
+    }
+    sum += __shfl_xor(sum, 32);
+    if (lane < 32) s_part[wm][wn * 128 + 32 * j + lane] = make_float2(m, sum);
+  }
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  const int c = threadIdx.x;
+  if (c < b_valid) {
+    const float2 p0 = s_part[0][c], p1 = s_part[1][c];
+    const float M = fmaxf(p0.x, p1.x);
+    float S2 = 0.f;
+    if (p0.y > 0.f) S2 += p0.y * __builtin_amdgcn_exp2f(p0.x - M);
+    if (p1.y > 0.f) S2 += p1.y * __builtin_amdgcn_exp2f(p1.x - M);
+    a.partials[(size_t)(c0 + c) * a.n_vtiles + vt] = make_float2(M, S2);
+  }
+  // s_part is rewritten by the next epilogue only after the next tile's
+  // slice barriers
+}
+
 __global__ __launch_bounds__(big::THREADS) void k_exit_big(ExitArgs a) {
   __shared__ __align__(16) char lds[2 * big::STAGE];
   __shared__ float2 s_part[2][big::BN];  // per row half: (max y, sum) per token column
@@ -1066,89 +1162,18 @@ __global__ __launch_bounds__(big::THREADS) void k_exit_big(ExitArgs a) {
   const int r0 = tid >> 3;
   const int cc = 8 * ((tid & 7) ^ swz(r0));
   const uint32_t w_lane = r0 * big::RB + (tid & 7) * 16;
-  const float ninf = -__builtin_inff();
-  const float kLog2e = 1.4426950408889634f;
+  BigRows q;
+  q.ra = buf_rsrc(a.W);
+  q.none = buf_rsrc_empty(a.W);
   Acc44 acc;
   for (int jt = 0; jt < ntiles; ++jt) {
-    int vt, tt, sp;
-    S.decode(jt, vt, tt, sp);
-    const int v0 = vt * big::BM, c0 = tt * big::BN;
-    const int a_valid = min(big::BM, a.V - v0), b_valid = min(big::BN, n_x - c0);
-    BigRows q;
-    q.ra = buf_rsrc(a.W);
-    q.rb0 = buf_rsrc(a.H + (size_t)c0 * a.K);
-    q.rb1 = q.rb0;
-    q.none = buf_rsrc_empty(a.W);
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      q.off[u] = (uint32_t)(((size_t)(v0 + min(r0 + big::RPP * u, a_valid - 1)) * a.K + cc) * 2);
-      q.off[8 + u] = (uint32_t)(((size_t)min(r0 + big::RPP * u, b_valid - 1) * a.K + cc) * 2);
-    }
+    exit_big_rows(q, a, S, n_x, jt, r0, cc);
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
     big_tile<false>(lds, q, nk, acc, a_lane, b_lane, w_lane);
-    // partials in base 2 (y = z log2 e): per token column the largest y and
-    // the sum of 2^(y - max y) over the tile's vocabulary rows.  Two passes
-    // over the accumulators (the logit z is recomputed, nothing written back):
-    // the largest z, then sum 2^(z log2 e - max y), one FMA and one
-    // v_exp_f32 per logit.  Partial tiles (last vocabulary tile, or a bias)
-    // take the bias and row mask in both passes.
-    const bool full = a_valid == big::BM && !a.bias;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float mz = ninf;
-      if (full) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) mz = fmaxf(mz, acc[i][j][r]);
-      } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = wm * 128 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3);
-            const float b = a.bias ? a.bias[v0 + min(row, a_valid - 1)] : 0.f;
-            if (row < a_valid) mz = fmaxf(mz, acc[i][j][r] + b);
-          }
-      }
-      mz = fmaxf(mz, __shfl_xor(mz, 32));
-      const float m = mz * kLog2e;
-      float sum = 0.f;
-      if (mz != ninf) {
-        if (full) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -m));
-        } else {
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const int row = wm * 128 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3);
-              const float b = a.bias ? a.bias[v0 + min(row, a_valid - 1)] : 0.f;
-              if (row < a_valid) sum += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r] + b, kLog2e, -m));
-            }
-        }
-      }
-      sum += __shfl_xor(sum, 32);
-      if (lane < 32) s_part[wm][wn * 128 + 32 * j + lane] = make_float2(m, sum);
-    }
-    __syncthreads();
-    const int c = tid;
-    if (c < b_valid) {
-      const float2 p0 = s_part[0][c], p1 = s_part[1][c];
-      const float M = fmaxf(p0.x, p1.x);
-      float S2 = 0.f;
-      if (p0.y > 0.f) S2 += p0.y * __builtin_amdgcn_exp2f(p0.x - M);
-      if (p1.y > 0.f) S2 += p1.y * __builtin_amdgcn_exp2f(p1.x - M);
-      a.partials[(size_t)(c0 + c) * a.n_vtiles + vt] = make_float2(M, S2);
-    }
-    // s_part is rewritten by the next tile's epilogue only after its main
-    // loop's barriers
+    exit_big_epilogue(a, S, n_x, jt, acc, s_part, wm, wn, lane);
   }
 }
 
