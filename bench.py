@@ -127,29 +127,31 @@ def algorithmic_work(cfg, counters):
     return out
 
 
-def counter_traffic(kernel, workload):
-    """Calibrated HBM-side bytes per launch of ``kernel`` on ``workload`` from
-    the committed rocprofv3 counter summaries (FETCH_SIZE and WRITE_SIZE
-    passes scaled by a plain copy), or (None, None) when no summary covers it
-    or the kernel's source file has changed since the counters were taken."""
+def counter_traffic(cls, workload):
+    """Calibrated HBM-side bytes per launch of the kernel class ``cls`` on
+    ``workload`` from the committed rocprofv3 counter summaries (FETCH_SIZE and
+    WRITE_SIZE passes scaled by a plain copy): (bytes, summary path, kernel
+    name), or (None, None, None) when no summary covers it or the kernel's
+    source file has changed since the counters were taken."""
     import glob
     import hashlib
+    keys = ("class", "kernel", "workload", "traffic_bytes_per_launch", "source", "source_sha256")
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
-        fields = {}
-        for line in open(path):
-            k, sep, v = line.strip().partition(": ")
-            if sep and k in ("kernel", "workload", "traffic_bytes_per_launch", "source",
-                             "source_sha256"):
-                fields[k] = v.strip()
-        if fields.get("kernel") != kernel or fields.get("workload") != workload:
-            continue
-        src = os.path.join(ROOT, fields.get("source", ""))
-        if not os.path.isfile(src):
-            return None, None
-        if hashlib.sha256(open(src, "rb").read()).hexdigest() != fields.get("source_sha256"):
-            return None, None
-        return float(fields["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
-    return None, None
+        for block in open(path).read().split("```"):
+            fields = {}
+            for line in block.splitlines():
+                k, sep, v = line.strip().partition(": ")
+                if sep and k in keys:
+                    fields[k] = v.strip()
+            if fields.get("class") != cls or fields.get("workload") != workload:
+                continue
+            src = os.path.join(ROOT, fields.get("source", ""))
+            if not os.path.isfile(src) or \
+                    hashlib.sha256(open(src, "rb").read()).hexdigest() != fields.get("source_sha256"):
+                return None, None, None
+            return (float(fields["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT),
+                    fields.get("kernel"))
+    return None, None, None
 
 
 def _f64_layer_bytes(cfg):
@@ -368,10 +370,7 @@ def main():
     dom = max((c for c in classes if launches[c]), key=lambda c: t_class[ci[c]])
     dom_s = t_class[ci[dom]] * 1e-3
     mfma_bound = flop[dom] / (peak * 1e12) >= byts[dom] / (PEAK_HBM_GBS * 1e9)
-    dom_kernel = {"route": "k_route", "bucket": "k_bucket", "up": "k_ffn_mma",
-                  "down": "k_ffn_mma", "shared": "k_ffn_mma", "combine": "k_combine",
-                  "exit": "k_exit_mma", "gate": "k_exit_reduce"}[dom]
-    traffic, traffic_src = counter_traffic(dom_kernel, cfg["name"])
+    traffic, traffic_src, traffic_kernel = counter_traffic(dom, cfg["name"])
     if mfma_bound:
         achieved, pk, unit = flop[dom] / dom_s / 1e12, peak, "TFLOP/s"
     else:
@@ -407,12 +406,13 @@ def main():
         "roofline": {
             "kernel": {"route": "k_route (route, substitution, skip)",
                        "bucket": "k_scan + k_bucket (bucketing)",
-                       "up": "k_ffn_mma (grouped up/gate + activation)",
-                       "down": "k_ffn_mma (grouped down)",
-                       "shared": "k_ffn_mma (shared expert)",
+                       "up": "k_ffn_mma / k_ffn_big (grouped up/gate + activation)",
+                       "down": "k_ffn_mma / k_ffn_big (grouped down)",
+                       "shared": "k_ffn_mma / k_ffn_big (shared expert)",
                        "combine": "k_combine (weighted combine)",
-                       "exit": "k_exit_mma (exit head + softmax partials)",
+                       "exit": "k_exit_mma / k_exit_big (exit head + softmax partials)",
                        "gate": "k_exit_reduce + k_compact (exit gate)"}[dom],
+            "class": dom,
             "bound": "mfma" if mfma_bound else "hbm",
             "achieved": achieved,
             "peak": pk,
@@ -421,6 +421,7 @@ def main():
             "traffic": traffic,
             "traffic_unit": "bytes per launch",
             "traffic_source": traffic_src,
+            "traffic_kernel": traffic_kernel,
             "avg_launch_ms": t_class[ci[dom]] / launches[dom],
             "algorithmic_flop_per_launch": flop[dom] / launches[dom],
             "algorithmic_bytes_per_launch": byts[dom] / launches[dom],

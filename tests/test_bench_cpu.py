@@ -16,10 +16,30 @@ def test_more_than_one_gpu_is_refused():
 
 
 def test_counter_traffic_lookup():
-    # no summary covers an unknown kernel or workload
-    assert bench.counter_traffic("k_no_such_kernel", "switch_base_8e") == (None, None)
-    assert bench.counter_traffic("k_exit_mma", "no_such_workload") == (None, None)
-    # a covered kernel gives bytes and the summary's path, or None once the
-    # kernel source no longer matches the recorded hash
-    val, src = bench.counter_traffic("k_exit_mma", "switch_base_8e")
-    assert (val is None and src is None) or (val > 0 and src.startswith("profiles/"))
+    # no summary covers an unknown kernel class or workload
+    assert bench.counter_traffic("no_such_class", "switch_base_8e") == (None, None, None)
+    assert bench.counter_traffic("exit", "no_such_workload") == (None, None, None)
+    # a covered class gives bytes, the summary's path and the kernel measured,
+    # or nothing once the kernel source no longer matches the recorded hash
+    val, src, kern = bench.counter_traffic("exit", "switch_base_8e")
+    assert (val is None and src is None and kern is None) or \
+        (val > 0 and src.startswith("profiles/") and kern.startswith("k_exit"))
+
+
+def test_counter_traffic_blocks(tmp_path, monkeypatch):
+    # several machine-readable blocks in one summary, each found by class;
+    # a block whose source hash differs gives nothing
+    import hashlib
+    src = tmp_path / "k.hip"
+    src.write_text("kernel source")
+    sha = hashlib.sha256(src.read_bytes()).hexdigest()
+    (tmp_path / "profiles").mkdir()
+    (tmp_path / "profiles" / "w.md").write_text(
+        "# summary\n\n```\nclass: exit\nkernel: k_exit_x\nworkload: w\n"
+        "traffic_bytes_per_launch: 123\nsource: k.hip\nsource_sha256: " + sha + "\n```\n\n"
+        "```\nclass: down\nkernel: k_down_x\nworkload: w\n"
+        "traffic_bytes_per_launch: 456\nsource: k.hip\nsource_sha256: 00\n```\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.counter_traffic("exit", "w") == (123.0, "profiles/w.md", "k_exit_x")
+    assert bench.counter_traffic("down", "w") == (None, None, None)
+    assert bench.counter_traffic("up", "w") == (None, None, None)
