@@ -387,12 +387,25 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
           }
         }
       }
-      for (int k0 = ng * 128; k0 < dk; k0 += 32) {
-        const bf16x8_t bv = *reinterpret_cast<const bf16x8_t*>(wr + k0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8_t*>(h0 + k0),
-                                                       bv, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(*reinterpret_cast<const bf16x8_t*>(h1 + k0),
-                                                       bv, acc1, 0, 0, 0);
+      // the remaining 0..3 k-steps: every load issued before the first MFMA
+      // (offsets clamped to the last k-step: in bounds; their MFMAs are skipped)
+      const int rem = (dk - ng * 128) / 32;
+      if (rem > 0) {
+        bf16x8_t a0[3], a1[3], b[3];
+#pragma unroll
+        for (int u = 0; u < 3; ++u) {
+          const int o = ng * 128 + 32 * min(u, rem - 1);
+          a0[u] = *reinterpret_cast<const bf16x8_t*>(h0 + o);
+          a1[u] = *reinterpret_cast<const bf16x8_t*>(h1 + o);
+          b[u] = *reinterpret_cast<const bf16x8_t*>(wr + o);
+        }
+#pragma unroll
+        for (int u = 0; u < 3; ++u) {
+          if (u < rem) {
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[u], b[u], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[u], b[u], acc1, 0, 0, 0);
+          }
+        }
       }
       // accumulator: column = lane % 16 (expert), row = 4 * (lane / 16) + r (token)
       float* dst = zs + (size_t)kq * RB * E;
