@@ -21,6 +21,10 @@
 // (one block per CU); each block streams the K slices of its tiles
 // back to back, tiles taken from its XCD's contiguous range in patch order.
 //
+// Large expert groups, the dense shared expert of large batches and the exit
+// head of wide models run on a second bf16 core (4 wavefronts, 256 x 256
+// tiles, operands staged through registers; described with its kernels).
+//
 // fp32 path: plain FMA kernels for fp32 models.
 #include <math.h>
 
@@ -497,8 +501,9 @@ __global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
 }
 
 // ------------------------------------------ large-group expert GEMMs --
-// Expert groups of prefill batches (about a thousand rows or more per expert)
-// and the dense shared expert of large batches use a second core with
+// Expert groups of prefill batches (about a thousand rows or more per expert),
+// the dense shared expert of large batches and the exit head of wide models
+// (k_exit_big, below) use a second core with
 // 256 x 256 block tiles and 4 wavefronts, one per SIMD, each owning a
 // 128 x 128 output patch (16 accumulators of 32 x 32, held in AGPRs).  A
 // k-step then reads 8 fragments for 16 MFMAs (half the LDS bytes per MFMA of
@@ -530,8 +535,7 @@ constexpr int BM = 256, BN = 256, THREADS = 256;
 constexpr int RB = 128;                  // bytes of a row segment (64 bf16)
 constexpr int AB = BM * RB;              // A rows of a stage
 constexpr int STAGE = AB + BN * RB;      // 64 KB
-constexpr int ND = 16;                   // DMAs per thread and slice: 8 A rows, 8 B rows
-constexpr int RPP = THREADS / 8;         // rows per DMA pass (8 threads per row)
+constexpr int RPP = THREADS / 8;         // rows per fetch pass (8 threads per 128-byte row)
 }  // namespace big
 
 struct Frag8 {
