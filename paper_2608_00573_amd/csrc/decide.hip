@@ -81,23 +81,35 @@ static __host__ __device__ inline int route_ks(int E, int d) {
 
 // Eq. (3): best local substitute c(e) = argmin over local j != e with
 // Sim[e][j] >= sim_min of Q(e, j) = min(1, phi_scale (1 - Sim[e][j]) / 2),
-// ties to the lower j (-1: none), and its Q
+// ties to the lower j (-1: none), and its Q.  One wavefront per row e: each
+// lane scans j = lane, lane + 64, ... in order, then a butterfly takes the
+// least (Q, j) pair, which is what a serial scan that keeps the first least
+// Q returns (Q is never NaN: fminf(1, NaN) = 1).  Every lane gets the result.
 __device__ inline void best_substitute(const float* sim, const uint8_t* local, int E, int e,
-                                       float phi_scale, float sim_min, int& c, float& q) {
-  int best = -1;
+                                       float phi_scale, float sim_min, int lane, int& c,
+                                       float& q) {
+  int best = E;
   float bq = 0.f;
-  for (int j = 0; j < E; ++j) {
-    if (j == e || !local[j]) continue;
+  for (int j = lane; j < E; j += 64) {
     const float sv = sim[(size_t)e * E + j];
-    if (!(sv >= sim_min)) continue;
+    if (j == e || !local[j] || !(sv >= sim_min)) continue;
     const float qj = fminf(1.f, phi_scale * (1.f - sv) * 0.5f);
-    if (best < 0 || qj < bq) {
+    if (best == E || qj < bq) {
       best = j;
       bq = qj;
     }
   }
-  c = best;
-  q = bq;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float oq = __shfl_xor(bq, off);
+    const int oj = __shfl_xor(best, off);
+    if (oj < E && (best == E || oq < bq || (oq == bq && oj < best))) {
+      best = oj;
+      bq = oq;
+    }
+  }
+  c = best < E ? best : -1;
+  q = best < E ? bq : 0.f;
 }
 
 // ------------------------------------------------ look-ahead (Eq. (39)) --
@@ -264,12 +276,14 @@ __host__ __device__ inline size_t la_carve(char* base, int E, int B, int k, int 
 }
 
 // One block = RB active tokens.  Phase 0: the layer's substitute table
-// (and, with look-ahead, the later layers' tables and transitions).
-// Phase 1: router logits into LDS (MFMA 16x16x32 bf16 tiles, or fp32 FMA).
-// Phase 2: one thread per token runs the decision; with look-ahead (LA) the
-// block first evaluates the cost-to-go of every candidate action of its
-// tokens, one wavefront per token, its lanes over (action, next-layer tuple)
-// branches.  Phase 3: per-block expert histogram for the bucketing.
+// (and, with look-ahead, the later layers' tables and transitions), one
+// wavefront per expert row.  Phase 1: router logits into LDS (MFMA 16x16x32
+// bf16 tiles, or fp32 FMA).  Phase 2: top-k and softmax weights with a lane
+// group per token, then one thread per token runs the decision; with
+// look-ahead (LA) the block first evaluates the cost-to-go of every
+// candidate action of its tokens, one wavefront per token, its lanes over
+// (action, next-layer tuple) branches.  Phase 3: per-block expert histogram
+// for the bucketing.
 template <bool BF16, bool LA>
 __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   extern __shared__ float zs[];  // [route_ks][RB][E] logits, K partial sums; then LaLds
@@ -283,6 +297,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   __shared__ int sRsub[RB][KMAX];   // ranks of substitutable remote slots
   __shared__ int sRx[RB][KMAX];     // merged rows: expert
   __shared__ float sRw[RB][KMAX];   // merged rows: summed weight
+  __shared__ float sI[RB];          // importance: summed weight of the picks
 
   const int n_a = *p.n_active;
   const int base = blockIdx.x * p.rb;
@@ -292,13 +307,16 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   for (int e = threadIdx.x; e < E; e += blockDim.x) s_cnt[e] = 0;
   if (threadIdx.x == 0) s_xcnt = 0;
 
-  // Eq. (3): the layer's substitute table
-  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+  // Eq. (3): the layer's substitute table, one wavefront per expert
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int e = wave; e < E; e += kRouteWaves) {
     int c;
     float q;
-    best_substitute(p.sim, p.local_mask, E, e, p.phi_scale, p.sim_min, c, q);
-    s_subc[e] = c;
-    s_subq[e] = q;
+    best_substitute(p.sim, p.local_mask, E, e, p.phi_scale, p.sim_min, lane, c, q);
+    if (lane == 0) {
+      s_subc[e] = c;
+      s_subq[e] = q;
+    }
   }
 
   LaLds la;
@@ -310,14 +328,16 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     la_carve(reinterpret_cast<char*>(zs + (size_t)ks * RB * E), E, B, k, nlev, &la);
     // later layers: placement, substitute tables, theta and slope; the
     // transitions out of this layer and every later one but the last
-    for (int idx = threadIdx.x; idx < nlev * E; idx += blockDim.x) {
+    for (int idx = wave; idx < nlev * E; idx += kRouteWaves) {
       const int j = idx / E, e = idx % E;
       int c;
       float q;
-      best_substitute(p.la_sim[j], p.la_mask[j], E, e, p.phi_scale, p.sim_min, c, q);
-      la.mask[idx] = p.la_mask[j][e] ? 1 : 0;
-      la.subc[idx] = (int16_t)c;
-      la.subq[idx] = q;
+      best_substitute(p.la_sim[j], p.la_mask[j], E, e, p.phi_scale, p.sim_min, lane, c, q);
+      if (lane == 0) {
+        la.mask[idx] = p.la_mask[j][e] ? 1 : 0;
+        la.subc[idx] = (int16_t)c;
+        la.subq[idx] = q;
+      }
     }
     for (int idx = threadIdx.x; idx < nlev * E * B; idx += blockDim.x) {
       const int j = idx / (E * B), r = idx % (E * B);
@@ -345,7 +365,6 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     // valid row (never stored).
     const bf16_t* h = static_cast<const bf16_t*>(p.h);
     const bf16_t* W = static_cast<const bf16_t*>(p.w_router);
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int nct = (E + 15) >> 4, ks = route_ks(E, d), dk = d / ks;
     const int tl = lane & 15, kl = 8 * (lane >> 4);
     const int t0 = p.active_idx[base + min(tl, nt - 1)];
@@ -439,48 +458,87 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   }
   __syncthreads();
 
+  // Eq. (4) per token, G lanes per token (G the least power of two >= E, at
+  // most 64; a wavefront takes 64 / G tokens at once), each lane over
+  // experts e = g, g + G, ...: biased logits (NaN ranks last), the top-k in
+  // rank order (larger logit first, ties to the lower id; each pick is the
+  // best logit ranked strictly after the previous one) and the softmax
+  // weights of the picks.  Butterflies stay inside the lane group.
+  {
+    int G = 1;
+    while (G < E && G < 64) G <<= 1;
+    const int tpw = 64 / G, g = lane & (G - 1);
+    for (int t0 = wave * tpw; t0 < nt; t0 += kRouteWaves * tpw) {
+      const int ti = t0 + lane / G;
+      if (ti >= nt) continue;
+      float* z = zs + ti * E;
+      const float ninf = -__builtin_inff();
+      for (int e = g; e < E; e += G) {
+        const float v = z[e] + (p.b_router ? p.b_router[e] : 0.f);
+        z[e] = (v == v) ? v : ninf;
+      }
+      float vprev = 0.f, vtop[KMAX];
+      int iprev = -1;
+#pragma unroll
+      for (int r = 0; r < KMAX; ++r) {
+        if (r >= k) break;
+        int be = E;
+        float bv = 0.f;
+        for (int e = g; e < E; e += G) {
+          const float v = z[e];
+          const bool after = (r == 0) || (v < vprev) || (v == vprev && e > iprev);
+          if (after && (be == E || v > bv)) {
+            be = e;
+            bv = v;
+          }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+          if (off >= G) continue;
+          const float ov = __shfl_xor(bv, off);
+          const int oe = __shfl_xor(be, off);
+          if (oe < E && (be == E || ov > bv || (ov == bv && oe < be))) {
+            be = oe;
+            bv = ov;
+          }
+        }
+        if (g == 0) sS[ti][r] = be < E ? be : -1;
+        vtop[r] = bv;
+        vprev = bv;
+        iprev = be;
+      }
+      // p_e = exp(z_e - max) / sum over all E; the lane partials of the sum
+      // are added in a fixed butterfly, so every lane of the group holds it
+      const float zmax = vtop[0];
+      float sum = 0.f;
+      for (int e = g; e < E; e += G) sum += expf(z[e] - zmax);
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1)
+        if (off < G) sum += __shfl_xor(sum, off);
+      if (g == 0) {
+        float imp = 0.f;
+#pragma unroll
+        for (int r = 0; r < KMAX; ++r) {
+          if (r >= k) break;
+          const float pr = expf(vtop[r] - zmax) / sum;
+          sW[ti][r] = pr;
+          imp += pr;
+        }
+        if (p.normalize)
+          for (int r = 0; r < k; ++r) sW[ti][r] = sW[ti][r] / imp;
+        sI[ti] = imp;
+      }
+    }
+  }
+  __syncthreads();
+
   const int i = threadIdx.x;
   int pos = 0, t = 0, n_loc = 0, n_rem = 0, nsub = 0;
   float I = 0.f, budget = 0.f, D = 0.f;
   if (i < nt) {
     pos = base + i;
     t = p.active_idx[pos];
-    float* z = zs + i * E;
-    const float ninf = -__builtin_inff();
-    for (int e = 0; e < E; ++e) {
-      float v = z[e] + (p.b_router ? p.b_router[e] : 0.f);
-      z[e] = (v == v) ? v : ninf;  // NaN ranks last
-    }
-    // top-k in rank order (ties to the lower id), selection without flags:
-    // the next pick is the largest logit ranked strictly after the last one
-    float vprev = 0.f;
-    int iprev = -1;
-    for (int r = 0; r < k; ++r) {
-      int be = -1;
-      float bv = 0.f;
-      for (int e = 0; e < E; ++e) {
-        const float v = z[e];
-        const bool after = (r == 0) || (v < vprev) || (v == vprev && e > iprev);
-        if (after && (be < 0 || v > bv)) {
-          be = e;
-          bv = v;
-        }
-      }
-      sS[i][r] = be;
-      vprev = bv;
-      iprev = be;
-    }
-    // softmax over all E (Eq. (4)): p_e = exp(z_e - max) / sum
-    const float zmax = z[sS[i][0]];
-    float sum = 0.f;
-    for (int e = 0; e < E; ++e) sum += expf(z[e] - zmax);
-    for (int r = 0; r < k; ++r) {
-      const float pr = expf(z[sS[i][r]] - zmax) / sum;
-      sW[i][r] = pr;
-      I += pr;
-    }
-    if (p.normalize)
-      for (int r = 0; r < k; ++r) sW[i][r] = sW[i][r] / I;
+    I = sI[i];
 
     // resolve slots: local exact, or remote with/without a local substitute
     for (int r = 0; r < k; ++r) {
@@ -521,7 +579,6 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     __syncthreads();
     // tokens in flight per round and wavefronts per token (a block of few
     // tokens gives each token several wavefronts)
-    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int tpr = min(p.rb, kRouteWaves), wpt = kRouteWaves / tpr;
     const int slot = wave / wpt, wsub = wave % wpt;
     const int ntup = lv.ntup, rem = nlev - 1;

@@ -13,8 +13,10 @@ if torch.cuda.is_available():
                                    gpu_trace_np, log, oracle_run, policy32, teacher_forced)
 
 
-def _run_and_compare(cfg, pol=None, **kw):
+def _run_and_compare(cfg, pol=None, edit=None, **kw):
     inp = make_inputs(cfg)
+    if edit is not None:
+        edit(inp)
     log(f"[parity] {cfg['name']} T={cfg['n_tokens']} N={cfg['n_layers']} {kw}")
     g = GpuRun(inp)
     st, tr = g.stack(pol=pol, **{k: v for k, v in kw.items() if k in ("p_exit_tok", "budget_tok")})
@@ -89,6 +91,37 @@ def test_sigmoid_exit_head(dtype):
     _, gst, gtr, _, _, _ = _run_and_compare(cfg)
     exits = [(gst["exit_layer"] == l).sum() for l in range(cfg["n_layers"])]
     assert sum(e > 0 for e in exits) >= 2
+
+
+def test_many_experts_bf16_top4_substitution():
+    # 160 SwiGLU experts, top-4, 80 local, in bf16: each lane of the
+    # substitute table's wavefront scans two or three candidates (160 =
+    # 2 x 64 + 32) and the router's MFMA tiles span 10 expert column tiles
+    cfg = workload("qwen_moe_a2_7b", n_tokens=512, n_layers=2, d_model=256, d_ff=128,
+                   d_ff_shared=128, n_experts=160, n_local=80, vocab_exit=1000)
+    _, _, gtr, _, _, _ = _run_and_compare(cfg)
+    assert (gtr["kind"] == O.KIND_SUB).any()
+    assert (gtr["action"] == O.ACT_SKIP).any()
+
+
+@pytest.mark.parametrize("E,k", [(8, 2), (60, 4)])
+def test_tied_router_logits_rank_lower_id_first(E, k):
+    # router rows duplicated in pairs: experts 2j and 2j + 1 get bitwise equal
+    # logits, so the rank order takes 2j first and its twin right after it
+    # (8 experts: 8-lane groups per token; 60: a whole wavefront per token)
+    cfg = workload("tiny_fp32", dtype="bf16", n_experts=E, n_local=E // 2, top_k=k,
+                   normalize_topk=1, n_tokens=300, n_layers=2)
+
+    def tie(inp):
+        for L in inp["layers"]:
+            L["w_router"][1::2] = L["w_router"][0::2]
+
+    _, _, gtr, _, _, _ = _run_and_compare(cfg, edit=tie)
+    tgt = gtr["target"].reshape(cfg["n_layers"], cfg["n_tokens"], k)
+    live = tgt[..., 0] >= 0
+    for r in range(0, k, 2):
+        assert np.all(tgt[..., r][live] % 2 == 0)
+        assert np.all(tgt[..., r + 1][live] == tgt[..., r][live] + 1)
 
 
 def test_ragged_tokens_bf16_relu():
