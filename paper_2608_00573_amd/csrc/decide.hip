@@ -836,40 +836,43 @@ __global__ __launch_bounds__(1024) void k_scan(LayerParams p) {
 // row_src[row] names the token whose h row the grouped GEMM gathers, and
 // exec_list / exec_pos list the executed tokens in active order.
 __global__ __launch_bounds__(256) void k_bucket(LayerParams p) {
-  __shared__ int s_exec[RB * KMAX];
-  __shared__ int s_act[RB];
+  static_assert(RB <= 32 && RB * KMAX <= 256, "token masks and one thread per slot");
+  __shared__ unsigned s_emask[TRIMMOE_MAX_EXPERTS];  // block tokens holding a row of e
+  __shared__ int s_off[TRIMMOE_MAX_EXPERTS];         // the block's first row of e
+  __shared__ unsigned s_xmask;                       // block tokens that execute
   const int n_a = *p.n_active;
   const int base = blockIdx.x * p.rb;
   if (base >= n_a) return;
   const int nt = min(p.rb, n_a - base);
   const int k = p.k, E = p.E;
-  const int i = threadIdx.x;
-  if (i < nt) {
-    const int pos = base + i;
-    s_act[i] = p.tok_action[pos];
-    for (int j = 0; j < k; ++j) s_exec[i * k + j] = p.tok_exec[(size_t)pos * k + j];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < E; e += blockDim.x) {
+    s_emask[e] = 0u;
+    s_off[e] = p.exp_off[e] + p.blk_off[(size_t)blockIdx.x * E + e];
   }
+  if (tid == 0) s_xmask = 0u;
   __syncthreads();
-  if (i < nt) {
-    const int pos = base + i;
-    const int t = p.active_idx[pos];
-    for (int j = 0; j < k; ++j) {
-      const int e = s_exec[i * k + j];
-      if (e < 0) break;
-      int rank = 0;
-      for (int i2 = 0; i2 < i; ++i2)
-        for (int j2 = 0; j2 < k; ++j2) rank += (s_exec[i2 * k + j2] == e);
-      const int row = p.exp_off[e] + p.blk_off[(size_t)blockIdx.x * E + e] + rank;
-      p.tok_row[(size_t)pos * k + j] = row;
-      p.row_src[row] = t;
-    }
-    if (s_act[i] == TRIMMOE_ACT_EXEC) {
-      int xr = 0;
-      for (int i2 = 0; i2 < i; ++i2) xr += (s_act[i2] == TRIMMOE_ACT_EXEC);
-      const int xidx = p.blk_xoff[blockIdx.x] + xr;
-      p.exec_list[xidx] = t;
-      p.exec_pos[xidx] = pos;
-    }
+  // thread (token i, slot j); a token's merged rows are distinct experts
+  // packed at the front of its slots, so the rows of e before token i's
+  // are one per earlier block token that holds e
+  const int i = tid / k, j = tid - (tid / k) * k;
+  const int pos = base + i;
+  int e = -1;
+  if (tid < nt * k) {
+    e = p.tok_exec[(size_t)pos * k + j];
+    if (e >= 0) atomicOr(&s_emask[e], 1u << i);
+  }
+  if (tid < nt && p.tok_action[base + tid] == TRIMMOE_ACT_EXEC) atomicOr(&s_xmask, 1u << tid);
+  __syncthreads();
+  if (e >= 0) {
+    const int row = s_off[e] + __popc(s_emask[e] & ((1u << i) - 1u));
+    p.tok_row[(size_t)pos * k + j] = row;
+    p.row_src[row] = p.active_idx[pos];
+  }
+  if (tid < nt && ((s_xmask >> tid) & 1u)) {
+    const int xidx = p.blk_xoff[blockIdx.x] + __popc(s_xmask & ((1u << tid) - 1u));
+    p.exec_list[xidx] = p.active_idx[base + tid];
+    p.exec_pos[xidx] = base + tid;
   }
 }
 
