@@ -773,18 +773,33 @@ __global__ __launch_bounds__(1024) void k_scan(LayerParams p) {
   const int L = (nb + S - 1) / S;        // route blocks per segment
   const int e = threadIdx.x % ep, g = threadIdx.x / ep;
   const int b0 = g * L, b1 = min(nb, b0 + L);
+  // the counts of a segment are read in chunks of 8, every load of a chunk
+  // before its stores, so the loads of a chunk are in flight together
+  constexpr int CH = 8;
   int sum = 0;
   if (e < E)
-    for (int b = b0; b < b1; ++b) sum += p.blk_cnt[(size_t)b * E + e];
+    for (int b = b0; b < b1; b += CH) {
+      int c[CH];
+#pragma unroll
+      for (int u = 0; u < CH; ++u) c[u] = b + u < b1 ? p.blk_cnt[(size_t)(b + u) * E + e] : 0;
+#pragma unroll
+      for (int u = 0; u < CH; ++u) sum += c[u];
+    }
   s_seg[g * ep + e] = sum;
   __syncthreads();
   if (e < E) {
     int run = 0;
     for (int q = 0; q < g; ++q) run += s_seg[q * ep + e];
-    for (int b = b0; b < b1; ++b) {
-      const int c = p.blk_cnt[(size_t)b * E + e];
-      p.blk_off[(size_t)b * E + e] = run;
-      run += c;
+    for (int b = b0; b < b1; b += CH) {
+      int c[CH];
+#pragma unroll
+      for (int u = 0; u < CH; ++u) c[u] = b + u < b1 ? p.blk_cnt[(size_t)(b + u) * E + e] : 0;
+#pragma unroll
+      for (int u = 0; u < CH; ++u)
+        if (b + u < b1) {
+          p.blk_off[(size_t)(b + u) * E + e] = run;
+          run += c[u];
+        }
     }
     if (g == S - 1) s_tot[e] = run;
   }
@@ -957,6 +972,9 @@ __global__ __launch_bounds__(256) void k_exit_reduce(LayerParams p) {
   if (j >= n_x) return;
   const int nv = p.n_vtiles;
   const float2* pr = p.partials + (size_t)j * nv;
+  // the token's ids are read first, so their latency overlaps the partials'
+  const int t = p.exec_list[j];
+  const int pos = p.exec_pos[j];
   float m = -__builtin_inff();
   for (int u = lane; u < nv; u += 64) m = fmaxf(m, pr[u].x);
   for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
@@ -971,8 +989,6 @@ __global__ __launch_bounds__(256) void k_exit_reduce(LayerParams p) {
     const float xi = p.conf_mode == TRIMMOE_CONF_SIGMOID
                          ? 1.f / (1.f + exp2f(-m))  // m = logit * log2 e
                          : 1.f / s;
-    const int t = p.exec_list[j];
-    const int pos = p.exec_pos[j];
     p.xi[t] = xi;
     if (p.tr_xi) p.tr_xi[t] = xi;
     const float pj = p.p_exit_tok ? p.p_exit_tok[t] : p.p_exit;
