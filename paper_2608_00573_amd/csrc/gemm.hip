@@ -1070,8 +1070,9 @@ __device__ __forceinline__ void exit_big_rows(BigRows& q, const ExitArgs& a, con
 // over the accumulators (the logit z is recomputed, nothing written back):
 // the largest z, then sum 2^(z log2 e - max y), one FMA and one v_exp_f32
 // per logit.  Partial tiles (last vocabulary tile, or a bias) take the bias
-// and row mask in both passes.  The LDS exchange waits for LDS work only, so
-// the next tile's fetches stay in flight.
+// and row mask in both passes.  The tile's loads have all landed by now (the
+// next tile fetches its first slices after this), so the LDS exchange waits
+// for LDS work only.
 __device__ __forceinline__ void exit_big_epilogue(const ExitArgs& a, const TileSched& S, int n_x,
                                                   int jt, const Acc44& acc,
                                                   float2 (*s_part)[big::BN], int wm, int wn,
