@@ -845,26 +845,119 @@ __global__ __launch_bounds__(1024) void k_scan(LayerParams p) {
 }
 
 // ------------------------------------------------- stable row permutation --
+// bounds of the fused scan: block histogram entries (route blocks x experts)
+// and route blocks a bucket block holds in LDS
+constexpr int kFusedScanEntries = 4096;
+constexpr int kFusedScanBlocks = 1024;
 // Row of (active position pos, merged row j with expert e) =
 //   exp_off[e] + (rows of e in earlier blocks) + (rows of e earlier in block),
 // i.e. rows of one expert stay in token order.  No hidden state is copied:
 // row_src[row] names the token whose h row the grouped GEMM gathers, and
 // exec_list / exec_pos list the executed tokens in active order.
+//
+// FUSED (small route grids, bucket_fused_scan): no k_scan launch.  Every
+// bucket block reads all block histograms into LDS and derives the offsets
+// it needs (its own per-expert run starts, the expert row offsets, its
+// executed-token offset) with the same integer sums k_scan makes; block 0
+// also writes the layer's expert offsets, tile list and counters.
+__device__ __forceinline__ void fused_scan(const LayerParams& p, int nb, int* s_cnt, int* s_x,
+                                           int* s_seg, int* s_wave, int* s_off, int* s_xoff) {
+  const int E = p.E, tid = threadIdx.x, b_me = blockIdx.x;
+  const int n_c = nb * E;
+  for (int i = tid; i < n_c; i += blockDim.x) s_cnt[i] = p.blk_cnt[i];
+  for (int b = tid; b < nb; b += blockDim.x) s_x[b] = p.blk_xcnt[b];
+  __syncthreads();
+  // thread (segment g, expert e) sums its run of blocks; the segment holding
+  // this block also sums the blocks before it
+  int ep = 1;
+  while (ep < E) ep <<= 1;
+  const int S = blockDim.x / ep, L = (nb + S - 1) / S;
+  const int e = tid % ep, g = tid / ep;
+  const int b0 = g * L, b1 = min(nb, b0 + L);
+  int sum = 0, before = 0;
+  if (e < E)
+    for (int b = b0; b < b1; ++b) {
+      if (b == b_me) before = sum;
+      sum += s_cnt[b * E + e];
+    }
+  s_seg[g * ep + e] = sum;
+  if (e < E && b_me >= b0 && b_me < b1) s_off[e] = before;  // in-segment part
+  __syncthreads();
+  int tot = 0, pre = 0;
+  if (tid < E) {
+    const int gme = L > 0 ? b_me / L : 0;
+    for (int q = 0; q < S; ++q) {
+      const int v = s_seg[q * ep + tid];
+      if (q < gme) pre += v;
+      tot += v;
+    }
+    pre += b_me < nb ? s_off[tid] : 0;
+  }
+  __syncthreads();
+  int total = 0, ttotal = 0;
+  const int off = block_exclusive_scan(tot, s_wave, &total);
+  const int nt_e = (tot + p.bm - 1) / p.bm;
+  const int toff = block_exclusive_scan(nt_e, s_wave, &ttotal);
+  if (tid < E) s_off[tid] = off + pre;
+  // executed-token offset of this block, and the layer's executed total
+  int xrun = 0;
+  for (int c0 = 0; c0 < nb; c0 += blockDim.x) {
+    const int b = c0 + tid;
+    const int v = b < nb ? s_x[b] : 0;
+    int chunk = 0;
+    const int o = block_exclusive_scan(v, s_wave, &chunk);
+    if (b == b_me) *s_xoff = xrun + o;
+    xrun += chunk;
+  }
+  if (b_me == 0) {
+    if (tid < E) {
+      p.exp_off[tid] = off;
+      for (int u = 0; u < nt_e; ++u) p.tiles[toff + u] = make_int4(tid, off + u * p.bm, off + tot, 0);
+    }
+    const int distinct = __syncthreads_count(tid < E && tot > 0);
+    if (tid == 0) {
+      p.exp_off[E] = total;
+      p.counts[kCntRows] = total;
+      p.counts[kCntTiles] = ttotal;
+      p.counts[kCntExec] = xrun;
+      if (p.tr_counters) {
+        p.tr_counters[6] = total;
+        p.tr_counters[7] = distinct;
+      }
+    }
+  }
+}
+
+template <bool FUSED>
 __global__ __launch_bounds__(256) void k_bucket(LayerParams p) {
   static_assert(RB <= 32 && RB * KMAX <= 256, "token masks and one thread per slot");
   __shared__ unsigned s_emask[TRIMMOE_MAX_EXPERTS];  // block tokens holding a row of e
   __shared__ int s_off[TRIMMOE_MAX_EXPERTS];         // the block's first row of e
   __shared__ unsigned s_xmask;                       // block tokens that execute
+  __shared__ int s_xoff;                             // the block's first executed token
   const int n_a = *p.n_active;
   const int base = blockIdx.x * p.rb;
-  if (base >= n_a) return;
-  const int nt = min(p.rb, n_a - base);
   const int k = p.k, E = p.E;
   const int tid = threadIdx.x;
-  for (int e = tid; e < E; e += blockDim.x) {
-    s_emask[e] = 0u;
-    s_off[e] = p.exp_off[e] + p.blk_off[(size_t)blockIdx.x * E + e];
+  if constexpr (FUSED) {
+    __shared__ int s_cnt[kFusedScanEntries];
+    __shared__ int s_x[kFusedScanBlocks];
+    __shared__ int s_seg[256];
+    __shared__ int s_wave[17];
+    const int nb = (n_a + p.rb - 1) / p.rb;
+    if (blockIdx.x > 0 && base >= n_a) return;  // block 0 writes the layer's offsets
+    fused_scan(p, nb, s_cnt, s_x, s_seg, s_wave, s_off, &s_xoff);
+    if (base >= n_a) return;
+    for (int e = tid; e < E; e += blockDim.x) s_emask[e] = 0u;
+  } else {
+    if (base >= n_a) return;
+    for (int e = tid; e < E; e += blockDim.x) {
+      s_emask[e] = 0u;
+      s_off[e] = p.exp_off[e] + p.blk_off[(size_t)blockIdx.x * E + e];
+    }
+    if (tid == 0) s_xoff = p.blk_xoff[blockIdx.x];
   }
+  const int nt = min(p.rb, n_a - base);
   if (tid == 0) s_xmask = 0u;
   __syncthreads();
   // thread (token i, slot j); a token's merged rows are distinct experts
@@ -885,7 +978,7 @@ __global__ __launch_bounds__(256) void k_bucket(LayerParams p) {
     p.row_src[row] = p.active_idx[pos];
   }
   if (tid < nt && ((s_xmask >> tid) & 1u)) {
-    const int xidx = p.blk_xoff[blockIdx.x] + __popc(s_xmask & ((1u << tid) - 1u));
+    const int xidx = s_xoff + __popc(s_xmask & ((1u << tid) - 1u));
     p.exec_list[xidx] = p.active_idx[base + tid];
     p.exec_pos[xidx] = base + tid;
   }
@@ -1075,13 +1168,24 @@ hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st) {
   return hipGetLastError();
 }
 
+// the bucket blocks derive the scan themselves when every block histogram
+// fits in their LDS (one launch fewer per layer)
+static bool bucket_fused_scan(const LayerParams& p) {
+  const int nb = cdiv(p.T, p.rb);
+  return nb <= kFusedScanBlocks && (size_t)nb * p.E <= (size_t)kFusedScanEntries;
+}
+
 hipError_t launch_scan(const LayerParams& p, hipStream_t st) {
+  if (bucket_fused_scan(p)) return hipSuccess;
   hipLaunchKernelGGL(k_scan, dim3(1), dim3(1024), 0, st, p);
   return hipGetLastError();
 }
 
 hipError_t launch_bucket(const LayerParams& p, hipStream_t st) {
-  hipLaunchKernelGGL(k_bucket, dim3(cdiv(p.T, p.rb)), dim3(256), 0, st, p);
+  if (bucket_fused_scan(p))
+    hipLaunchKernelGGL(k_bucket<true>, dim3(cdiv(p.T, p.rb)), dim3(256), 0, st, p);
+  else
+    hipLaunchKernelGGL(k_bucket<false>, dim3(cdiv(p.T, p.rb)), dim3(256), 0, st, p);
   return hipGetLastError();
 }
 
