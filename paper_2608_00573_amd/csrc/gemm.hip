@@ -28,8 +28,6 @@
 // fp32 path: plain FMA kernels for fp32 models.
 #include <math.h>
 
-#include <type_traits>
-
 #include "common.h"
 
 namespace trimmoe {
@@ -231,24 +229,21 @@ struct FragAddr {
 template <class T>
 using Acc = f32x16_t[T::TM][T::TN * T::NB];
 
-// acc[i][j] += A_i B_j^T for the k-step held in f; FRESH: acc = A_i B_j^T
-// (the tile's first k-step: a zero C operand, so no register is cleared)
-template <class T, bool FRESH = false>
+// acc[i][j] += A_i B_j^T for the k-step held in f
+template <class T>
 __device__ __forceinline__ void mma_step(const Frags<T>& f, Acc<T>& acc) {
 #pragma unroll
   for (int i = 0; i < T::TM; ++i)
 #pragma unroll
     for (int j = 0; j < T::TN * T::NB; ++j)
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j],
-                                                          FRESH ? f32x16_t{} : acc[i][j], 0, 0, 0);
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
 }
 
 // One slice from stage cur (its k-step-0 fragments already in f0), with the
 // next slice's k-step-0 fragments read from stage nxt under the last
 // k-step's MFMAs.  `issue` starts the DMA of the slice DEPTH ahead; the
-// barrier waits for the DMAs of the next slice only.  FIRST: the slice is
-// the tile's first, whose first k-step starts the accumulators.
-template <class T, bool FIRST, class Issue>
+// barrier waits for the DMAs of the next slice only.
+template <class T, class Issue>
 __device__ __forceinline__ void dma_slice_mma(const FragAddr<T>& fa, uint32_t cur, uint32_t nxt,
                                               Frags<T>& f0, Frags<T>& f1, Acc<T>& acc,
                                               Issue issue) {
@@ -256,7 +251,7 @@ __device__ __forceinline__ void dma_slice_mma(const FragAddr<T>& fa, uint32_t cu
   issue();
   fa.read(f1, cur, 1);
   lgkm_wait<D::NF>(f0);
-  mma_step<T, FIRST>(f0, acc);
+  mma_step<T>(f0, acc);
   fa.read(f0, cur, 2);
   lgkm_wait<D::NF>(f1);
   mma_step<T>(f1, acc);
@@ -325,7 +320,15 @@ __device__ __forceinline__ void dma_gemm_stream(char* lds, int ntiles, int nk, c
   const FragAddr<T> fa(wave / T::GN, wave % T::GN, lane);
   const uint32_t st0 = lds_addr(lds);
   using D = DmaTile<T>;
-  Acc<T> acc;  // started by each tile's first k-step
+  Acc<T> acc;
+  const f32x16_t z = {};
+  auto zero = [&] {
+#pragma unroll
+    for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+      for (int j = 0; j < T::TN * T::NB; ++j) acc[i][j] = z;
+  };
+  zero();
 
   // DMA side: slice dk of tile dj through pointers qp; n1 / n2 describe
   // tiles dj+1 / dj+2 and rn1 holds the A rows of dj+1
@@ -373,20 +376,22 @@ __device__ __forceinline__ void dma_gemm_stream(char* lds, int ntiles, int nk, c
   for (int s = 1; s < D::DEPTH; ++s) issue(s);
   slice_barrier<D::NDMA * (D::DEPTH - 1)>(f1);
   fa.read(f0, st0, 0);
-  int sx = 0;  // stage of the slice being computed
-  auto slice = [&](auto first) {
+  const int G = ntiles * nk;
+  int sx = 0, kk = 0;  // stage of the slice being computed, its index in the tile
+  for (int g = 0; g < G; ++g) {
     const int sn = sx + 1 == D::STAGES ? 0 : sx + 1;
-    const int sp = (sx + D::DEPTH) % D::STAGES;  // stage of the slice DEPTH ahead
-    dma_slice_mma<T, decltype(first)::value>(fa, st0 + sx * T::STAGE, st0 + sn * T::STAGE, f0,
-                                             f1, acc, [&] { issue(sp); });
+    const int sp = (sx + D::DEPTH) % D::STAGES;  // stage of slice g + DEPTH
+    dma_slice_mma<T>(fa, st0 + sx * T::STAGE, st0 + sn * T::STAGE, f0, f1, acc,
+                     [&] { issue(sp); });
+    if (++kk == nk) {
+      src.epilogue(c0, acc);
+      zero();
+      c0 = c1;
+      c1 = c2;
+      ++jc;
+      kk = 0;
+    }
     sx = sn;
-  };
-  for (; jc < ntiles; ++jc) {
-    slice(std::true_type{});
-    for (int kk = 1; kk < nk; ++kk) slice(std::false_type{});
-    src.epilogue(c0, acc);
-    c0 = c1;
-    c1 = c2;
   }
 }
 
@@ -968,43 +973,43 @@ struct ExitSrc {
     const int b_valid = min(T::BN, n_x - j0);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wm = wave / T::GN, wn = wave % T::GN;
-    // partials in base 2 (y = z log2 e): per token column the largest y and
-    // the sum of 2^(y - max y) = exp(z - max z).  A pass over the logits z
-    // for the largest, then one FMA (z log2 e - max y) and one v_exp_f32 per
-    // logit; rounding is monotonic, so max y = (max z) log2 e exactly
+    // partials in base 2: y = z * log2(e), so exp(z - max z) = exp2(y - max y)
+    // is one FMA and one v_exp_f32 per logit; the pair stored is (max y, sum)
     const float ninf = -__builtin_inff();
     const float kLog2e = 1.4426950408889634f;
     const bool full = a_valid == T::BM && !a.bias;
 #pragma unroll
     for (int jj = 0; jj < T::TN; ++jj) {
-      float mz = ninf;
+      float m = ninf;
       if (full) {
 #pragma unroll
         for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) mz = fmaxf(mz, acc[i][jj][r]);
+          for (int r = 0; r < 16; ++r) {
+            const float y = acc[i][jj][r] * kLog2e;
+            acc[i][jj][r] = y;
+            m = fmaxf(m, y);
+          }
       } else {
 #pragma unroll
         for (int i = 0; i < T::TM; ++i)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int row = acc_row<T>(wm, i, r, lane);
-            float z = acc[i][jj][r];
-            if (a.bias) z += a.bias[v0 + min(row, a_valid - 1)];
-            z = row < a_valid ? z : ninf;
-            acc[i][jj][r] = z;
-            mz = fmaxf(mz, z);
+            float y = acc[i][jj][r];
+            if (a.bias) y += a.bias[v0 + min(row, a_valid - 1)];
+            y = row < a_valid ? y * kLog2e : ninf;
+            acc[i][jj][r] = y;
+            m = fmaxf(m, y);
           }
       }
-      mz = fmaxf(mz, __shfl_xor(mz, 32));
-      const float m = mz * kLog2e;
+      m = fmaxf(m, __shfl_xor(m, 32));
       float sum = 0.f;
-      if (mz != ninf) {
+      if (m != ninf) {
 #pragma unroll
         for (int i = 0; i < T::TM; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            sum += __builtin_amdgcn_exp2f(fmaf(acc[i][jj][r], kLog2e, -m));
+          for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(acc[i][jj][r] - m);
       }
       sum += __shfl_xor(sum, 32);
       if (lane < 32) s_part[wm][acc_col<T>(wn, jj, lane)] = make_float2(m, sum);
