@@ -7,7 +7,12 @@ exit gate, compaction), inputs already resident in HBM.  For the decode
 workload each step takes a fresh batch (32 tokens, its own seed).  Prints
 one JSON line:
 
-* value: tokens/s = tokens per batch * steps / timed seconds;
+* value: tokens/s = tokens per batch / median step time.  Every timed step
+  is bracketed by its own HIP events on the library's stream; a 512 MiB
+  buffer is written between steps, outside those events, so that no step
+  finds the previous one's operands in the 256 MB Infinity Cache.  The
+  line also gives the p10-p90 spread of the step times, their mean, the
+  device's CU count and peak engine clock;
 * roofline: the dominant kernel class (by measured time) against its own
   roofline (MFMA or HBM, whichever its algorithmic FLOPs and bytes make
   binding), from HIP events recorded around each kernel class on the
@@ -52,7 +57,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=None,
                     help="timed steps (default 20; the decode workload: its step count, 128)")
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="switch_base_8e")
+    ap.add_argument("--workload", default="mixtral_8x7b_prefill",
+                    help="workload (default: the Mixtral-8x7B-shaped prefill batch, the "
+                         "largest that fits one GPU)")
+    ap.add_argument("--flush-mib", type=int, default=512,
+                    help="MiB written between timed steps to evict the Infinity Cache "
+                         "(0 = off)")
     ap.add_argument("--horizon", type=int, default=None,
                     help="look-ahead horizon H of the decision (default: the workload's, 1)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -87,6 +97,74 @@ def calibrate_copy():
     torch.cuda.synchronize()
     print(json.dumps({"calibrate_copy_bytes_read": n, "calibrate_copy_bytes_written": n,
                       "dispatches": 5}), flush=True)
+
+
+def device_info():
+    """CU count and peak engine clock of device 0 (hipDeviceGetAttribute)."""
+    import ctypes as C
+    hip = C.CDLL("libamdhip64.so")
+    out = {}
+    for key, attr in (("compute_units", 63), ("peak_engine_clock_mhz", 5)):
+        v = C.c_int(0)
+        rc = hip.hipDeviceGetAttribute(C.byref(v), attr, 0)
+        out[key] = v.value if rc == 0 else None
+    if out["peak_engine_clock_mhz"]:
+        out["peak_engine_clock_mhz"] //= 1000   # the attribute is in kHz
+    return out
+
+
+def host_cpu():
+    """Model name and logical CPU counts of the host."""
+    model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"model": model, "nproc": os.cpu_count(),
+            "usable": len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else None}
+
+
+def class_kernel(cls, cfg):
+    """The library kernel(s) of a kernel class at the workload's batch size,
+    by the library's tile selection: grouped GEMMs with at least 1024 rows
+    per expert on average and the shared expert from 2048 tokens run the
+    256 x 256 large-group core, the exit head of models with d >= 2048 from
+    1024 tokens too; everything else the 8-wavefront streaming core."""
+    T, k, E, d = cfg["n_tokens"], cfg["top_k"], cfg["n_experts"], cfg["d_model"]
+    bf16 = cfg["dtype"] == "bf16"
+    swiglu = cfg["act"] == "swiglu"
+    big = bf16 and T * k >= 1024 * E
+    if cls == "up":
+        name = ("k_ffn_big<0>" if swiglu else "k_ffn_big<1>") if big else \
+            ("k_ffn_mma<128x128 dual, up>" if swiglu else "k_ffn_mma<128x256, up>")
+        return name + " (grouped up/gate + activation)"
+    if cls == "down":
+        return ("k_ffn_big<2>" if big else "k_ffn_mma<128x256, down>") + " (grouped down)"
+    if cls == "exit":
+        return ("k_exit_big" if bf16 and T >= 1024 and d >= 2048 else "k_exit_mma") + \
+            " (exit head + softmax partials)"
+    return {"route": "k_route (route, substitution, skip)",
+            "bucket": "k_scan + k_bucket (bucketing)",
+            "shared": "k_ffn_mma / k_ffn_big (shared expert)",
+            "combine": "k_combine (weighted combine)",
+            "gate": "k_exit_reduce + k_compact (exit gate)"}[cls]
+
+
+def log(msg):
+    """Progress on stderr (the JSON line is the only stdout)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def step_stats(ms):
+    """Median, p10, p90 and mean of per-step times (ms)."""
+    import numpy as np
+    a = np.asarray(ms, dtype=np.float64)
+    return dict(median=float(np.median(a)), p10=float(np.percentile(a, 10)),
+                p90=float(np.percentile(a, 90)), mean=float(a.mean()), min=float(a.min()),
+                max=float(a.max()))
 
 
 def algorithmic_work(cfg, counters):
@@ -201,17 +279,25 @@ def cpu_baseline(inp, target_s, max_f64_bytes=24e9):
     layers = f"all {N} layers" if n_l == N else \
         f"layers 0-{n_l - 1} of {N} (fp64 weights of the whole stack exceed " \
         f"{max_f64_bytes / 1e9:.0f} GB; time scaled by {scale:g})"
+    extrap = S < T or n_l < N
+    cpu = host_cpu()
     return dict(value=S / (dt * scale), unit="tokens/s", cores=1, kind="oracle",
+                extrapolated=extrap, host_cpu=cpu["model"], host_nproc=cpu["nproc"],
+                host_cpus_usable=cpu["usable"],
                 sample=f"first {S} of {T} tokens of the {cfg['name']} batch through "
-                       f"{layers}, fp64 numpy oracle, 1 BLAS thread, {dt:.1f} s timed; "
-                       f"tokens are independent so tokens/s scales to the batch")
+                       f"{layers}, fp64 numpy oracle, 1 BLAS thread (1 core of "
+                       f"{cpu['nproc']}: {cpu['model']}), {dt:.1f} s timed; "
+                       + ("extrapolated linearly to the batch and depth (tokens are "
+                          "independent in this step)" if extrap else "the whole workload"))
 
 
-def feedback_loop(abi, cfg, mh, pol0, batches, K, window, ws, eta, kappa, p_floor):
+def feedback_loop(abi, cfg, mh, pol0, batches, K, window, ws, eta, kappa, p_floor,
+                  observe=True):
     """K passes over the batches with the runtime feedback rules applied after
     every `window` passes; the window's observations accumulate on the GPU and
     one host copy of six numbers per window feeds the host update.  Returns
-    (ms, per-window trajectory)."""
+    (ms, per-window trajectory).  observe=False: the same K passes back to
+    back with no observation and no update (the plain loop)."""
     import torch
     dev = batches[0].device
     policy = abi.make_policy(**pol0)
@@ -226,6 +312,9 @@ def feedback_loop(abi, cfg, mh, pol0, batches, K, window, ws, eta, kappa, p_floo
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for i in range(K):
+        if not observe:
+            abi.trimmoe_stack_forward(mh.model, policy, states[i].state, None, ws)
+            continue
         abi.trimmoe_stack_forward(mh.model, policy, states[i].state, ct.trace, ws)
         abi.trimmoe_window_stats(mh.model, policy, states[i].state, ct.trace, stats)
         if (i + 1) % window == 0 or i == K - 1:
@@ -298,6 +387,7 @@ def main():
     K = args.steps if args.steps is not None else (cfg["decode_steps"] if decode else 20)
     W = args.warmup
     t_gen = time.perf_counter()
+    log(f"{cfg['name']}: generating inputs on the GPU")
     inp = make_inputs(cfg, device=dev)
     T, N = cfg["n_tokens"], cfg["n_layers"]
     # one token batch per step for decode (fresh tokens, seeds base + s), else
@@ -308,6 +398,7 @@ def main():
         batches = [inp["h0"].to(dev)]
     torch.cuda.synchronize()
     t_gen = time.perf_counter() - t_gen
+    log(f"inputs ready in {t_gen:.1f} s; {W} warmup + {K} timed steps")
     mh = abi.model_handle(cfg, inp["layers"])
     policy = abi.make_policy(**inp["policy"])
     ws = abi.alloc_workspace(mh.model, T, dev)
@@ -315,23 +406,39 @@ def main():
     states = [abi.StateBuffers(batches[i % nb].clone()) for i in range(K + W)]
     stream = torch.cuda.current_stream()
 
+    # a buffer written between steps (outside the step events) so that no
+    # step starts with the previous step's operands in the Infinity Cache
+    flush = torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev) \
+        if args.flush_mib > 0 else None
+
+    def evict(i):
+        if flush is not None:
+            flush.fill_(i & 0xff)
+
     # warmup, then the timed region (inputs resident, no host sync inside)
     for i in range(W):
+        evict(i)
         abi.trimmoe_stack_forward(mh.model, policy, states[K + i].state, None, ws)
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
     t0 = time.perf_counter()
-    e0.record(stream)
     for i in range(K):
+        evict(i)
+        ev0[i].record(stream)
         abi.trimmoe_stack_forward(mh.model, policy, states[i].state, None, ws)
-    e1.record(stream)
+        ev1[i].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms_total = e0.elapsed_time(e1)
-    ms_step = ms_total / K
+    step_ms = [a.elapsed_time(b) for a, b in zip(ev0, ev1)]
+    sst = step_stats(step_ms)
+    ms_step = sst["median"]
+    ms_total = float(sum(step_ms))
     del states
 
-    # per-kernel-class timing: HIP events on the same stream, same work
+    log(f"timed: median {ms_step:.3f} ms per step; kernel-class pass")
+    # per-kernel-class timing: HIP events on the same stream, same work, the
+    # same eviction between steps
     classes = list(abi.TIMED_CLASSES)
     per = len(classes) + 1
     events = [torch.cuda.Event(enable_timing=True) for _ in range(N * per)]
@@ -340,6 +447,7 @@ def main():
     class_ms = np.zeros((N, per - 1))
     for i in range(K):
         st = abi.StateBuffers(batches[i % nb].clone())
+        evict(i)
         abi.trimmoe_stack_forward_timed(mh.model, policy, st.state, None, ws, events)
         torch.cuda.synchronize()
         for l in range(N):
@@ -347,6 +455,7 @@ def main():
                 class_ms[l, c] += events[l * per + c].elapsed_time(events[l * per + c + 1])
     class_ms /= K
 
+    log("traced pass for the algorithmic work")
     # traced passes (one per distinct batch) for the algorithmic work
     work_steps = []
     for bt in batches:
@@ -386,7 +495,7 @@ def main():
 
     out = {
         "metric": METRIC,
-        "value": T * K / (ms_total * 1e-3),
+        "value": T / (ms_step * 1e-3),
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": K,
@@ -404,14 +513,7 @@ def main():
                    "horizon": cfg["horizon"], "transition_row_entries": cfg["trans_support"],
                    "parallelism": "single-gpu"},
         "roofline": {
-            "kernel": {"route": "k_route (route, substitution, skip)",
-                       "bucket": "k_scan + k_bucket (bucketing)",
-                       "up": "k_ffn_mma / k_ffn_big (grouped up/gate + activation)",
-                       "down": "k_ffn_mma / k_ffn_big (grouped down)",
-                       "shared": "k_ffn_mma / k_ffn_big (shared expert)",
-                       "combine": "k_combine (weighted combine)",
-                       "exit": "k_exit_mma / k_exit_big (exit head + softmax partials)",
-                       "gate": "k_exit_reduce + k_compact (exit gate)"}[dom],
+            "kernel": class_kernel(dom, cfg),
             "class": dom,
             "bound": "mfma" if mfma_bound else "hbm",
             "achieved": achieved,
@@ -431,8 +533,15 @@ def main():
         "class_hbm_frac": {c: (byts[c] / (t_class[ci[c]] * 1e-3) / 1e9 / PEAK_HBM_GBS
                                if t_class[ci[c]] > 0 else 0.0) for c in classes},
         "step_algorithmic_gb_per_s": step_bytes / (ms_step * 1e-3) / 1e9,
-        "active_token_layers_per_s": active_layers * K / (ms_total * 1e-3),
+        "active_token_layers_per_s": active_layers / (ms_step * 1e-3),
         "stack_roofline_frac": stack_bound_s / (ms_step * 1e-3),
+        "step_ms": {k: round(v, 4) for k, v in sst.items()},
+        "tokens_per_s_p10_p90": [T / (sst["p90"] * 1e-3), T / (sst["p10"] * 1e-3)],
+        "tokens_per_s_mean": T * K / (ms_total * 1e-3),
+        "timing": f"median of {K} steps, each between its own HIP events; "
+                  + (f"{args.flush_mib} MiB written between steps (outside the events)"
+                     if flush is not None else "no cache eviction between steps"),
+        "device": device_info(),
         "kernel_ms_per_step": {n: float(t_class[i]) for i, n in enumerate(classes)},
         "per_layer": [{k: w[k] for k in ("n_active", "n_exec", "rows", "distinct")}
                       for w in work_steps[0]],
@@ -441,6 +550,8 @@ def main():
     }
     fw = args.feedback_window if args.feedback_window is not None else (16 if decode else 0)
     if fw > 0:
+        ms_plain, _ = feedback_loop(abi, cfg, mh, inp["policy"], batches, K, fw, ws, 0.0, 0.0,
+                                    args.p_floor, observe=False)
         ms_obs, _ = feedback_loop(abi, cfg, mh, inp["policy"], batches, K, fw, ws, 0.0, 0.0,
                                   args.p_floor)
         ms_fb, traj = feedback_loop(abi, cfg, mh, inp["policy"], batches, K, fw, ws, args.eta,
@@ -448,12 +559,14 @@ def main():
         out["feedback"] = {
             "window": fw, "eta": args.eta, "kappa": args.kappa, "p_floor": args.p_floor,
             "tokens_per_s": T * K / (ms_fb * 1e-3), "ms_per_step": ms_fb / K,
-            "observation_cost_frac": ms_obs / ms_total - 1.0,
+            "plain_loop_tokens_per_s": T * K / (ms_plain * 1e-3),
+            "observation_cost_frac": ms_obs / ms_plain - 1.0,
             "p_exit_start": inp["policy"]["p_exit"], "omega_t_start": inp["policy"]["omega_t"],
             "windows": traj}
     if args.offline:
         out["offline"] = offline_stage(abi, cfg, mh, inp, batches[0], ws)
     if not args.no_cpu_baseline:
+        log("cpu baseline (oracle on a sample)")
         inp["h0"] = batches[0]
         out["cpu_baseline"] = cpu_baseline(inp, args.cpu_seconds)
     print(json.dumps(out), flush=True)

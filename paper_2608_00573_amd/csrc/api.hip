@@ -102,7 +102,38 @@ int validate_state(const trimmoe_model* m, const trimmoe_state* s) {
   return TRIMMOE_OK;
 }
 
-// Carve the workspace (base == NULL: only measure).  Returns total bytes.
+// Rows of split-K partial slices (splits x rows) the routed down GEMM may
+// use for any batch of at most T tokens.  The split count depends on the
+// row-tile count and is not monotone in it (a smaller batch can need more
+// slice rows than a larger one), so take the largest product over every
+// tile count up to T's, each at its largest batch.
+size_t down_slice_rows_max(const trimmoe_model* m, int T) {
+  const int E = m->n_experts, k = m->top_k;
+  const long long R = (long long)T * k;
+  if (m->dtype != TRIMMOE_BF16) return (size_t)R;
+  const int tiles_T = cdiv((int)R, kGemmBM) + E;
+  long long best = R * down_splits(tiles_T, m->d_model, m->d_ff);
+  for (int tiles = E + 1; tiles < tiles_T; ++tiles) {
+    // largest batch whose row count gives this many tiles
+    const long long Tt = std::min<long long>(T, (long long)(tiles - E) * kGemmBM / k);
+    best = std::max(best, Tt * k * down_splits(tiles, m->d_model, m->d_ff));
+  }
+  return (size_t)best;
+}
+
+// Per-(token, vocabulary tile) exit partials for any batch of at most T
+// tokens: decode-sized batches use finer vocabulary tiles, so the largest of
+// them can need more than a slightly larger batch.
+size_t exit_partials_max(const trimmoe_model* m, int T) {
+  const bool bf16 = m->dtype == TRIMMOE_BF16;
+  size_t n = (size_t)T * cdiv(m->vocab_exit, exit_tile_rows(bf16, T));
+  const int Ts = std::min(T, kExitSmallTokens);
+  return std::max(n, (size_t)Ts * cdiv(m->vocab_exit, exit_tile_rows(bf16, Ts)));
+}
+
+// Carve the workspace (base == NULL: only measure).  Returns total bytes,
+// which never decrease as T grows: a workspace carved for T tokens serves
+// every smaller batch.
 size_t carve(const trimmoe_model* m, int T, char* base, LayerParams* p) {
   const bool bf16 = m->dtype == TRIMMOE_BF16;
   const int E = m->n_experts, k = m->top_k, d = m->d_model, F = m->d_ff, Fs = m->d_ff_shared;
@@ -137,13 +168,13 @@ size_t carve(const trimmoe_model* m, int T, char* base, LayerParams* p) {
   P.row_src = (int32_t*)take(R * 4);
   P.act_buf = take(R * F * es);
   const int splits = bf16 ? down_splits(max_tiles, d, F) : 1;
-  P.y_buf = (float*)take((size_t)splits * R * d * 4);
+  P.y_buf = (float*)take(down_slice_rows_max(m, Tm) * d * 4);
   P.y_split_stride = R * d;
   P.down_splits = splits;
   P.act_s = Fs ? take((size_t)Tm * Fs * es) : nullptr;
   P.y_s = Fs ? (float*)take((size_t)Tm * d * 4) : nullptr;
   P.hx = take((size_t)Tm * d * es);
-  P.partials = (float2*)take((size_t)Tm * n_vtiles * 8);
+  P.partials = (float2*)take(exit_partials_max(m, Tm) * 8);
   P.n_vtiles = n_vtiles;
   P.max_tiles = max_tiles;
   return off;
@@ -336,12 +367,9 @@ int trimmoe_workspace_size(const trimmoe_model* m, int32_t max_tokens, size_t* b
   int rc = validate_model(m);
   if (rc) return rc;
   if (max_tokens < 0) return TRIMMOE_ERR_SHAPE;
-  // enough for every token count up to max_tokens: the carve grows with T
-  // except where small batches switch to finer exit-head vocabulary tiles
-  size_t bytes = carve(m, max_tokens, nullptr, nullptr);
-  if (max_tokens > kExitSmallTokens)
-    bytes = std::max(bytes, carve(m, kExitSmallTokens, nullptr, nullptr));
-  *bytes_out = bytes;
+  // the carve never shrinks as the token count grows, so this covers every
+  // batch of at most max_tokens tokens
+  *bytes_out = carve(m, max_tokens, nullptr, nullptr);
   return TRIMMOE_OK;
 }
 

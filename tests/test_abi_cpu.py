@@ -8,6 +8,7 @@ import ctypes as C
 import os
 import re
 
+import numpy as np
 import pytest
 import torch
 
@@ -72,6 +73,60 @@ def test_workspace_size_covers_every_smaller_batch(dtype):
     mh = _handle(dtype=dtype)
     sizes = [abi.trimmoe_workspace_size(mh.model, t) for t in range(1, 200)]
     assert all(x <= y for x, y in zip(sizes, sizes[1:]))
+
+
+# the full per-layer dimensions of the Switch-, Qwen1.5-MoE- and
+# Mixtral-shaped workloads (only the dimensions matter to the sizing)
+FULL_DIMS = {
+    "switch_base_8e": dict(n_layers=6, d_model=768, n_experts=8, top_k=1, d_ff=3072,
+                           d_ff_shared=0, vocab_exit=32128, act="relu", normalize_topk=0),
+    "qwen_moe_a2_7b": dict(n_layers=24, d_model=2048, n_experts=60, top_k=4, d_ff=1408,
+                           d_ff_shared=5632, vocab_exit=151936, act="swiglu",
+                           normalize_topk=0),
+    "mixtral_8x7b": dict(n_layers=32, d_model=4096, n_experts=8, top_k=2, d_ff=14336,
+                         d_ff_shared=0, vocab_exit=32000, act="swiglu", normalize_topk=1),
+}
+
+
+def _accepts(L, mh, pol, T, bytes_):
+    """Whether a stack call on T tokens accepts a workspace of bytes_ bytes.
+    The call stops before any HIP work: after the workspace check it rejects
+    the wrong event count (TRIMMOE_ERR_SHAPE); a workspace that is too small
+    gives TRIMMOE_ERR_WORKSPACE first.  No pointer is dereferenced."""
+    st = abi.State(T, 256, 256, 256, 256, 256, 256)
+    ev = (C.c_void_p * 1)(C.c_void_p(256))
+    rc = L.trimmoe_stack_forward_timed(C.byref(mh.model), C.byref(pol), C.byref(st), None,
+                                       C.c_void_p(256), bytes_, None, ev, 1)
+    assert rc in (-2, -6), rc
+    return rc == -2
+
+
+@pytest.mark.parametrize("name", sorted(FULL_DIMS))
+def test_workspace_for_max_tokens_serves_every_smaller_batch(name):
+    # the down GEMM's K split and the exit head's vocabulary tile both change
+    # with the batch size; a workspace sized for max_tokens must still be
+    # accepted by every batch of at most max_tokens tokens (measured failures
+    # of an earlier sizing: 18048 tokens under a size for 18112, 12032 under
+    # one for 12992, at the Switch dimensions)
+    dims = dict(FULL_DIMS[name], dtype="bf16")
+    mh = abi.model_handle(dims, _fake_layers(dims["n_layers"], dims["n_experts"],
+                                             dims["act"] == "swiglu", dims["d_ff_shared"] > 0))
+    L = abi.lib()
+    pol = abi.make_policy(**POL)
+    sizes = np.array([abi.trimmoe_workspace_size(mh.model, t) for t in range(0, 40001)])
+    assert np.all(np.diff(sizes) >= 0), "workspace size shrinks with more tokens"
+    for tmax in (64, 65, 1600, 1665, 12032, 12992, 18048, 18112, 40000):
+        ws = int(sizes[tmax])
+        for t in sorted({1, 2, 63, 64, 65, 127, 128, 129, tmax // 3, tmax // 2, tmax - 1, tmax}
+                        | set(range(max(1, tmax - 300), tmax + 1, 7))):
+            if 1 <= t <= tmax:
+                assert _accepts(L, mh, pol, t, ws), (tmax, t)
+        assert not _accepts(L, mh, pol, tmax, ws - 1)
+    # every batch up to 40000 tokens under the size for 40000, and each at its own size
+    ws = int(sizes[40000])
+    for t in range(1, 40001, 13):
+        assert _accepts(L, mh, pol, t, ws), t
+        assert _accepts(L, mh, pol, t, int(sizes[t])), t
 
 
 @pytest.mark.parametrize("over,code", [

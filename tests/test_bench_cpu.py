@@ -43,3 +43,25 @@ def test_counter_traffic_blocks(tmp_path, monkeypatch):
     assert bench.counter_traffic("exit", "w") == (123.0, "profiles/w.md", "k_exit_x")
     assert bench.counter_traffic("down", "w") == (None, None, None)
     assert bench.counter_traffic("up", "w") == (None, None, None)
+
+
+def test_step_statistics():
+    st = bench.step_stats([5.0, 1.0, 2.0, 4.0, 3.0])
+    assert st["median"] == 3.0 and st["mean"] == 3.0
+    assert st["min"] == 1.0 and st["max"] == 5.0
+    assert 1.0 <= st["p10"] <= st["median"] <= st["p90"] <= 5.0
+
+
+def test_host_cpu_description():
+    h = bench.host_cpu()
+    assert h["nproc"] == os.cpu_count() and h["nproc"] >= 1
+    assert h["usable"] is None or 1 <= h["usable"] <= h["nproc"]
+
+
+def test_kernel_names_follow_the_tile_selection():
+    from synthgen import workload
+    assert bench.class_kernel("up", workload("mixtral_8x7b_prefill")).startswith("k_ffn_big<0>")
+    assert bench.class_kernel("down", workload("mixtral_8x7b_prefill")).startswith("k_ffn_big<2>")
+    assert bench.class_kernel("exit", workload("qwen_moe_a2_7b")).startswith("k_exit_big")
+    assert bench.class_kernel("exit", workload("switch_base_8e")).startswith("k_exit_mma")
+    assert bench.class_kernel("up", workload("mixtral_8x7b_decode")).startswith("k_ffn_mma")
