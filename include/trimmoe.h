@@ -31,10 +31,11 @@
  *  - Calls are asynchronous on `stream` (a hipStream_t passed as void*; NULL
  *    is the null stream).  TRIMMOE_OK means "enqueued"; kernel faults
  *    surface at the caller's next synchronisation.
- *  - The library never allocates, frees or synchronises; it keeps no
- *    global state.  The caller owns the workspace (size from
- *    trimmoe_workspace_size).  Calls that share a workspace or a state must
- *    be ordered on one stream.
+ *  - The library never allocates, frees or synchronises.  The caller owns
+ *    the workspace (size from trimmoe_workspace_size); the one exception is
+ *    trimmoe_stack_forward_static, whose workspace is a fixed device array
+ *    per device held by the library.  Calls that share a workspace or a
+ *    state must be ordered on one stream.
  */
 #ifndef TRIMMOE_H
 #define TRIMMOE_H
@@ -46,7 +47,7 @@
 extern "C" {
 #endif
 
-#define TRIMMOE_ABI_VERSION 3
+#define TRIMMOE_ABI_VERSION 4
 
 /* status codes */
 #define TRIMMOE_OK 0
@@ -244,6 +245,30 @@ int trimmoe_stack_forward(const trimmoe_model* m, const trimmoe_policy* p,
                           trimmoe_state* s, trimmoe_trace* trace,
                           void* workspace, size_t workspace_bytes,
                           void* stream);
+
+/*
+ * trimmoe_stack_forward without a caller workspace and without any
+ * allocation, for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * The caller still passes the model, policy, state and optional trace.
+ *
+ * The workspace is a library-owned device array of
+ * TRIMMOE_STATIC_SCRATCH_BYTES bytes, one per device, created when the
+ * library's code object is loaded on that device and held until the process
+ * ends; its address is looked up (hipGetSymbolAddress) at the first call on
+ * each device.  A batch whose workspace (trimmoe_workspace_size of n_tokens)
+ * exceeds that size is rejected with TRIMMOE_ERR_WORKSPACE before anything
+ * is enqueued; other errors as trimmoe_stack_forward, plus TRIMMOE_ERR_HIP
+ * if the array cannot be located.  No memory is allocated or freed (no
+ * hipMalloc, no allocating library routine); nothing needs clearing between
+ * calls (the array keeps the last call's contents, which no call reads).
+ * All calls on one device share its array: calls that may overlap on one
+ * device (different streams, or different host threads without ordering)
+ * race and must be serialised by the caller.
+ */
+#define TRIMMOE_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+int trimmoe_stack_forward_static(const trimmoe_model* m, const trimmoe_policy* p,
+                                 trimmoe_state* s, trimmoe_trace* trace, void* stream);
 
 /*
  * Kernel classes of one layer, in launch order, as timed by

@@ -18,7 +18,8 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libtrimmoe.so")
 
-ABI_VERSION = 3   # TRIMMOE_ABI_VERSION this binding is written for
+ABI_VERSION = 4   # TRIMMOE_ABI_VERSION this binding is written for
+STATIC_SCRATCH_BYTES = 64 << 20  # TRIMMOE_STATIC_SCRATCH_BYTES
 N_COUNTERS = 16   # per-layer trace counters (row stride of trimmoe_trace.counters)
 TRIMMOE_OK = 0
 STATUS = {0: "OK", -1: "ERR_NULL", -2: "ERR_SHAPE", -3: "ERR_DTYPE", -4: "ERR_POLICY",
@@ -68,7 +69,8 @@ class Trace(C.Structure):
 
 EXPORTS = ["trimmoe_abi_version", "trimmoe_status_str", "trimmoe_workspace_size",
            "trimmoe_state_reset", "trimmoe_layer_step", "trimmoe_stack_forward",
-           "trimmoe_stack_forward_timed", "trimmoe_window_stats", "trimmoe_feedback_update",
+           "trimmoe_stack_forward_timed", "trimmoe_stack_forward_static",
+           "trimmoe_window_stats", "trimmoe_feedback_update",
            "trimmoe_calib_exit_layers", "trimmoe_calib_stats", "trimmoe_calib_transitions",
            "trimmoe_place_replicas", "trimmoe_head_argmax_workspace_size",
            "trimmoe_head_argmax", "trimmoe_consistency_labels",
@@ -107,6 +109,10 @@ def lib():
                                                   C.POINTER(State), C.POINTER(Trace),
                                                   C.c_void_p, C.c_size_t, C.c_void_p,
                                                   C.POINTER(C.c_void_p), C.c_int32]
+        L.trimmoe_stack_forward_static.restype = C.c_int
+        L.trimmoe_stack_forward_static.argtypes = [C.POINTER(Model), C.POINTER(Policy),
+                                                   C.POINTER(State), C.POINTER(Trace),
+                                                   C.c_void_p]
         L.trimmoe_window_stats.restype = C.c_int
         L.trimmoe_window_stats.argtypes = [C.POINTER(Model), C.POINTER(Policy),
                                            C.POINTER(State), C.POINTER(Trace), C.c_void_p,
@@ -199,6 +205,16 @@ def trimmoe_stack_forward(model: Model, policy: Policy, state: State, trace,
            lib().trimmoe_stack_forward(C.byref(model), C.byref(policy), C.byref(state), tr,
                                        _ptr(workspace), workspace.numel(),
                                        _stream_handle(stream)))
+
+
+def trimmoe_stack_forward_static(model: Model, policy: Policy, state: State, trace,
+                                 stream=None):
+    """trimmoe_stack_forward on the library's per-device scratch array: no
+    workspace argument, nothing allocated."""
+    tr = C.byref(trace) if trace is not None else None
+    _check("trimmoe_stack_forward_static",
+           lib().trimmoe_stack_forward_static(C.byref(model), C.byref(policy), C.byref(state),
+                                              tr, _stream_handle(stream)))
 
 
 def trimmoe_stack_forward_timed(model: Model, policy: Policy, state: State, trace,

@@ -13,10 +13,18 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "common.h"
 
 using namespace trimmoe;
+
+// Workspace of trimmoe_stack_forward_static: a file-scope device array, one
+// copy per device (each device that loads the library holds it until the
+// process ends).  In host code its name is only a stand-in for the symbol:
+// the device address comes from hipGetSymbolAddress (static_scratch below)
+// and is what kernels and copies receive.
+static __device__ __align__(256) char scratch[TRIMMOE_STATIC_SCRATCH_BYTES];
 
 namespace {
 
@@ -408,6 +416,46 @@ int trimmoe_stack_forward_timed(const trimmoe_model* m, const trimmoe_policy* p,
                                 int32_t n_events) {
   if (!events) return TRIMMOE_ERR_NULL;
   return stack(m, p, s, trace, workspace, workspace_bytes, stream, events, n_events);
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];  // device address of `scratch` per device, once looked up
+
+// The current device's copy of `scratch`: its address is looked up once per
+// device, with that device current, and kept.
+int static_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TRIMMOE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+      return TRIMMOE_ERR_HIP;
+    g_scratch[dev] = ptr;
+  }
+  *out = g_scratch[dev];
+  return TRIMMOE_OK;
+}
+}  // namespace
+
+int trimmoe_stack_forward_static(const trimmoe_model* m, const trimmoe_policy* p,
+                                 trimmoe_state* s, trimmoe_trace* trace, void* stream) {
+  // every argument check first (no HIP call before them), then the size limit
+  int rc = validate_model(m);
+  if (rc) return rc;
+  if ((rc = validate_policy(p))) return rc;
+  if ((rc = validate_lookahead(m, p, 0, m->n_layers - 1))) return rc;
+  if ((rc = validate_state(m, s))) return rc;
+  const size_t need = carve(m, s->n_tokens, nullptr, nullptr);
+  if (need > TRIMMOE_STATIC_SCRATCH_BYTES) return TRIMMOE_ERR_WORKSPACE;
+  if (s->n_tokens == 0) return TRIMMOE_OK;
+  void* ws = nullptr;
+  if ((rc = static_scratch(&ws))) return rc;
+  // the carve needs no cleared memory: every kernel writes what it reads
+  // later in the same layer before reading it
+  return stack(m, p, s, trace, ws, TRIMMOE_STATIC_SCRATCH_BYTES, stream, nullptr, 0);
 }
 
 int trimmoe_window_stats(const trimmoe_model* m, const trimmoe_policy* p, const trimmoe_state* s,

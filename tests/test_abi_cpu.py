@@ -282,3 +282,24 @@ def test_look_ahead_needs_the_transitions_a_decision_reads():
     pol3 = abi.make_policy(**POL, horizon=3)
     assert L.trimmoe_layer_step(C.byref(mh.model), 0, C.byref(pol3), C.byref(st), None, None, 0,
                                 None) == -1
+
+
+def test_static_entry_validates_before_any_device_call():
+    # the allocation-free entry point checks its arguments and its array's
+    # size limit before touching the device: a batch larger than the array
+    # is rejected with TRIMMOE_ERR_WORKSPACE, bad arguments as usual
+    dims = dict(FULL_DIMS["switch_base_8e"], dtype="bf16")
+    mh = abi.model_handle(dims, _fake_layers(dims["n_layers"], dims["n_experts"], False))
+    L = abi.lib()
+    pol = abi.make_policy(**POL)
+    T = 8192
+    assert abi.trimmoe_workspace_size(mh.model, T) > abi.STATIC_SCRATCH_BYTES
+    st = abi.State(T, 256, 256, 256, 256, 256, 256)
+    assert L.trimmoe_stack_forward_static(C.byref(mh.model), C.byref(pol), C.byref(st), None,
+                                          None) == -6
+    bad = abi.make_policy(**dict(POL, omega_t=2.0))
+    assert L.trimmoe_stack_forward_static(C.byref(mh.model), C.byref(bad), C.byref(st), None,
+                                          None) == -4
+    st.xi = None
+    assert L.trimmoe_stack_forward_static(C.byref(mh.model), C.byref(pol), C.byref(st), None,
+                                          None) == -1
