@@ -758,6 +758,129 @@ __device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Ac
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// ---------------------------------------------- large-group epilogues --
+// Activation tile (MODE 0 SwiGLU: silu(g) u with g, u from accumulators j + 2
+// and j; MODE 1 ReLU) as bf16 through LDS, so that it leaves as 16-byte row
+// chunks instead of one 2-byte store per element.  A lane holds one column
+// of 16 rows per accumulator; lanes c and c ^ 1 swap one value of each row
+// pair (rows r, r + 1) so that each holds two adjacent columns of one row,
+// which v_cvt_pk_bf16_f32 packs (round to nearest even) into one dword of
+// the LDS image [256 rows][NT columns].  Every wave's LDS accesses of the
+// tile's last slice are done when this runs (the main loop ends on a
+// barrier), and it ends on a barrier before the next tile's operands go to
+// LDS.  silu uses the hardware exp2 and reciprocal (about 1 ulp in fp32;
+// the result is rounded to bf16).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float swap_pair(float v) {
+  // lane l reads lane l ^ 1 (quad_perm [1, 0, 3, 2])
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xb1, 0xf,
+                                                             0xf, false));
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  return g * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-g * 1.4426950408889634f)) * u;
+}
+
+template <int MODE>
+__device__ __forceinline__ void big_store_act(char* lds, const FfnArgs& a, Acc44& acc, int m0,
+                                              int n0, int a_valid, int b_valid, int wm, int wn,
+                                              int lane) {
+  constexpr bool DUAL = MODE == 0;
+  constexpr int NT = DUAL ? 128 : 256;      // output columns of the tile
+  constexpr int RS = NT * 2 + (DUAL ? 16 : 0);  // LDS bytes per row (padded when it fits)
+  static_assert(256 * RS <= 2 * big::STAGE, "activation tile fits the two stages");
+  const int c = lane & 31, hi = lane >> 5;
+  const bool odd = c & 1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < (DUAL ? 2 : 4); ++j) {
+      const int col = (DUAL ? wn * 64 : wn * 128) + 32 * j + (c & ~1);
+#pragma unroll
+      for (int s = 0; s < 8; ++s) {
+        const int r = 2 * s;
+        float v0, v1;
+        if constexpr (DUAL) {
+          v0 = silu_mul(acc[i][j + 2][r], acc[i][j][r]);
+          v1 = silu_mul(acc[i][j + 2][r + 1], acc[i][j][r + 1]);
+        } else {
+          v0 = fmaxf(acc[i][j][r], 0.f);
+          v1 = fmaxf(acc[i][j][r + 1], 0.f);
+        }
+        const float got = swap_pair(odd ? v0 : v1);
+        const uint32_t w = odd ? pack_bf16x2(got, v1) : pack_bf16x2(v0, got);
+        const int row = wm * 128 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3) + (odd ? 1 : 0);
+        *reinterpret_cast<uint32_t*>(lds + row * RS + col * 2) = w;
+      }
+    }
+  __syncthreads();
+  // 16-byte chunks of the valid rows and columns (N is a multiple of 64, so
+  // a chunk is valid or not as a whole)
+  constexpr int CPR = NT / 8;
+  int N = a.N;
+  asm volatile("" : "+s"(N));  // per-tile value: keeps the offsets below inside the tile loop
+  const __amdgpu_buffer_rsrc_t ro = buf_rsrc(static_cast<bf16_t*>(a.out) + (size_t)m0 * N + n0);
+#pragma unroll 4
+  for (int idx = threadIdx.x; idx < 256 * CPR; idx += big::THREADS) {
+    const int row = idx / CPR, ch = idx % CPR;
+    if (row < a_valid && ch * 8 < b_valid) {
+      const u32x4_t v = *reinterpret_cast<const u32x4_t*>(lds + row * RS + ch * 16);
+      __builtin_amdgcn_raw_buffer_store_b128(v, ro, (uint32_t)((row * N + ch * 8) * 2), 0, 0);
+    }
+  }
+  __syncthreads();
+}
+
+// fp32 down partials straight from the accumulators: per store, 32 lanes
+// write 128 contiguous bytes of one row.  Addresses are a per-lane 32-bit
+// offset from the tile's first element plus a wave-uniform one per
+// accumulator row (an SGPR), so nothing per element is kept across tiles;
+// full tiles skip the per-element bounds tests.
+template <bool CHECK>
+__device__ __forceinline__ void big_store_partial_rows(Acc44& acc, __amdgpu_buffer_rsrc_t ro,
+                                                       uint32_t voff, int N, int rl, int cl,
+                                                       int a_valid, int b_valid) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (CHECK && cl + 32 * j >= b_valid) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int dr = 32 * i + 8 * (r >> 2) + (r & 3);
+        if (CHECK && rl + dr >= a_valid) continue;
+        // through a VGPR: stored straight from the accumulator registers, every
+        // element of a 32 x 32 block came out as its first one
+        float v = acc[i][j][r];
+        asm volatile("" : "+v"(v));
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), ro, voff,
+                                              (uint32_t)((dr * N + 32 * j) * 4), 0);
+      }
+    }
+}
+
+__device__ __forceinline__ void big_store_partial(const FfnArgs& a, Acc44& acc, int m0, int n0,
+                                                  int sp, int a_valid, int b_valid, int wm, int wn,
+                                                  int lane) {
+  int N = a.N;
+  asm volatile("" : "+s"(N));  // per-tile value: keeps the offsets below inside the tile loop
+  const int c = lane & 31, hi = lane >> 5;
+  const int rl = wm * 128 + 4 * hi, cl = wn * 128 + c;  // the lane's first row and column
+  const __amdgpu_buffer_rsrc_t ro = buf_rsrc(static_cast<float*>(a.out) + sp * a.split_stride +
+                                             (size_t)m0 * N + n0);
+  const uint32_t voff = (uint32_t)((rl * N + cl) * 4);
+  if (a_valid == big::BM && b_valid == big::BN)
+    big_store_partial_rows<false>(acc, ro, voff, N, rl, cl, a_valid, b_valid);
+  else
+    big_store_partial_rows<true>(acc, ro, voff, N, rl, cl, a_valid, b_valid);
+}
+
 // MODE 0: SwiGLU up and gate (NB operands W0 / W1, 128 output columns per
 // tile), MODE 1: ReLU up, MODE 2: down (fp32 out, K splits)
 template <int MODE>
@@ -801,9 +924,9 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
       m1 = dense_m1;
     } else {
       const int4 tl = a.tiles[mt];
-      e = tl.x;
-      m0 = tl.y;
-      m1 = tl.z;
+      e = __builtin_amdgcn_readfirstlane(tl.x);
+      m0 = __builtin_amdgcn_readfirstlane(tl.y);
+      m1 = __builtin_amdgcn_readfirstlane(tl.z);
     }
     const int n0 = nt * NT;
     const int a_valid = min(big::BM, m1 - m0), b_valid = min(NT, a.N - n0);
@@ -830,29 +953,10 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
     big_tile<DUAL>(lds, q, nk, acc, a_lane, b_lane, w_lane);
-    // epilogue: wavefront rows wm * 128 + .., columns (DUAL) wn * 64 + 32 j
-    // with the gate in accumulator j + 2, else wn * 128 + 32 j
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < (DUAL ? 2 : 4); ++j) {
-        const int col = (DUAL ? wn * 64 : wn * 128) + 32 * j + (lane & 31);
-        if (col >= b_valid) continue;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = wm * 128 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3);
-          if (row >= a_valid) continue;
-          const size_t o = (size_t)(m0 + row) * a.N + n0 + col;
-          if constexpr (MODE == 0) {
-            const float u = acc[i][j][r], g = acc[i][j + 2][r];
-            static_cast<bf16_t*>(a.out)[o] = f2bf(g / (1.f + expf(-g)) * u);
-          } else if constexpr (MODE == 1) {
-            static_cast<bf16_t*>(a.out)[o] = f2bf(fmaxf(acc[i][j][r], 0.f));
-          } else {
-            static_cast<float*>(a.out)[sp * a.split_stride + o] = acc[i][j][r];
-          }
-        }
-      }
+    if constexpr (MODE == 2)
+      big_store_partial(a, acc, m0, n0, sp, a_valid, b_valid, wm, wn, lane);
+    else
+      big_store_act<MODE>(lds, a, acc, m0, n0, a_valid, b_valid, wm, wn, lane);
   }
 }
 
