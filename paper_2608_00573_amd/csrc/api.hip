@@ -173,6 +173,12 @@ size_t carve(const trimmoe_model* m, int T, char* base, LayerParams* p) {
   P.exp_off = (int32_t*)take((size_t)(E + 1) * 4);
   P.counts = (int32_t*)take(kCntSlots * 4);
   P.tiles = (int4*)take((size_t)max_tiles * 16);
+  P.exp_toff = (int32_t*)take((size_t)E * 4);
+  // the large-group core (and its cut down-GEMM tiles) is open to some batch
+  // of at most Tm tokens once Tm k >= kBigRowsPerExpert E
+  const bool big_any = bf16 && R >= (size_t)kBigRowsPerExpert * E;
+  P.sk_flag = (int32_t*)take((size_t)max_tiles * cdiv(d, 256) * 4);
+  P.sk_part = big_any ? (float*)take((size_t)kSkSlots * 256 * 256 * 4) : nullptr;
   P.row_src = (int32_t*)take(R * 4);
   P.act_buf = take(R * F * es);
   const int splits = bf16 ? down_splits(max_tiles, d, F) : 1;
@@ -230,8 +236,14 @@ void fill_params(LayerParams& P, const trimmoe_model* m, int l, const trimmoe_po
   P.trans_b = m->trans_b;
   P.rb = route_block_tokens(T, P.horizon > 1);
   P.bm = expert_tile_rows(m->dtype == TRIMMOE_BF16, T, k, m->n_experts, m->d_model, m->d_ff);
-  // the large-group down GEMM has enough tiles without K splits
-  if (P.bm == kBigBM) P.down_splits = 1;
+  // the large-group down GEMM cuts the tiles of its last round along K
+  // instead of splitting every tile
+  if (P.bm == kBigBM) {
+    P.down_splits = 1;
+  } else {
+    P.sk_flag = nullptr;
+    P.sk_part = nullptr;
+  }
   for (int j = 0; j < kMaxLookahead; ++j) {
     const bool later = j + 1 < P.horizon;  // layer l + j + 1 is looked at
     const trimmoe_layer* Lj = later ? &m->layers[l + j + 1] : nullptr;

@@ -38,6 +38,10 @@ inline int route_blocks_max(int T) {
 constexpr int kGemmBM = 128;
 constexpr int kBigBM = 256;
 constexpr int kBigRowsPerExpert = 1024;
+// the large-group down GEMM cuts the tiles of its last round into at most
+// kSkPieces runs of K slices, with at most kSkSlots 256 x 256 extra partials
+constexpr int kSkPieces = 8;
+constexpr int kSkSlots = 256;
 // the dense shared-expert GEMMs use the large-group core from this many tokens
 constexpr int kBigDenseTokens = 2048;
 // the large-group core addresses its operands with 32-bit byte offsets
@@ -182,6 +186,12 @@ struct LayerParams {
   int32_t* exp_off;    // [E+1]
   int32_t* counts;     // [kCntSlots]
   int4* tiles;         // [max_tiles] (expert, row begin, row end, 0)
+  int32_t* exp_toff;   // [E]   first tile of each expert in `tiles`
+  int32_t* sk_flag;    // [max_tiles * cdiv(d, 256)] large-group down GEMM: per tile,
+                       // 0 (whole) or (first compact partial << 4 | pieces) when
+                       // its K slices were cut; NULL when the layer's down GEMM
+                       // is not on that core
+  float* sk_part;      // [kSkSlots][256][256] compact partials of later pieces
   int32_t* row_src;    // [T*k] token whose h row feeds each permuted row
   void* act_buf;       // [T*k, F]
   float* y_buf;        // [down_splits][T*k, d] partial down-projection slices

@@ -814,6 +814,7 @@ __global__ __launch_bounds__(1024) void k_scan(LayerParams p) {
     s_off[threadIdx.x] = off;
     s_toff[threadIdx.x] = toff;
     p.exp_off[threadIdx.x] = off;
+    p.exp_toff[threadIdx.x] = toff;
     for (int u = 0; u < nt_e; ++u)
       p.tiles[toff + u] = make_int4(threadIdx.x, off + u * p.bm, off + tot, 0);
   }
@@ -912,6 +913,7 @@ __device__ __forceinline__ void fused_scan(const LayerParams& p, int nb, int* s_
   if (b_me == 0) {
     if (tid < E) {
       p.exp_off[tid] = off;
+      p.exp_toff[tid] = toff;
       for (int u = 0; u < nt_e; ++u) p.tiles[toff + u] = make_int4(tid, off + u * p.bm, off + tot, 0);
     }
     const int distinct = __syncthreads_count(tid < E && tot > 0);
@@ -1017,6 +1019,19 @@ __global__ __launch_bounds__(256) void k_combine(LayerParams p) {
         const float4 a0 = yq[0], a1 = yq[1];
         v0.x += a0.x; v0.y += a0.y; v0.z += a0.z; v0.w += a0.w;
         v1.x += a1.x; v1.y += a1.y; v1.z += a1.z; v1.w += a1.w;
+      }
+      // large-group down GEMM: the later K pieces of a cut tile, in order
+      if (p.sk_flag) {
+        const int rt = row - p.exp_off[e];
+        const int mt = p.exp_toff[e] + rt / p.bm;
+        const int word = p.sk_flag[mt * ((p.d + 255) >> 8) + (c >> 8)];
+        for (int q = 1; q < (word & 15); ++q) {
+          const float4* yq = reinterpret_cast<const float4*>(
+              p.sk_part + (size_t)((word >> 4) + q - 1) * 65536 + (rt % p.bm) * 256 + (c & 255));
+          const float4 a0 = yq[0], a1 = yq[1];
+          v0.x += a0.x; v0.y += a0.y; v0.z += a0.z; v0.w += a0.w;
+          v1.x += a1.x; v1.y += a1.y; v1.z += a1.z; v1.w += a1.w;
+        }
       }
       acc[0] += w * v0.x; acc[1] += w * v0.y; acc[2] += w * v0.z; acc[3] += w * v0.w;
       acc[4] += w * v1.x; acc[5] += w * v1.y; acc[6] += w * v1.z; acc[7] += w * v1.w;

@@ -275,9 +275,12 @@ struct TileSched {
   int tb, i0, bx, n_mt, n_nt;
   // false when this block has no tile, else its tile count in ntiles
   __device__ __forceinline__ bool init(int n_mt_, int n_nt_, int n_split, int& ntiles) {
+    return init_total(n_mt_ * n_nt_ * n_split, n_mt_, n_nt_, ntiles);
+  }
+  // the first `total` tile indices only
+  __device__ __forceinline__ bool init_total(int total, int n_mt_, int n_nt_, int& ntiles) {
     n_mt = n_mt_;
     n_nt = n_nt_;
-    const int total = n_mt * n_nt * n_split;
     const int nx = min(kXcd, (int)gridDim.x);  // fewer groups for a small grid
     const int x = blockIdx.x % nx;
     i0 = blockIdx.x / nx;
@@ -290,7 +293,10 @@ struct TileSched {
     return true;
   }
   __device__ __forceinline__ void decode(int j, int& mt, int& nt, int& sp) const {
-    int L = tb + i0 + j * bx;
+    decode_abs(tb + i0 + j * bx, mt, nt, sp);
+  }
+  // tile index L of the whole patch order
+  __device__ __forceinline__ void decode_abs(int L, int& mt, int& nt, int& sp) const {
     const int per = n_mt * n_nt;
     sp = L / per;
     L -= sp * per;
@@ -395,6 +401,26 @@ __device__ __forceinline__ void dma_gemm_stream(char* lds, int ntiles, int nk, c
   }
 }
 
+// ----------------------------------------------- activation helpers --
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float swap_pair(float v) {
+  // lane l reads lane l ^ 1 (quad_perm [1, 0, 3, 2])
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xb1, 0xf,
+                                                             0xf, false));
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// silu(g) u = g u / (1 + e^-g) with the hardware exp2 and reciprocal (about
+// 1 ulp each in fp32; callers round the result to bf16)
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  return g * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-g * 1.4426950408889634f)) * u;
+}
+
 // ------------------------------------------------------ grouped FFN GEMMs --
 // Row tiles come from the device tile list (expert, first row, end row) of
 // the expert-sorted rows, or (dense mode, shared expert) cover the first
@@ -414,6 +440,8 @@ struct FfnArgs {
   size_t split_stride;    // elements between split slices of `out`
   int n_split;            // K splits (down GEMM); 1 otherwise
   int act;                // up: TRIMMOE_ACT_*
+  int* sk_flag;           // large-group down GEMM: per-tile piece words (see SkPlan), or NULL
+  float* sk_part;         // ... and the compact partials of pieces 1.. of cut tiles
 };
 
 template <class T, bool UP>
@@ -472,12 +500,11 @@ struct FfnSrc {
             const float u = acc[i][j][r];
             float v;
             if constexpr (T::NB == 2) {
-              const float g = acc[i][T::TN + j][r];  // gate, same column
-              v = g / (1.f + expf(-g)) * u;          // silu(g) * u
+              v = silu_mul(acc[i][T::TN + j][r], u);  // gate of the same column
             } else {
               v = fmaxf(u, 0.f);
             }
-            static_cast<bf16_t*>(a.out)[o] = f2bf(v);
+            static_cast<__bf16*>(a.out)[o] = (__bf16)v;
           } else {
             static_cast<float*>(a.out)[d.sp * a.split_stride + o] = acc[i][j][r];
           }
@@ -768,25 +795,7 @@ __device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Ac
 // the LDS image [256 rows][NT columns].  Every wave's LDS accesses of the
 // tile's last slice are done when this runs (the main loop ends on a
 // barrier), and it ends on a barrier before the next tile's operands go to
-// LDS.  silu uses the hardware exp2 and reciprocal (about 1 ulp in fp32;
-// the result is rounded to bf16).
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ float swap_pair(float v) {
-  // lane l reads lane l ^ 1 (quad_perm [1, 0, 3, 2])
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xb1, 0xf,
-                                                             0xf, false));
-}
-
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
-  return __builtin_bit_cast(uint32_t, v);
-}
-
-__device__ __forceinline__ float silu_mul(float g, float u) {
-  return g * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(-g * 1.4426950408889634f)) * u;
-}
-
+// LDS.
 template <int MODE>
 __device__ __forceinline__ void big_store_act(char* lds, const FfnArgs& a, Acc44& acc, int m0,
                                               int n0, int a_valid, int b_valid, int wm, int wn,
@@ -865,24 +874,46 @@ __device__ __forceinline__ void big_store_partial_rows(Acc44& acc, __amdgpu_buff
     }
 }
 
-__device__ __forceinline__ void big_store_partial(const FfnArgs& a, Acc44& acc, int m0, int n0,
-                                                  int sp, int a_valid, int b_valid, int wm, int wn,
-                                                  int lane) {
-  int N = a.N;
-  asm volatile("" : "+s"(N));  // per-tile value: keeps the offsets below inside the tile loop
+// tile partials to `out` (the tile's first element; rows ld floats apart)
+__device__ __forceinline__ void big_store_partial(float* out, int ld, Acc44& acc, int a_valid,
+                                                  int b_valid, int wm, int wn, int lane) {
+  asm volatile("" : "+s"(ld));  // per-tile value: keeps the offsets below inside the tile loop
   const int c = lane & 31, hi = lane >> 5;
   const int rl = wm * 128 + 4 * hi, cl = wn * 128 + c;  // the lane's first row and column
-  const __amdgpu_buffer_rsrc_t ro = buf_rsrc(static_cast<float*>(a.out) + sp * a.split_stride +
-                                             (size_t)m0 * N + n0);
-  const uint32_t voff = (uint32_t)((rl * N + cl) * 4);
+  const __amdgpu_buffer_rsrc_t ro = buf_rsrc(out);
+  const uint32_t voff = (uint32_t)((rl * ld + cl) * 4);
   if (a_valid == big::BM && b_valid == big::BN)
-    big_store_partial_rows<false>(acc, ro, voff, N, rl, cl, a_valid, b_valid);
+    big_store_partial_rows<false>(acc, ro, voff, ld, rl, cl, a_valid, b_valid);
   else
-    big_store_partial_rows<true>(acc, ro, voff, N, rl, cl, a_valid, b_valid);
+    big_store_partial_rows<true>(acc, ro, voff, ld, rl, cl, a_valid, b_valid);
 }
 
+// Down GEMM of the large-group core (routed experts): with one tile per CU
+// and round, the persistent grid's last round is often nearly empty (a
+// layer's row tiles x column tiles rarely divide by the CU count).  The
+// tiles of full rounds run whole; each of the nr < P tiles left over is cut
+// into s equal runs of its K slices (s the largest power of two up to
+// kSkPieces with s nr <= P, and at most kSkSlots extra partials), so the
+// last round takes 1/s of a tile's time.  All pieces of that round start
+// together and pieces with the same K run stay in step, as whole tiles do.
+// Piece 0 of a cut tile writes the partial slot of its rows and the tile's
+// word (base slot << 4 | s; 0 for a whole tile); piece q > 0 writes the
+// compact 256 x 256 partial base + q - 1.  The combine adds them in piece
+// order (deterministic).
+struct SkPlan {
+  int dp, nr, s;  // whole tiles, tiles cut, pieces per cut tile
+  __device__ __forceinline__ SkPlan(int nt_all, int P) {
+    nr = nt_all % P;
+    s = 1;
+    while (nr > 0 && s < kSkPieces && 2 * s * nr <= P && nr * (2 * s - 1) <= kSkSlots) s *= 2;
+    if (s == 1) nr = 0;
+    dp = nt_all - nr;
+  }
+};
+
 // MODE 0: SwiGLU up and gate (NB operands W0 / W1, 128 output columns per
-// tile), MODE 1: ReLU up, MODE 2: down (fp32 out, K splits)
+// tile), MODE 1: ReLU up, MODE 2: down (fp32 out; K splits, or stream-K
+// pieces when a.sk_flag is set)
 template <int MODE>
 __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
   constexpr bool DUAL = MODE == 0;
@@ -894,10 +925,7 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
   const int n_nt = (a.N + NT - 1) / NT;
   const int dense_m1 = a.dense_rows ? *a.dense_rows : 0;
   const int n_mt = a.dense_rows ? (dense_m1 + big::BM - 1) / big::BM : *a.n_tiles;
-  TileSched S;
-  int ntiles;
-  if (!S.init(n_mt, n_nt, a.n_split, ntiles)) return;
-  const int nk = (a.K / BK) / a.n_split;
+  const bool sk = MODE == 2 && a.sk_flag != nullptr;
   // per-lane LDS offsets of the fragments, per k-step (16-byte chunk swizzle)
   const int fr = lane & 31, hi = lane >> 5;
   uint32_t a_lane[4], b_lane[4];
@@ -915,9 +943,9 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
   const uint32_t w_lane = r0 * big::RB + (tid & 7) * 16;
   const __amdgpu_buffer_rsrc_t ra = buf_rsrc(a.X);
   Acc44 acc;
-  for (int jt = 0; jt < ntiles; ++jt) {
-    int mt, nt, sp;
-    S.decode(jt, mt, nt, sp);
+  // output tile (mt, nt) over K slices [ka, ka + nkp) into partial slot sp
+  // of its rows, or (cslot >= 0, down GEMM) compact partial cslot
+  auto piece = [&](int mt, int nt, int ka, int nkp, int sp, int cslot) {
     int e = 0, m0, m1;
     if (a.dense_rows) {
       m0 = mt * big::BM;
@@ -930,7 +958,7 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
     }
     const int n0 = nt * NT;
     const int a_valid = min(big::BM, m1 - m0), b_valid = min(NT, a.N - n0);
-    const int k0 = sp * nk * BK;
+    const int k0 = ka * BK;
     BigRows q;
     q.ra = ra;
     q.none = buf_rsrc_empty(a.X);
@@ -952,11 +980,57 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
-    big_tile<DUAL>(lds, q, nk, acc, a_lane, b_lane, w_lane);
-    if constexpr (MODE == 2)
-      big_store_partial(a, acc, m0, n0, sp, a_valid, b_valid, wm, wn, lane);
-    else
+    big_tile<DUAL>(lds, q, nkp, acc, a_lane, b_lane, w_lane);
+    if constexpr (MODE == 2) {
+      if (cslot >= 0)
+        big_store_partial(a.sk_part + (size_t)cslot * big::BM * big::BN, big::BN, acc, a_valid,
+                          b_valid, wm, wn, lane);
+      else
+        big_store_partial(static_cast<float*>(a.out) + sp * a.split_stride + (size_t)m0 * a.N + n0,
+                          a.N, acc, a_valid, b_valid, wm, wn, lane);
+    } else {
       big_store_act<MODE>(lds, a, acc, m0, n0, a_valid, b_valid, wm, wn, lane);
+    }
+  };
+  if (!sk) {
+    TileSched S;
+    int ntiles;
+    if (!S.init(n_mt, n_nt, a.n_split, ntiles)) return;
+    const int nk = (a.K / BK) / a.n_split;
+    for (int jt = 0; jt < ntiles; ++jt) {
+      int mt, nt, sp;
+      S.decode(jt, mt, nt, sp);
+      piece(mt, nt, sp * nk, nk, sp, -1);
+    }
+    return;
+  }
+  const int P = gridDim.x, nk = a.K / BK;
+  const SkPlan plan(n_mt * n_nt, P);
+  // whole tiles, in the usual XCD-range order
+  TileSched S;
+  int ntiles;
+  if (S.init_total(plan.dp, n_mt, n_nt, ntiles)) {
+    for (int jt = 0; jt < ntiles; ++jt) {
+      int mt, nt, sp;
+      S.decode(jt, mt, nt, sp);
+      piece(mt, nt, 0, nk, 0, -1);
+      if (tid == 0) a.sk_flag[mt * n_nt + nt] = 0;
+    }
+  }
+  // the cut tiles of the last round: CU v (numbered XCD by XCD) takes piece
+  // v % s of tile v / s
+  const int nx = min(kXcd, P), x = blockIdx.x % nx;
+  const int v = x * (P / nx) + min(x, P % nx) + (int)blockIdx.x / nx;
+  if (v < plan.nr * plan.s) {
+    const int t = v / plan.s, q = v % plan.s;
+    const int k0 = q * nk / plan.s, k1 = (q + 1) * nk / plan.s;
+    int mt, nt, sp;
+    S.n_mt = n_mt;
+    S.n_nt = n_nt;
+    S.decode_abs(plan.dp + t, mt, nt, sp);
+    const int base = t * (plan.s - 1);
+    piece(mt, nt, k0, k1 - k0, 0, q == 0 ? -1 : base + q - 1);
+    if (q == 0 && tid == 0) a.sk_flag[mt * n_nt + nt] = (base << 4) | plan.s;
   }
 }
 
@@ -1420,7 +1494,8 @@ static void launch_ffn_mma(const FfnArgs& a, int max_mt, int n_cu, hipStream_t s
 template <int MODE>
 static void launch_ffn_big(const FfnArgs& a, int max_mt, int n_cu, hipStream_t st) {
   const int nt = cdiv(a.N, MODE == 0 ? 128 : big::BN);
-  const dim3 grid(min(max_mt * nt * a.n_split, n_cu));
+  // cut tiles of the down GEMM: up to kSkPieces pieces each
+  const dim3 grid(min(max_mt * nt * (a.sk_flag ? kSkPieces : a.n_split), n_cu));
   hipLaunchKernelGGL(k_ffn_big<MODE>, grid, dim3(big::THREADS), 0, st, a);
 }
 
@@ -1442,11 +1517,12 @@ static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared
   if (max_mt <= 0) return hipSuccess;
   if (bf16) {
     const int n_split = (!up && !shared) ? p.down_splits : 1;
-    FfnArgs a{static_cast<const bf16_t*>(X), x_idx, static_cast<const bf16_t*>(w0),
-              static_cast<const bf16_t*>(w1), w_stride, K, N, p.tiles, &p.counts[kCntTiles],
-              dense, out, p.y_split_stride, n_split, act};
     // large groups: the routed tile list was built with kBigBM rows per tile
     const bool big = shared ? big_dense(true, p.T, p.d, p.Fs) : p.bm == kBigBM;
+    FfnArgs a{static_cast<const bf16_t*>(X), x_idx, static_cast<const bf16_t*>(w0),
+              static_cast<const bf16_t*>(w1), w_stride, K, N, p.tiles, &p.counts[kCntTiles],
+              dense, out, p.y_split_stride, n_split, act,
+              (!up && !shared && big) ? p.sk_flag : nullptr, p.sk_part};
     if (big) {
       const int big_mt = shared ? cdiv(p.T, kBigBM) : cdiv(p.T * p.k, kBigBM) + p.E;
       if (up && dual)
