@@ -87,19 +87,25 @@ _INF = float("inf")
 def round_bf16(x):
     """Round fp64 values to the nearest bf16 (ties to even), returned as fp64.
 
-    Operates on the fp64 bit pattern directly (52 -> 7 mantissa bits), so
-    there is no intermediate fp32 rounding.  Valid for finite values whose
-    magnitude is 0 or at least 2^-126 (bf16 normal range), which covers all
-    values of this step; smaller nonzero magnitudes raise.
+    Normal range: on the fp64 bit pattern directly (52 -> 7 mantissa bits),
+    so there is no intermediate fp32 rounding.  Below 2^-126 the bf16 values
+    are the multiples of 2^-133 (subnormals), and a value rounds to the
+    nearest of them, ties to even (so magnitudes up to 2^-134 become zero).
+    Non-finite values raise.
     """
     a = np.ascontiguousarray(np.asarray(x, dtype=np.float64))
-    tiny = (a != 0) & (np.abs(a) < 2.0 ** -126)
-    if np.any(tiny) or not np.all(np.isfinite(a)):
+    if not np.all(np.isfinite(a)):
         raise ValueError("round_bf16: value outside the supported range")
     b = a.view(np.uint64)
     lsb = (b >> np.uint64(45)) & np.uint64(1)
     b = (b + np.uint64((1 << 44) - 1) + lsb) & ~np.uint64((1 << 45) - 1)
-    return b.view(np.float64)
+    out = b.view(np.float64)
+    tiny = np.abs(a) < 2.0 ** -126
+    if np.any(tiny):
+        out = np.array(out, copy=True)
+        # scaling by a power of two is exact; np.round ties to even
+        out[tiny] = np.round(a[tiny] * 2.0 ** 133) * 2.0 ** -133
+    return out
 
 
 def round_f32(x):

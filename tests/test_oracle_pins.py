@@ -41,6 +41,26 @@ def test_round_bf16_ties_to_even_by_hand():
     assert O.round_bf16(np.array([0.0]))[0] == 0.0
 
 
+def test_round_bf16_below_the_normal_range():
+    # bf16 subnormals are the multiples of 2^-133 below 2^-126; IEEE rounding
+    # to nearest, ties to even, reaches them and zero
+    u = 2.0 ** -133
+    cases = [(8 * u, 8 * u), (2.5 * u, 2 * u), (3.5 * u, 4 * u), (-2.5 * u, -2 * u),
+             (0.5 * u, 0.0), (0.5 * u * (1 + 2.0 ** -20), u), (2.0 ** -140, 0.0),
+             (1e-300, 0.0), (127.75 * u, 128 * u), (2.0 ** -126 * (1 - 2.0 ** -30), 2.0 ** -126)]
+    got = O.round_bf16(np.array([c for c, _ in cases]))
+    assert np.array_equal(got, np.array([w for _, w in cases]))
+    assert np.signbit(O.round_bf16(np.array([-0.25 * u]))[0])  # -0
+    # fp32 subnormal inputs against torch's float -> bfloat16 conversion
+    g = torch.Generator().manual_seed(1)
+    bits = torch.randint(1, 1 << 23, (50000,), generator=g, dtype=torch.int32)
+    x = bits.view(torch.float32) * torch.where(torch.rand(50000, generator=g) < 0.5, -1.0, 1.0)
+    want = x.to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(O.round_bf16(x.to(torch.float64).numpy()), want)
+    with pytest.raises(ValueError):
+        O.round_bf16(np.array([np.inf]))
+
+
 # -------------------------------------------------------------- Eq. (3) -----
 def test_q_loss_closed_forms():
     assert O.q_loss(1.0, 1.0) == 0.0            # identical experts
