@@ -104,8 +104,20 @@ FTOL = {"f32": (1e-5, 1e-6), "bf16": (1e-2, 1e-4), "forced": (1e-5, 1e-6)}
 XI_RTOL_FORCED_BF16 = 2e-3
 
 
+def xi_rtol_from_outputs(L, conf_mode, h_ref, h_gpu, slack=5e-4):
+    """Per token, how far the two sides' confidences may lie apart when each
+    is computed from its own rounded layer output: the exact (fp64) relative
+    shift of xi between the oracle's output h_ref and the GPU's output h_gpu
+    through layer L's exit head, plus `slack` for the GPU's fp32 logits and
+    reduction.  So the GPU's xi is checked against the exact confidence of
+    its own output, and the outputs themselves against the state tolerance."""
+    xr = O.exit_confidence(np.asarray(h_ref, np.float64), L["w_exit"], L["b_exit"], conf_mode)
+    xg = O.exit_confidence(np.asarray(h_gpu, np.float64), L["w_exit"], L["b_exit"], conf_mode)
+    return np.abs(xg / xr - 1.0) + slack
+
+
 def compare_stack(cfg, ref_state, ref_traces, gst, gtr, band=BAND, tol=None, layer0=0,
-                  excluded=None, ftol=None, band_exit=None, band_budget=None):
+                  excluded=None, ftol=None, band_exit=None, band_budget=None, xi_rtol=None):
     """Compare a GPU stack (or a suffix of it starting at layer0) with the oracle.
 
     band_budget: when given, the oracle's budget comparisons (D-hat plus a
@@ -113,6 +125,8 @@ def compare_stack(cfg, ref_state, ref_traces, gst, gtr, band=BAND, tol=None, lay
     computes from the same stored Sim values, so to within fp32 rounding)
     get this band and only the importance, logit and cost margins get
     `band`; otherwise every pre-FFN margin gets `band`.
+    xi_rtol: when given (one value per token, single-layer comparisons), the
+    relative tolerance of each token's xi instead of the fixed one.
     Returns a dict of statistics; raises AssertionError on any mismatch.
     """
     tol = TOL[cfg["dtype"]] if tol is None else tol
@@ -161,6 +175,8 @@ def compare_stack(cfg, ref_state, ref_traces, gst, gtr, band=BAND, tol=None, lay
             stats.setdefault("xi_max_rel", []).append(float((dxi / np.abs(rx[ok])).max()))
         xrt = XI_RTOL_FORCED_BF16 if (ftol == "forced" and cfg["dtype"] == "bf16") \
             else max(frel, 1e-4)
+        if xi_rtol is not None:
+            xrt = np.asarray(xi_rtol)[cmp][ok]
         assert np.allclose(gx[ok], rx[ok], rtol=xrt, atol=1e-7), \
             f"layer {l}: xi values, max abs {stats['xi_max_abs'][-1]} max rel {stats['xi_max_rel'][-1]}"
         # inactive tokens untouched in the trace
