@@ -43,9 +43,11 @@ A11 with top-k > 1 every routed slot is resolved on its own under the one
     skip bypasses all slots of the layer.
 A12 normalised per-slot delays t_local, t_remote; the execute cost is
     omega_T * sum of slot delays + omega_D * sum Q / budget.
-A13 a remote slot's only useful substitute is its minimum-Q local expert
-    with Sim >= sim_min (ties to the lower id): any other local substitute
-    has the same delay and spends more budget.
+A13 at H = 1 a remote slot's only useful substitute is its minimum-Q local
+    expert with Sim >= sim_min (ties to the lower id): any other local
+    substitute has the same delay and spends more budget.  Under look-ahead
+    that no longer holds (the cost-to-go depends on which expert runs), see
+    L8.
 A14 ties: lower expert id in top-k; among execute options fewer
     substitutions, then the lower slot bitmask; execute before skip.
 A15 slots that end on the same expert are merged into one row whose weight
@@ -120,21 +122,20 @@ def q_loss(sim: float, phi_scale: float) -> float:
     return min(1.0, phi_scale * (1.0 - sim) / 2.0)
 
 
-def substitutes(sim, local, phi_scale: float, sim_min: float):
-    """Best local substitute c(e) for every expert e of one layer.
+def substitute_candidates(sim, local, phi_scale: float, sim_min: float, n: int):
+    """Local substitute candidates of every expert e of one layer.
 
-    Returns (c, q, margins): c[e] = argmin over local j != e with
-    Sim[e][j] >= sim_min of Q(e, j) (ties to the lower j), -1 if none;
-    q[e] = Q(e, c[e]); margins[e] = the smallest deciding margin of that
-    choice (gap to the second-best candidate, distance of any candidate's
-    Sim to sim_min).
+    The local experts j != e with Sim[e][j] >= sim_min (the feasible set
+    V_{l,e} of Sec. III-A restricted to this device's experts), the n of
+    least Q(e, j) in ascending (Q, j) order (ties to the lower j).  Returns
+    (cands, margins): cands[e] = [(j, Q), ...]; margins[e] = the smallest
+    deciding margin of the list (gaps between consecutive Q among the first
+    n + 1 candidates, and any candidate's distance of Sim to sim_min).
     """
     E = len(local)
-    c = [-1] * E
-    q = [math.nan] * E
-    margins = [_INF] * E
+    cands, margins = [], []
     for e in range(E):
-        cands = []
+        lst = []
         m = _INF
         for j in range(E):
             if j == e or not local[j]:
@@ -142,15 +143,33 @@ def substitutes(sim, local, phi_scale: float, sim_min: float):
             s = float(sim[e][j])
             m = min(m, abs(s - sim_min))
             if s >= sim_min:
-                cands.append((q_loss(s, phi_scale), j))
-        cands.sort()
-        if cands:
-            c[e] = cands[0][1]
-            q[e] = cands[0][0]
-            if len(cands) > 1:
-                m = min(m, cands[1][0] - cands[0][0])
-        margins[e] = m
+                lst.append((q_loss(s, phi_scale), j))
+        lst.sort()
+        for (qa, _), (qb, _) in zip(lst[:n], lst[1:n + 1]):
+            m = min(m, qb - qa)
+        cands.append([(j, q) for q, j in lst[:n]])
+        margins.append(m)
+    return cands, margins
+
+
+def substitutes(sim, local, phi_scale: float, sim_min: float):
+    """Best local substitute c(e) for every expert e of one layer (A13).
+
+    Returns (c, q, margins): c[e] = argmin over local j != e with
+    Sim[e][j] >= sim_min of Q(e, j) (ties to the lower j), -1 if none;
+    q[e] = Q(e, c[e]); margins[e] = the smallest deciding margin of that
+    choice (gap to the second-best candidate, distance of any candidate's
+    Sim to sim_min).
+    """
+    cands, margins = substitute_candidates(sim, local, phi_scale, sim_min, 1)
+    c = [lst[0][0] if lst else -1 for lst in cands]
+    q = [lst[0][1] if lst else math.nan for lst in cands]
     return c, q, margins
+
+
+def as_candidates(c, q):
+    """Candidate lists holding each expert's best substitute only."""
+    return [[(int(ce), float(qe))] if ce >= 0 else [] for ce, qe in zip(c, q)]
 
 
 # ----------------------------------------------------------------------------
@@ -178,58 +197,69 @@ def route(z, k: int, normalize: bool):
 # ----------------------------------------------------------------------------
 # Algorithm 2 for one token at one layer
 # ----------------------------------------------------------------------------
-def step_options(S, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol,
+def step_options(S, I, local, cands, d_hat, budget, theta, slope, pol,
                  m_logit, m_budget):
     """The feasible actions of one token at one layer and their per-step costs.
 
-    Eq. (31) execute costs over the substitution subsets A that Eq. (34)'s
-    budget filter admits, Eq. (35) transmission necessity, the importance
-    admission of Sec. V-C and the Eq. (32) skip cost (readings A8-A18).
+    Eq. (31) execute costs over every way of serving the slots that Eq.
+    (34)'s budget filter admits: each remote slot with substitute candidates
+    (cands[e], see substitute_candidates) runs its target or one of them,
+    local slots run their target (reading A13); Eq. (35) transmission
+    necessity, the importance admission of Sec. V-C and the Eq. (32) skip
+    cost (readings A8-A18).  Options are numbered in mixed radix over the
+    remote slots with candidates, the highest-ranked one the lowest digit
+    (digit 0: the target, d: its d-th candidate); with one candidate per
+    slot the number is the bitmask of the substituted slots.
     Returns (execs, skip, gamma_pos, lam, kinds0): execs is a list of
-    (f, n_sub, mask, charge, x) with x the expert each slot would run (its
-    target, or the substitute on the bits of mask); skip is (f, charge, x)
-    with x the routed targets, or None.  Deciding margins are appended to
-    m_logit (importance against theta) and m_budget (budget comparisons).
+    (f, n_sub, mask, option, charge, x) with x the expert each slot would run
+    and mask the substituted slots; skip is (f, charge, x) with x the routed
+    targets, or None.  Deciding margins are appended to m_logit (importance
+    against theta) and m_budget (budget comparisons).
     """
     wt = pol["omega_t"]
     wd = 1.0 - wt
     t_loc, t_rem = pol["t_local"], pol["t_remote"]
-    kinds0, qs = [], []
+    kinds0 = []
     n_local = n_remote = 0
     rsub = []  # ranks of remote slots that have a local substitute
     for r, e in enumerate(S):
         if local[e]:
             kinds0.append(KIND_LOCAL)
             n_local += 1
-            qs.append(0.0)
         else:
             kinds0.append(KIND_REMOTE)
             n_remote += 1
-            qs.append(sub_q[e] if sub_c[e] >= 0 else math.nan)
-            if sub_c[e] >= 0:
+            if cands[e]:
                 rsub.append(r)
+    radix = [1 + len(cands[S[r]]) for r in rsub]
 
     def quality(charge):
         return wd * charge / budget if budget > 0 else 0.0
 
     execs = []
-    for sel in range(1 << len(rsub)):
+    n_opt = math.prod(radix)
+    for o in range(n_opt):
         mask = 0
         sq = 0.0
-        for i, r in enumerate(rsub):
-            if sel >> i & 1:
+        x = list(S)
+        rest = o
+        for r, rad in zip(rsub, radix):
+            digit = rest % rad
+            rest //= rad
+            if digit:
+                j, q = cands[S[r]][digit - 1]
                 mask |= 1 << r
-                sq += qs[r]
+                sq += q
+                x[r] = j
         n_sub = bin(mask).count("1")
         if mask:
             m_budget.append(abs(budget - d_hat - sq))
         if d_hat + sq <= budget:
             f = wt * ((n_local + n_sub) * t_loc + (n_remote - n_sub) * t_rem) + quality(sq)
-            x = [sub_c[e] if mask >> r & 1 else e for r, e in enumerate(S)]
-            execs.append((f, n_sub, mask, sq, x))
+            execs.append((f, n_sub, mask, o, sq, x))
 
     # Eq. (35): Gamma > 0 iff no feasible assignment leaves no remote slot
-    gamma_pos = not any(n_sub == n_remote for (_, n_sub, _, _, _) in execs)
+    gamma_pos = not any(e[1] == n_remote for e in execs)
     lam = min(1.0, slope * I)  # Eq. (5), reading A8
     skip = None
     if gamma_pos:
@@ -240,25 +270,28 @@ def step_options(S, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol,
     return execs, skip, gamma_pos, lam, kinds0
 
 
-def decide(S, w, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol, phi=None):
+def decide(S, w, I, local, cands, d_hat, budget, theta, slope, pol, phi=None):
     """Execute/skip decision and server-expert selection for one token.
 
     Eq. (40): the action minimising the per-step cost plus the look-ahead
     cost-to-go phi(x, D-hat after the action) (zero at H = 1, Sec. V-E);
-    ties as in A14.  Returns a dict with the action, per-slot (target, exec,
-    kind, weight), the merged execute rows, the degradation charged, and the
-    margins (all, importance/cost ones, budget ones).
+    ties as in A14 (then the lower option number of step_options).  cands:
+    each expert's local substitute candidates (as_candidates turns a table
+    of best substitutes into them).  Returns a dict with the action, per-slot
+    (target, exec, kind, weight), the merged execute rows, the degradation
+    charged, and the margins (all, importance/cost ones, budget ones).
     """
     k = len(S)
     m_logit, m_budget = [], []
     execs, skip_opt, gamma_pos, lam, kinds0 = step_options(
-        S, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol, m_logit, m_budget)
+        S, I, local, cands, d_hat, budget, theta, slope, pol, m_logit, m_budget)
 
     def total(f, charge, x):
         return f + (phi(x, d_hat + charge) if phi is not None else 0.0)
 
-    options = sorted((total(f, sq, x), n_sub, mask, sq) for (f, n_sub, mask, sq, x) in execs)
-    best_t, best_nsub, best_mask, best_sq = options[0]
+    options = sorted((total(f, sq, x), n_sub, mask, o, sq, x)
+                     for (f, n_sub, mask, o, sq, x) in execs)
+    best_t, _, best_mask, _, best_sq, best_x = options[0]
     if len(options) > 1:
         m_logit.append(options[1][0] - options[0][0])
     skip = False
@@ -275,14 +308,8 @@ def decide(S, w, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol, phi=N
         out.update(action=ACT_SKIP, exec=[-1] * k, kind=[KIND_NONE] * k,
                    d_inc=lam, rows=[])
         return out
-    exec_ids, kinds = [], []
-    for r, e in enumerate(S):
-        if best_mask >> r & 1:
-            exec_ids.append(sub_c[e])
-            kinds.append(KIND_SUB)
-        else:
-            exec_ids.append(e)
-            kinds.append(kinds0[r])
+    exec_ids = list(best_x)
+    kinds = [KIND_SUB if best_mask >> r & 1 else kinds0[r] for r in range(k)]
     rows = []  # merged (expert, weight), first-occurrence rank order (A15)
     for x, wx in zip(exec_ids, w):
         for i, (y, wy) in enumerate(rows):
@@ -314,7 +341,16 @@ def decide(S, w, I, local, sub_c, sub_q, d_hat, budget, theta, slope, pol, phi=N
 # confidence is unknown; the calibration sets of Eq. (36) are not part of
 # the step), so the recursion ranges over execute and skip.  L6 the
 # recursion stops at the last layer.  L7 the decision at the current layer
-# keeps the tie order of A14 on the totals f + Phi.
+# keeps the tie order of A14 on the totals f + Phi, then the lower option
+# number (step_options).  L8 every level of the recursion, and the decision
+# itself, offer each remote slot its target and its local substitute
+# candidates (Sim >= sim_min; the policy's la_subs of least loss, ties to
+# the lower id): Eq. (34) admits every deployed feasible expert, and with a
+# cost-to-go a higher-loss substitute whose transition row leads to local
+# experts can win.  Substitutes are offered for remote targets only, among
+# local experts: on one device a remote substitute costs the same round trip
+# as the exact target, and a local target already costs the least delay,
+# which is what substitution exists to reach (Sec. III-A).
 # ----------------------------------------------------------------------------
 def cost_to_go(model, tables, l: int, h: int, x, d_hat: float, I: float, budget: float, pol,
                m_logit, m_budget, memo=None):
@@ -328,7 +364,7 @@ def cost_to_go(model, tables, l: int, h: int, x, d_hat: float, I: float, budget:
         return memo[key]
     rows = model["layers"][l]["trans"]
     nxt = model["layers"][l + 1]
-    sub_c, sub_q, sub_m = tables[l + 1]
+    cands, sub_m = tables[l + 1]
     acc = 0.0
     for combo in _tuples([rows[e] for e in x]):
         prob = 1.0
@@ -338,15 +374,15 @@ def cost_to_go(model, tables, l: int, h: int, x, d_hat: float, I: float, budget:
             continue
         tau = [t for t, _ in combo]
         m_budget.extend(sub_m[e] for e in tau if not nxt["local_mask"][e])
-        execs, skip, _, _, _ = step_options(tau, I, nxt["local_mask"], sub_c, sub_q, d_hat,
+        execs, skip, _, _, _ = step_options(tau, I, nxt["local_mask"], cands, d_hat,
                                             budget, nxt["theta"], nxt["skip_slope"], pol,
                                             m_logit, m_budget)
-        cands = [(f, sq, xo) for (f, _, _, sq, xo) in execs]
+        acts = [(f, sq, xo) for (f, _, _, _, sq, xo) in execs]
         if skip is not None:
-            cands.append(skip)
+            acts.append(skip)
         best = min(f + cost_to_go(model, tables, l + 1, h - 1, xo, d_hat + charge, I, budget,
                                   pol, m_logit, m_budget, memo)
-                   for f, charge, xo in cands)
+                   for f, charge, xo in acts)
         acc += prob * best
     if memo is not None:
         memo[key] = acc
@@ -425,15 +461,18 @@ def layer_step(model, l: int, pol, state, token_budget=None, token_p_exit=None):
     T = state["h"].shape[0]
     bf16 = model["dtype"] == "bf16"
     local = [bool(v) for v in L["local_mask"]]
-    sub_c, sub_q, sub_m = substitutes(L["sim"], local, pol["phi_scale"],
-                                      pol["sim_min"])
     # look-ahead over the next H - 1 layers (Eq. (39)); H = 1 is the myopic rule
     H = int(pol.get("horizon", 1))
+    # substitute candidates per remote slot: the best one at H = 1 (A13),
+    # the la_subs least-loss ones under look-ahead (L8)
+    n_cand = int(pol.get("la_subs", 1)) if H > 1 else 1
+    cands, sub_m = substitute_candidates(L["sim"], local, pol["phi_scale"], pol["sim_min"],
+                                         n_cand)
     tables = {}
     for j in range(l + 1, min(l + H, N)):
         Lj = model["layers"][j]
-        tables[j] = substitutes(Lj["sim"], [bool(v) for v in Lj["local_mask"]],
-                                pol["phi_scale"], pol["sim_min"])
+        tables[j] = substitute_candidates(Lj["sim"], [bool(v) for v in Lj["local_mask"]],
+                                          pol["phi_scale"], pol["sim_min"], n_cand)
 
     tr = dict(action=np.zeros(T, np.int8),
               target=np.full((T, k), -1, np.int16),
@@ -465,7 +504,7 @@ def layer_step(model, l: int, pol, state, token_budget=None, token_p_exit=None):
             def phi(x, d, I=I, budget=budget, memo=memo):
                 return cost_to_go(model, tables, l, H - 1, x, d, I, budget, pol, la_logit,
                                   la_budget, memo)
-        dec = decide(S, w, I, local, sub_c, sub_q, state["d_acc"][q], budget,
+        dec = decide(S, w, I, local, cands, state["d_acc"][q], budget,
                      L["theta"], L["skip_slope"], pol, phi)
         m_logit = min([m_route] + dec["margins_logit"] + la_logit)
         m_budget = min(dec["margins_budget"] + la_budget

@@ -162,7 +162,7 @@ def test_decide_matches_exhaustive_action_set(seed):
     theta = rs.uniform(0, 1)
     slope = rs.uniform(0, 0.2)
     c, q, _ = O.substitutes(sim, local, pol["phi_scale"], pol["sim_min"])
-    dec = O.decide(S, w, I, local, c, q, d_hat, budget, theta, slope, pol)
+    dec = O.decide(S, w, I, local, O.as_candidates(c, q), d_hat, budget, theta, slope, pol)
     f_min, act, assigns = _brute_force_decision(S, w, I, local, sim, d_hat,
                                                 budget, theta, slope, pol)
     assert dec["action"] == act
@@ -189,7 +189,7 @@ def test_golden_decisions(case):
     assert S == case["expect"]["S"]
     assert I == pytest.approx(case["expect"]["I"], abs=5e-5)
     c, q, _ = O.substitutes(sim, local, pol["phi_scale"], pol["sim_min"])
-    dec = O.decide(S, w, I, local, c, q, case["d_hat"], pol["budget"],
+    dec = O.decide(S, w, I, local, O.as_candidates(c, q), case["d_hat"], pol["budget"],
                    case["theta"], case["slope"], pol)
     ex = case["expect"]
     assert dec["action"] == ex["action"]
