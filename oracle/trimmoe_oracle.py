@@ -129,8 +129,11 @@ def substitute_candidates(sim, local, phi_scale: float, sim_min: float, n: int):
     V_{l,e} of Sec. III-A restricted to this device's experts), the n of
     least Q(e, j) in ascending (Q, j) order (ties to the lower j).  Returns
     (cands, margins): cands[e] = [(j, Q), ...]; margins[e] = the smallest
-    deciding margin of the list (gaps between consecutive Q among the first
-    n + 1 candidates, and any candidate's distance of Sim to sim_min).
+    deciding margin of the list: the Q gap at its cut (between the n-th and
+    the (n + 1)-th candidate, which decides which experts are offered at
+    all) and any candidate's distance of Sim to sim_min.  The order inside
+    the list decides nothing by itself: options differ by their costs,
+    whose own gaps are recorded where they are compared.
     """
     E = len(local)
     cands, margins = [], []
@@ -145,8 +148,8 @@ def substitute_candidates(sim, local, phi_scale: float, sim_min: float, n: int):
             if s >= sim_min:
                 lst.append((q_loss(s, phi_scale), j))
         lst.sort()
-        for (qa, _), (qb, _) in zip(lst[:n], lst[1:n + 1]):
-            m = min(m, qb - qa)
+        if len(lst) > n:
+            m = min(m, lst[n][0] - lst[n - 1][0])
         cands.append([(j, q) for q, j in lst[:n]])
         margins.append(m)
     return cands, margins
