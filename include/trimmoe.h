@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define TRIMMOE_ABI_VERSION 4
+#define TRIMMOE_ABI_VERSION 5
 
 /* status codes */
 #define TRIMMOE_OK 0
@@ -72,11 +72,13 @@ extern "C" {
 #define TRIMMOE_MAX_EXPERTS 256
 #define TRIMMOE_MAX_TOPK 8
 /* look-ahead (policy.horizon > 1): H <= 4, top_k <= 4, 1 <= trans_b <= 8,
- * (2^k + 1) * trans_b^k <= 1024 first-level branches per token, and
- * (2^k + 1)^H * trans_b^(k (H - 1)) <= 2^21 cost evaluations per token */
+ * 1 <= la_subs <= 4, and with O = (1 + la_subs)^k + 1 options per token:
+ * O * trans_b^k <= 1024 first-level branches per token and
+ * O^H * trans_b^(k (H - 1)) <= 2^23 cost evaluations per token */
 #define TRIMMOE_MAX_HORIZON 4
 #define TRIMMOE_MAX_LOOKAHEAD_TOPK 4
 #define TRIMMOE_MAX_TRANS_B 8
+#define TRIMMOE_MAX_LA_SUBS 4
 
 /* actions recorded in the trace */
 #define TRIMMOE_ACT_INACTIVE 0
@@ -147,7 +149,12 @@ typedef struct trimmoe_model {
  * (its routed target after a skip), starting from the budget the action
  * leaves.  The token's importance at this layer stands in for later ones,
  * exits are not predicted inside the recursion, and the token never moves
- * (one GPU: the location in Eq. (39) is always this device).
+ * (one GPU: the location in Eq. (39) is always this device).  Under the
+ * look-ahead each remote slot may run its target or any of its la_subs
+ * least-loss local substitutes (Sim >= sim_min, ties to the lower id), at
+ * this layer and at every level of the recursion: Eq. (34) admits every
+ * feasible one, and the cost-to-go depends on the expert run.  At H = 1 only
+ * the least-loss one can be optimal and la_subs is not read.
  */
 typedef struct trimmoe_policy {
   float p_exit;      /* confidence requirement p_J (Eq. (8))               */
@@ -161,6 +168,9 @@ typedef struct trimmoe_policy {
   const float* budget_tok; /* [T] device, per-token budget, or NULL         */
   int32_t horizon;   /* look-ahead horizon H, 1..TRIMMOE_MAX_HORIZON (Sec. V-E,
                         Eq. (39), (40)); 1 = the myopic rule                */
+  int32_t la_subs;   /* H > 1: local substitute candidates per remote slot,
+                        1..TRIMMOE_MAX_LA_SUBS (the least-loss ones); not
+                        read at H = 1                                      */
 } trimmoe_policy;
 
 /*

@@ -18,7 +18,7 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libtrimmoe.so")
 
-ABI_VERSION = 4   # TRIMMOE_ABI_VERSION this binding is written for
+ABI_VERSION = 5   # TRIMMOE_ABI_VERSION this binding is written for
 STATIC_SCRATCH_BYTES = 64 << 20  # TRIMMOE_STATIC_SCRATCH_BYTES
 N_COUNTERS = 16   # per-layer trace counters (row stride of trimmoe_trace.counters)
 TRIMMOE_OK = 0
@@ -52,7 +52,7 @@ class Policy(C.Structure):
     _fields_ = [("p_exit", C.c_float), ("budget", C.c_float), ("omega_t", C.c_float),
                 ("t_local", C.c_float), ("t_remote", C.c_float), ("phi_scale", C.c_float),
                 ("sim_min", C.c_float), ("p_exit_tok", C.c_void_p),
-                ("budget_tok", C.c_void_p), ("horizon", C.c_int32)]
+                ("budget_tok", C.c_void_p), ("horizon", C.c_int32), ("la_subs", C.c_int32)]
 
 
 class State(C.Structure):
@@ -406,10 +406,11 @@ class ModelHandle:
 
 
 def make_policy(*, p_exit, budget, omega_t, t_local, t_remote, phi_scale, sim_min,
-                p_exit_tok=None, budget_tok=None, horizon=1) -> Policy:
+                p_exit_tok=None, budget_tok=None, horizon=1, la_subs=4) -> Policy:
     return Policy(p_exit, budget, omega_t, t_local, t_remote, phi_scale, sim_min,
                   None if p_exit_tok is None else p_exit_tok.data_ptr(),
-                  None if budget_tok is None else budget_tok.data_ptr(), int(horizon))
+                  None if budget_tok is None else budget_tok.data_ptr(), int(horizon),
+                  int(la_subs))
 
 
 class StateBuffers:

@@ -77,11 +77,14 @@ int validate_policy(const trimmoe_policy* p) {
     return TRIMMOE_ERR_POLICY;
   if (!(p->phi_scale >= 0.f) || isinf(p->phi_scale)) return TRIMMOE_ERR_POLICY;
   if (p->horizon < 1 || p->horizon > TRIMMOE_MAX_HORIZON) return TRIMMOE_ERR_POLICY;
+  if (p->horizon > 1 && (p->la_subs < 1 || p->la_subs > TRIMMOE_MAX_LA_SUBS))
+    return TRIMMOE_ERR_POLICY;
   return TRIMMOE_OK;
 }
 
 // The look-ahead's limits (policy.horizon > 1): its work per token grows as
-// (2^k + 1)^H * B^(k (H - 1)) cost evaluations.  Layers first..last run;
+// O^H * B^(k (H - 1)) cost evaluations, O = (1 + la_subs)^k + 1 options per
+// level.  Layers first..last run;
 // layer l reads the transitions of layers l .. l + H - 2 (not past N - 2).
 int validate_lookahead(const trimmoe_model* m, const trimmoe_policy* p, int first, int last) {
   // the horizon the first layer run sees (later layers see no more)
@@ -91,9 +94,12 @@ int validate_lookahead(const trimmoe_model* m, const trimmoe_policy* p, int firs
   if (k > TRIMMOE_MAX_LOOKAHEAD_TOPK || B < 1 || B > TRIMMOE_MAX_TRANS_B) return TRIMMOE_ERR_SHAPE;
   double tuples = 1.0;
   for (int s = 0; s < k; ++s) tuples *= B;
-  const double opts = (double)((1 << k) + 1);
+  const double opts = pow(1.0 + p->la_subs, k) + 1.0;
   if (opts * tuples > kMaxBranches) return TRIMMOE_ERR_SHAPE;
-  if (pow(opts, H) * pow(tuples, H - 1) > (double)(1 << 21)) return TRIMMOE_ERR_SHAPE;
+  if (pow(opts, H) * pow(tuples, H - 1) > (double)(1 << 23)) return TRIMMOE_ERR_SHAPE;
+  if (route_lds_bytes(m->dtype == TRIMMOE_BF16, m->n_experts, m->d_model, H, B, k, p->la_subs) >
+      kRouteLdsMax)
+    return TRIMMOE_ERR_SHAPE;
   const int end = std::min(last + H - 1, m->n_layers - 1);
   for (int l = first; l < end; ++l)
     if (!m->layers[l].trans_to || !m->layers[l].trans_p) return TRIMMOE_ERR_NULL;
@@ -233,6 +239,7 @@ void fill_params(LayerParams& P, const trimmoe_model* m, int l, const trimmoe_po
   P.p_exit_tok = pol->p_exit_tok;
   P.budget_tok = pol->budget_tok;
   P.horizon = std::min(pol->horizon, m->n_layers - l);
+  P.la_subs = P.horizon > 1 ? pol->la_subs : 1;
   P.trans_b = m->trans_b;
   P.rb = route_block_tokens(T, P.horizon > 1);
   P.bm = expert_tile_rows(m->dtype == TRIMMOE_BF16, T, k, m->n_experts, m->d_model, m->d_ff);

@@ -145,6 +145,7 @@ struct LayerParams {
   // look-ahead (Eq. (39)): la_*[j - 1] describe layer + j for j = 1 ..
   // horizon - 1; la_tto/la_tp[j] the transitions from layer + j to the next
   int horizon;  // effective horizon: min(policy horizon, N - layer)
+  int la_subs;  // look-ahead: local substitute candidates per remote slot (1 at H = 1)
   int trans_b;
   int rb;       // tokens per route block (route, scan and bucket agree on it)
   int bm;       // rows per expert tile of the grouped GEMMs (kGemmBM or kBigBM)
@@ -254,5 +255,10 @@ hipError_t launch_expert_down(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_shared_expert(const LayerParams& p, bool bf16, hipStream_t st);
 hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st);
 int down_splits(int max_tiles, int N, int K);
+// dynamic LDS of a route block (logits, and the look-ahead tables at H > 1)
+size_t route_lds_bytes(bool bf16, int E, int d, int horizon, int trans_b, int k, int la_subs);
+// dynamic LDS a route block may take next to its static arrays (gfx950: 160 KB
+// per workgroup)
+constexpr size_t kRouteLdsMax = 150 * 1024;
 
 }  // namespace trimmoe

@@ -112,20 +112,67 @@ __device__ inline void best_substitute(const float* sim, const uint8_t* local, i
   q = best < E ? bq : 0.f;
 }
 
+// Under look-ahead a remote slot may run its target or any of its local
+// substitute candidates (the C = la_subs of least Q with Sim >= sim_min, in
+// ascending (Q, j) order): Eq. (34) admits every feasible one, and the
+// cost-to-go depends on which expert runs.  One wavefront per row e: C
+// rounds, each taking the least (Q, j) after the previous pick (lanes scan
+// j = lane, lane + 64, ..., then a butterfly).  c[r] = -1 past the last.
+__device__ inline void best_candidates(const float* sim, const uint8_t* local, int E, int e,
+                                       float phi_scale, float sim_min, int lane, int C,
+                                       int16_t* c, float* q) {
+  int pj = -1;
+  float pq = -1.f;
+  for (int r = 0; r < C; ++r) {
+    int best = E;
+    float bq = 0.f;
+    for (int j = lane; j < E; j += 64) {
+      const float sv = sim[(size_t)e * E + j];
+      if (j == e || !local[j] || !(sv >= sim_min)) continue;
+      const float qj = fminf(1.f, phi_scale * (1.f - sv) * 0.5f);
+      const bool after = qj > pq || (qj == pq && j > pj);
+      if (after && (best == E || qj < bq)) {
+        best = j;
+        bq = qj;
+      }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const float oq = __shfl_xor(bq, off);
+      const int oj = __shfl_xor(best, off);
+      if (oj < E && (best == E || oq < bq || (oq == bq && oj < best))) {
+        best = oj;
+        bq = oq;
+      }
+    }
+    if (lane == 0) {
+      c[r] = (int16_t)(best < E ? best : -1);
+      q[r] = best < E ? bq : 0.f;
+    }
+    if (best == E) {
+      for (int t = r + 1; t < C; ++t)
+        if (lane == 0) c[t] = -1;
+      break;
+    }
+    pj = best;
+    pq = bq;
+  }
+}
+
 // ------------------------------------------------ look-ahead (Eq. (39)) --
 // Cost-to-go of a token over the later layers of the horizon.  The token
 // never moves (one GPU), so it depends on an action only through the
 // experts the slots run (sources of the next-layer transitions) and the
 // budget the action leaves.  Level j is layer + j; its placement and
-// substitute table are at [j - 1], the transitions out of level j at [j].
+// candidate lists are at [j - 1], the transitions out of level j at [j].
 // Every slot moves independently (a tuple's probability is the product of
 // its slots'); the token's current importance stands in for later ones;
 // exits are not predicted.  All arrays live in the route block's LDS.
 struct LaView {
-  int E, k, B, ntup;          // ntup = B^k next-layer tuples
+  int E, k, B, ntup, C;       // ntup = B^k next-layer tuples; C candidates per row
   const uint8_t* mask;        // [horizon - 1][E]
-  const int16_t* subc;        // [horizon - 1][E]
-  const float* subq;          // [horizon - 1][E]
+  const int16_t* cand;        // [horizon - 1][E][C], -1 = none
+  const float* candq;         // [horizon - 1][E][C]
   const int16_t* tto;         // [horizon - 1][E * B], -1 = padding
   const float* tp;            // [horizon - 1][E * B]
   const float* theta;         // [horizon - 1]
@@ -150,6 +197,39 @@ __device__ inline float la_tuple(const LaView& v, int j, const int* x, int it, i
   return prob;
 }
 
+// number of candidates in a row of C entries (-1 padded)
+__device__ inline int la_ncand(const int16_t* row, int C) {
+  int n = 0;
+  while (n < C && row[n] >= 0) ++n;
+  return n;
+}
+
+// Execute option o of a token: slots in rank order, the remote ones with
+// candidates (ranks rs[0..nsub), radices rad[u] = 1 + candidates) as mixed-
+// radix digits, rs[0] the lowest; digit d > 0 runs candidate d - 1 of the
+// slot's row.  Writes the experts run into x and returns the summed Q;
+// *mask gets the substituted ranks.
+__device__ inline float la_option(int o, int k, const int* tau, const int* rs, const int* rad,
+                                  int nsub, const int16_t* cand, const float* candq, int C,
+                                  int* x, int* mask) {
+  for (int s = 0; s < k; ++s) x[s] = tau[s];
+  float sq = 0.f;
+  int m = 0;
+  for (int u = 0; u < nsub; ++u) {
+    const int d = o % rad[u];
+    o /= rad[u];
+    if (d > 0) {
+      const int s = rs[u];
+      const size_t at = (size_t)tau[s] * C + d - 1;
+      x[s] = cand[at];
+      sq += candq[at];
+      m |= 1 << s;
+    }
+  }
+  *mask = m;
+  return sq;
+}
+
 template <int R>
 __device__ float la_phi(const LaView& v, int j, const int* x, float D, float I, float b);
 
@@ -160,37 +240,31 @@ template <int R>
 __device__ float la_inner(const LaView& v, int j, const int* tau, float D, float I, float b) {
   const int lev = j - 1;
   const uint8_t* mask = v.mask + (size_t)lev * v.E;
-  const int16_t* subc = v.subc + (size_t)lev * v.E;
-  const float* subq = v.subq + (size_t)lev * v.E;
-  int n_loc = 0, n_rem = 0, nsub = 0;
-  int rs[TRIMMOE_MAX_LOOKAHEAD_TOPK];
-  float q[TRIMMOE_MAX_LOOKAHEAD_TOPK];
+  const int16_t* cand = v.cand + (size_t)lev * v.E * v.C;
+  const float* candq = v.candq + (size_t)lev * v.E * v.C;
+  int n_loc = 0, n_rem = 0, nsub = 0, nopt = 1;
+  int rs[TRIMMOE_MAX_LOOKAHEAD_TOPK], rad[TRIMMOE_MAX_LOOKAHEAD_TOPK];
   for (int s = 0; s < v.k; ++s) {
     const int e = tau[s];
     if (mask[e]) {
       ++n_loc;
-      q[s] = 0.f;
     } else {
       ++n_rem;
-      const int c = subc[e];
-      q[s] = c >= 0 ? subq[e] : 0.f;
-      if (c >= 0) rs[nsub++] = s;
+      const int n = la_ncand(cand + (size_t)e * v.C, v.C);
+      if (n > 0) {
+        rs[nsub] = s;
+        rad[nsub++] = 1 + n;
+        nopt *= 1 + n;
+      }
     }
   }
   float best = __builtin_inff();
   bool all_local = false;
-  for (int sel = 0; sel < (1 << nsub); ++sel) {
-    float sq = 0.f;
-    int ns = 0;
-    int x[TRIMMOE_MAX_LOOKAHEAD_TOPK];
-    for (int s = 0; s < v.k; ++s) x[s] = tau[s];
-    for (int u = 0; u < nsub; ++u)
-      if ((sel >> u) & 1) {
-        sq += q[rs[u]];
-        ++ns;
-        x[rs[u]] = subc[tau[rs[u]]];
-      }
+  for (int o = 0; o < nopt; ++o) {
+    int x[TRIMMOE_MAX_LOOKAHEAD_TOPK], m;
+    const float sq = la_option(o, v.k, tau, rs, rad, nsub, cand, candq, v.C, x, &m);
     if (D + sq <= b) {
+      const int ns = __popc(m);
       if (ns == n_rem) all_local = true;
       float f = v.wt * ((float)(n_loc + ns) * v.tl + (float)(n_rem - ns) * v.tr) +
                 (b > 0.f ? v.wd * sq / b : 0.f);
@@ -229,15 +303,24 @@ __device__ inline float la_inner_top(const LaView& v, int rem, const int* tau, f
   return la_inner<2>(v, 1, tau, D, I, b);
 }
 
+// options of a token at the layer itself: (1 + C)^k execute options at most,
+// plus the skip
+__host__ __device__ inline int la_opt_max(int C, int k) {
+  int n = 1;
+  for (int s = 0; s < k; ++s) n *= 1 + C;
+  return n + 1;
+}
+
 // A route block's look-ahead LDS, after the logits: 4-byte arrays first,
 // then 2-byte, then bytes.  base == NULL only measures.  Returns bytes.
 struct LaLds {
-  float *tp, *subq, *theta, *slope;  // later layers (see LaView)
-  float* branch;                      // [waves][(2^k + 1) B^k] first-level values
-  float* phi;                         // [RB][2^kmax + 1] cost-to-go per option
+  float *tp, *candq, *theta, *slope;  // later layers (see LaView)
+  float* candq0;                      // [E][C] this layer's candidate losses
+  float* branch;                      // [waves][opt_max B^k] first-level values
+  float* phi;                         // [RB][opt_max] cost-to-go per option
   float *tokI, *tokD, *tokB;          // [RB] importance, D-hat, budget
-  int* nsub;                          // [RB] substitutable remote slots
-  int16_t *tto, *subc;
+  int* nopt;                          // [RB] execute options
+  int16_t *tto, *cand, *cand0;        // cand0: [E][C] this layer's candidates
   uint8_t *mask, *skipok;             // skipok: [RB] skip admitted at this layer
 };
 
@@ -247,7 +330,7 @@ __host__ __device__ inline int la_ntup(int B, int k) {
   return n;
 }
 
-__host__ __device__ inline size_t la_carve(char* base, int E, int B, int k, int nlev,
+__host__ __device__ inline size_t la_carve(char* base, int E, int B, int k, int nlev, int C,
                                            LaLds* o) {
   size_t off = 0;
   auto take = [&](size_t bytes) -> char* {
@@ -255,21 +338,23 @@ __host__ __device__ inline size_t la_carve(char* base, int E, int B, int k, int 
     off += (bytes + 3) & ~(size_t)3;
     return q;
   };
-  const size_t branches = (size_t)((1 << k) + 1) * la_ntup(B, k);
+  const size_t opts = (size_t)la_opt_max(C, k);
   LaLds tmp;
   LaLds& L = o ? *o : tmp;
   L.tp = (float*)take((size_t)nlev * E * B * 4);
-  L.subq = (float*)take((size_t)nlev * E * 4);
+  L.candq = (float*)take((size_t)nlev * E * C * 4);
   L.theta = (float*)take((size_t)nlev * 4);
   L.slope = (float*)take((size_t)nlev * 4);
-  L.branch = (float*)take((size_t)kRouteWaves * branches * 4);
-  L.phi = (float*)take((size_t)RB * ((1 << TRIMMOE_MAX_LOOKAHEAD_TOPK) + 1) * 4);
+  L.candq0 = (float*)take((size_t)E * C * 4);
+  L.branch = (float*)take((size_t)kRouteWaves * opts * la_ntup(B, k) * 4);
+  L.phi = (float*)take((size_t)RB * opts * 4);
   L.tokI = (float*)take((size_t)RB * 4);
   L.tokD = (float*)take((size_t)RB * 4);
   L.tokB = (float*)take((size_t)RB * 4);
-  L.nsub = (int*)take((size_t)RB * 4);
+  L.nopt = (int*)take((size_t)RB * 4);
   L.tto = (int16_t*)take((size_t)nlev * E * B * 2);
-  L.subc = (int16_t*)take((size_t)nlev * E * 2);
+  L.cand = (int16_t*)take((size_t)nlev * E * C * 2);
+  L.cand0 = (int16_t*)take((size_t)E * C * 2);
   L.mask = (uint8_t*)take((size_t)nlev * E);
   L.skipok = (uint8_t*)take((size_t)RB);
   return off;
@@ -288,13 +373,14 @@ template <bool BF16, bool LA>
 __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   extern __shared__ float zs[];  // [route_ks][RB][E] logits, K partial sums; then LaLds
   __shared__ int s_cnt[TRIMMOE_MAX_EXPERTS];
-  __shared__ int s_subc[TRIMMOE_MAX_EXPERTS];
+  __shared__ int16_t s_subc[TRIMMOE_MAX_EXPERTS];  // best substitute (H = 1)
   __shared__ float s_subq[TRIMMOE_MAX_EXPERTS];
   __shared__ int s_xcnt;
   __shared__ int sS[RB][KMAX];
-  __shared__ float sQ[RB][KMAX];
   __shared__ float sW[RB][KMAX];    // slot weights in rank order
   __shared__ int sRsub[RB][KMAX];   // ranks of substitutable remote slots
+  __shared__ int sRad[RB][KMAX];    // their radices: 1 + candidates
+  __shared__ int sNsub[RB];
   __shared__ int sRx[RB][KMAX];     // merged rows: expert
   __shared__ float sRw[RB][KMAX];   // merged rows: summed weight
   __shared__ float sI[RB];          // importance: summed weight of the picks
@@ -314,7 +400,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     float q;
     best_substitute(p.sim, p.local_mask, E, e, p.phi_scale, p.sim_min, lane, c, q);
     if (lane == 0) {
-      s_subc[e] = c;
+      s_subc[e] = (int16_t)c;
       s_subq[e] = q;
     }
   }
@@ -323,21 +409,20 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   LaView lv;
   const int nlev = LA ? p.horizon - 1 : 0;
   if constexpr (LA) {
-    const int B = p.trans_b;
+    const int B = p.trans_b, C = p.la_subs;
     const int ks = BF16 ? route_ks(E, d) : 1;
-    la_carve(reinterpret_cast<char*>(zs + (size_t)ks * RB * E), E, B, k, nlev, &la);
-    // later layers: placement, substitute tables, theta and slope; the
-    // transitions out of this layer and every later one but the last
+    la_carve(reinterpret_cast<char*>(zs + (size_t)ks * RB * E), E, B, k, nlev, C, &la);
+    // this layer's candidate lists, then the later layers': placement,
+    // candidate lists, theta and slope; the transitions out of this layer
+    // and every later one but the last
+    for (int e = wave; e < E; e += kRouteWaves)
+      best_candidates(p.sim, p.local_mask, E, e, p.phi_scale, p.sim_min, lane, C,
+                      la.cand0 + (size_t)e * C, la.candq0 + (size_t)e * C);
     for (int idx = wave; idx < nlev * E; idx += kRouteWaves) {
       const int j = idx / E, e = idx % E;
-      int c;
-      float q;
-      best_substitute(p.la_sim[j], p.la_mask[j], E, e, p.phi_scale, p.sim_min, lane, c, q);
-      if (lane == 0) {
-        la.mask[idx] = p.la_mask[j][e] ? 1 : 0;
-        la.subc[idx] = (int16_t)c;
-        la.subq[idx] = q;
-      }
+      best_candidates(p.la_sim[j], p.la_mask[j], E, e, p.phi_scale, p.sim_min, lane, C,
+                      la.cand + (size_t)idx * C, la.candq + (size_t)idx * C);
+      if (lane == 0) la.mask[idx] = p.la_mask[j][e] ? 1 : 0;
     }
     for (int idx = threadIdx.x; idx < nlev * E * B; idx += blockDim.x) {
       const int j = idx / (E * B), r = idx % (E * B);
@@ -350,7 +435,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
       la.theta[threadIdx.x] = p.la_theta[threadIdx.x];
       la.slope[threadIdx.x] = p.la_slope[threadIdx.x];
     }
-    lv = LaView{E, k, B, la_ntup(B, k), la.mask, la.subc, la.subq, la.tto, la.tp,
+    lv = LaView{E, k, B, la_ntup(B, k), C, la.mask, la.cand, la.candq, la.tto, la.tp,
                 la.theta, la.slope, p.omega_t, 1.f - p.omega_t, p.t_local, p.t_remote};
   }
 
@@ -533,45 +618,56 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   __syncthreads();
 
   const int i = threadIdx.x;
-  int pos = 0, t = 0, n_loc = 0, n_rem = 0, nsub = 0;
+  int pos = 0, t = 0, n_loc = 0, n_rem = 0, nsub = 0, nopt = 1;
   float I = 0.f, budget = 0.f, D = 0.f;
+  // each remote slot's candidates: its best substitute at H = 1 (A13), its
+  // C = la_subs least-loss local candidates under look-ahead
+  const int C = LA ? p.la_subs : 1;
+  const int16_t* cand = LA ? la.cand0 : s_subc;
+  const float* candq = LA ? la.candq0 : s_subq;
   if (i < nt) {
     pos = base + i;
     t = p.active_idx[pos];
     I = sI[i];
 
-    // resolve slots: local exact, or remote with/without a local substitute
+    // resolve slots: local exact, or remote with or without candidates
     for (int r = 0; r < k; ++r) {
       const int e = sS[i][r];
       if (p.local_mask[e]) {
         ++n_loc;
-        sQ[i][r] = 0.f;
       } else {
         ++n_rem;
-        const int c = s_subc[e];
-        sQ[i][r] = c >= 0 ? s_subq[e] : 0.f;
-        if (c >= 0) sRsub[i][nsub++] = r;
+        const int n = la_ncand(cand + (size_t)e * C, C);
+        if (n > 0) {
+          sRsub[i][nsub] = r;
+          sRad[i][nsub++] = 1 + n;
+          nopt *= 1 + n;
+        }
       }
     }
+    sNsub[i] = nsub;
     budget = p.budget_tok ? p.budget_tok[t] : p.budget;
     D = p.d_acc[t];
   }
 
   if constexpr (LA) {
     // Eq. (39)-(40): cost-to-go of every candidate action of the block's
-    // tokens.  Options 0 .. 2^nsub - 1 execute (bit u substitutes slot
-    // sRsub[u]); option 2^nsub skips.  Every branch (option, next-layer
-    // tuple) is one lane's work; a wavefront takes one token at a time and
-    // sums the branches of each option in tuple order.
+    // tokens.  Options 0 .. nopt - 1 execute (la_option's mixed-radix
+    // numbering over the substitutable remote slots); option nopt skips.
+    // Every branch (option, next-layer tuple) is one lane's work; a
+    // wavefront takes one token at a time and sums the branches of each
+    // option in tuple order.
+    const int opt_max = la_opt_max(C, k);
     if (i < nt) {
       la.tokI[i] = I;
       la.tokD[i] = D;
       la.tokB[i] = budget;
-      la.nsub[i] = nsub;
+      la.nopt[i] = nopt;
       // the skip is a candidate iff Gamma > 0 (no feasible all-local
-      // assignment, Eq. (35)), I <= theta and the budget admits Lambda
+      // assignment, Eq. (35): the cheapest one takes every slot's least-loss
+      // candidate), I <= theta and the budget admits Lambda
       float sq_all = 0.f;
-      for (int u = 0; u < nsub; ++u) sq_all += sQ[i][sRsub[i][u]];
+      for (int u = 0; u < nsub; ++u) sq_all += candq[(size_t)sS[i][sRsub[i][u]] * C];
       const bool all_local = nsub == n_rem && D + sq_all <= budget;
       const float lam = fminf(1.f, p.skip_slope * I);
       la.skipok[i] = !all_local && I <= p.theta && D + lam <= budget;
@@ -582,27 +678,23 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     const int tpr = min(p.rb, kRouteWaves), wpt = kRouteWaves / tpr;
     const int slot = wave / wpt, wsub = wave % wpt;
     const int ntup = lv.ntup, rem = nlev - 1;
-    float* br = la.branch + (size_t)slot * ((1 << k) + 1) * ntup;
+    float* br = la.branch + (size_t)slot * opt_max * ntup;
     for (int r = 0; r * tpr < p.rb; ++r) {
       const int ti = slot + tpr * r;
-      const int nopt = ti < nt ? (1 << la.nsub[ti]) + 1 : 0;
-      for (int it = wsub * 64 + lane; it < nopt * ntup; it += wpt * 64) {
+      const int nall = ti < nt ? la.nopt[ti] + 1 : 0;  // with the skip
+      for (int it = wsub * 64 + lane; it < nall * ntup; it += wpt * 64) {
         const int o = it / ntup, tup = it % ntup;
-        const int ns = la.nsub[ti];
         const float Dt = la.tokD[ti], bt = la.tokB[ti], It = la.tokI[ti];
         int x[TRIMMOE_MAX_LOOKAHEAD_TOPK];
-        for (int s = 0; s < k; ++s) x[s] = sS[ti][s];
-        float charge = 0.f;
+        float charge;
         bool feasible;
-        if (o < (1 << ns)) {
-          for (int u = 0; u < ns; ++u)
-            if ((o >> u) & 1) {
-              const int s = sRsub[ti][u];
-              charge += sQ[ti][s];
-              x[s] = s_subc[sS[ti][s]];
-            }
+        if (o < nall - 1) {
+          int m;
+          charge = la_option(o, k, sS[ti], sRsub[ti], sRad[ti], sNsub[ti], cand, candq, C, x,
+                             &m);
           feasible = Dt + charge <= bt;
         } else {
+          for (int s = 0; s < k; ++s) x[s] = sS[ti][s];
           charge = fminf(1.f, p.skip_slope * It);
           feasible = la.skipok[ti] != 0;
         }
@@ -615,44 +707,44 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
         br[it] = val;
       }
       __syncthreads();
-      if (wsub == 0 && lane < nopt) {
-        float acc = 0.f;
-        for (int u = 0; u < ntup; ++u) acc += br[lane * ntup + u];
-        la.phi[ti * ((1 << TRIMMOE_MAX_LOOKAHEAD_TOPK) + 1) + lane] = acc;
-      }
+      if (wsub == 0)
+        for (int o = lane; o < nall; o += 64) {
+          float acc = 0.f;
+          for (int u = 0; u < ntup; ++u) acc += br[o * ntup + u];
+          la.phi[ti * opt_max + o] = acc;
+        }
       __syncthreads();
     }
   }
 
   if (i < nt) {
     const float wt = p.omega_t, wd = 1.f - p.omega_t;
-    const float* phi = LA ? la.phi + i * ((1 << TRIMMOE_MAX_LOOKAHEAD_TOPK) + 1) : nullptr;
-    // Eq. (34) + Eq. (31): enumerate substitution subsets of remote slots
+    const float* phi = LA ? la.phi + i * la_opt_max(C, k) : nullptr;
+    // Eq. (34) + Eq. (31): every way of serving the remote slots (target or
+    // a candidate) within the budget
     bool have = false, all_local = false;
     float bf = 0.f, bsq = 0.f;
-    int bns = 0, bmask = 0;
-    for (int sel = 0; sel < (1 << nsub); ++sel) {
-      float sq = 0.f;
-      int mask = 0;
-      for (int u = 0; u < nsub; ++u) {
-        if ((sel >> u) & 1) {
-          mask |= 1 << sRsub[i][u];
-          sq += sQ[i][sRsub[i][u]];
-        }
-      }
+    int bns = 0, bmask = 0, bo = 0, bx[KMAX];
+    for (int o = 0; o < nopt; ++o) {
+      int x[KMAX], mask;
+      const float sq = la_option(o, k, sS[i], sRsub[i], sRad[i], nsub, cand, candq, C, x, &mask);
       if (!(D + sq <= budget)) continue;
-      const int ns = __popc(sel);
+      const int ns = __popc(mask);
       if (ns == n_rem) all_local = true;
       float f = wt * ((float)(n_loc + ns) * p.t_local + (float)(n_rem - ns) * p.t_remote) +
                 (budget > 0.f ? wd * sq / budget : 0.f);
-      if constexpr (LA) f += phi[sel];  // Eq. (40): per-step cost + cost-to-go
-      const bool better = !have || f < bf || (f == bf && (ns < bns || (ns == bns && mask < bmask)));
+      if constexpr (LA) f += phi[o];  // Eq. (40): per-step cost + cost-to-go
+      const bool better =
+          !have || f < bf ||
+          (f == bf && (ns < bns || (ns == bns && (mask < bmask || (mask == bmask && o < bo)))));
       if (better) {
         have = true;
         bf = f;
         bns = ns;
         bmask = mask;
+        bo = o;
         bsq = sq;
+        for (int s = 0; s < k; ++s) bx[s] = x[s];
       }
     }
     // Eq. (35) + importance threshold + Eq. (32): skip admission and choice
@@ -660,7 +752,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     bool skip = false;
     if (!all_local && I <= p.theta && D + lam <= budget) {
       float fs = budget > 0.f ? wd * lam / budget : 0.f;
-      if constexpr (LA) fs += phi[1 << nsub];
+      if constexpr (LA) fs += phi[nopt];
       skip = fs < bf;
     }
     if (!have) skip = false;  // unreachable: the empty assignment is feasible
@@ -673,7 +765,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
       int x = -1, kind = TRIMMOE_KIND_NONE;
       if (!skip) {
         if ((bmask >> r) & 1) {
-          x = s_subc[e];
+          x = bx[r];
           kind = TRIMMOE_KIND_SUBST;
           ++nsubst;
         } else {
@@ -1161,12 +1253,17 @@ hipError_t launch_trace_fill(const LayerParams& p, int n_layers, hipStream_t st)
   return hipGetLastError();
 }
 
+size_t route_lds_bytes(bool bf16, int E, int d, int horizon, int trans_b, int k, int la_subs) {
+  size_t lds = (size_t)(bf16 ? route_ks(E, d) : 1) * RB * E * sizeof(float);
+  if (horizon > 1) lds += la_carve(nullptr, E, trans_b, k, horizon - 1, la_subs, nullptr);
+  return lds;
+}
+
 hipError_t launch_route(const LayerParams& p, bool bf16, hipStream_t st) {
   const int nb = cdiv(p.T, p.rb);
-  size_t lds = (size_t)(bf16 ? route_ks(p.E, p.d) : 1) * RB * p.E * sizeof(float);
+  const size_t lds = route_lds_bytes(bf16, p.E, p.d, p.horizon, p.trans_b, p.k, p.la_subs);
   const dim3 grid(nb), block(64 * kRouteWaves);
   if (p.horizon > 1) {
-    lds += la_carve(nullptr, p.E, p.trans_b, p.k, p.horizon - 1, nullptr);
     auto kern = bf16 ? k_route<true, true> : k_route<false, true>;
     if (lds > 65536) {
       const hipError_t e =

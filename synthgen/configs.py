@@ -15,9 +15,10 @@ _COMMON_POLICY = dict(budget=0.02, omega_t=0.5, t_local=1.0, t_remote=100.0,
                       # exit confidence: max softmax of a vocabulary head, or the
                       # sigmoid of a one-row head (vocab_exit = 1)
                       conf_mode="softmax",
-                      # look-ahead horizon H (1: the myopic rule) and the support of
-                      # each row of the expert transition matrices it reads
-                      horizon=1, trans_support=4)
+                      # look-ahead horizon H (1: the myopic rule), the support of
+                      # each row of the expert transition matrices it reads, and the
+                      # local substitute candidates per remote slot it weighs
+                      horizon=1, trans_support=4, la_subs=4)
 
 WORKLOADS = {
     # 2 layers, d=64, ReLU 64->256->64, 8 experts top-1, 64 tokens, fp32

@@ -252,6 +252,7 @@ def make_inputs(cfg, device="cpu", token_seed: int | None = None,
                                   "phi_scale", "sim_min")}
     policy["p_exit"] = cfg["p_exit"]
     policy["horizon"] = int(cfg.get("horizon", 1))
+    policy["la_subs"] = int(cfg.get("la_subs", 4))
     return dict(cfg=cfg, layers=layers, h0=h0, policy=policy)
 
 

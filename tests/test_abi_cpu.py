@@ -241,19 +241,23 @@ def _la_layers(n, E, B, with_trans=True):
     return layers
 
 
-@pytest.mark.parametrize("over,B,horizon,code", [
-    (dict(), 4, 5, -4),                      # horizon above the maximum
-    (dict(), 4, 0, -4),                      # horizon below 1
-    (dict(n_experts=16, top_k=5), 2, 2, -2),  # look-ahead needs top-k <= 4
-    (dict(), 9, 2, -2),                      # rows of more than 8 entries
-    (dict(n_experts=16, top_k=4), 3, 2, -2),  # 17 * 81 first-level branches > 1024
-    (dict(n_layers=4, top_k=2), 8, 4, -2),   # 5^4 * 64^3 evaluations > 2^21
+@pytest.mark.parametrize("over,B,horizon,subs,code", [
+    (dict(), 4, 5, 4, -4),                      # horizon above the maximum
+    (dict(), 4, 0, 4, -4),                      # horizon below 1
+    (dict(), 4, 2, 0, -4),                      # no substitute candidate weighed
+    (dict(), 4, 2, 5, -4),                      # more candidates than the maximum
+    (dict(n_experts=16, top_k=5), 2, 2, 1, -2),  # look-ahead needs top-k <= 4
+    (dict(), 9, 2, 1, -2),                      # rows of more than 8 entries
+    (dict(n_experts=16, top_k=4), 3, 2, 1, -2),  # (2^4 + 1) * 81 first-level branches > 1024
+    (dict(n_experts=16, top_k=4), 2, 2, 2, -2),  # (3^4 + 1) * 16 first-level branches > 1024
+    (dict(n_layers=4, top_k=2), 8, 4, 1, -2),   # 5^4 * 64^3 evaluations > 2^23
+    (dict(n_layers=4, top_k=2), 4, 4, 4, -2),   # 26^4 * 16^3 evaluations > 2^23
 ])
-def test_look_ahead_limits_rejected_before_launch(over, B, horizon, code):
+def test_look_ahead_limits_rejected_before_launch(over, B, horizon, subs, code):
     dims = dict(DIMS, **over)
     mh = abi.model_handle(dims, _la_layers(dims["n_layers"], dims["n_experts"], B))
     st, keep = _state_stub()
-    pol = abi.make_policy(**POL, horizon=horizon)
+    pol = abi.make_policy(**POL, horizon=horizon, la_subs=subs)
     rc = abi.lib().trimmoe_stack_forward(C.byref(mh.model), C.byref(pol), C.byref(st), None,
                                          None, 0, None)
     assert rc == code
