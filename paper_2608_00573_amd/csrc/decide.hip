@@ -197,10 +197,13 @@ __device__ inline float la_tuple(const LaView& v, int j, const int* x, int it, i
   return prob;
 }
 
-// number of candidates in a row of C entries (-1 padded)
-__device__ inline int la_ncand(const int16_t* row, int C) {
+// candidates of a row of C entries (-1 padded, ascending Q) that fit the
+// budget on their own: D + Q <= b.  An option using any other one is
+// infeasible (Q >= 0 only adds), so leaving them out of the enumeration
+// changes no decision, and the options that remain keep their order.
+__device__ inline int la_nfit(const int16_t* row, const float* rq, int C, float D, float b) {
   int n = 0;
-  while (n < C && row[n] >= 0) ++n;
+  while (n < C && row[n] >= 0 && D + rq[n] <= b) ++n;
   return n;
 }
 
@@ -250,7 +253,7 @@ __device__ float la_inner(const LaView& v, int j, const int* tau, float D, float
       ++n_loc;
     } else {
       ++n_rem;
-      const int n = la_ncand(cand + (size_t)e * v.C, v.C);
+      const int n = la_nfit(cand + (size_t)e * v.C, candq + (size_t)e * v.C, v.C, D, b);
       if (n > 0) {
         rs[nsub] = s;
         rad[nsub++] = 1 + n;
@@ -630,14 +633,17 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     t = p.active_idx[pos];
     I = sI[i];
 
-    // resolve slots: local exact, or remote with or without candidates
+    budget = p.budget_tok ? p.budget_tok[t] : p.budget;
+    D = p.d_acc[t];
+    // resolve slots: local exact, or remote with or without candidates that
+    // fit the budget
     for (int r = 0; r < k; ++r) {
       const int e = sS[i][r];
       if (p.local_mask[e]) {
         ++n_loc;
       } else {
         ++n_rem;
-        const int n = la_ncand(cand + (size_t)e * C, C);
+        const int n = la_nfit(cand + (size_t)e * C, candq + (size_t)e * C, C, D, budget);
         if (n > 0) {
           sRsub[i][nsub] = r;
           sRad[i][nsub++] = 1 + n;
@@ -646,8 +652,6 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
       }
     }
     sNsub[i] = nsub;
-    budget = p.budget_tok ? p.budget_tok[t] : p.budget;
-    D = p.d_acc[t];
   }
 
   if constexpr (LA) {
@@ -668,7 +672,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
       // candidate), I <= theta and the budget admits Lambda
       float sq_all = 0.f;
       for (int u = 0; u < nsub; ++u) sq_all += candq[(size_t)sS[i][sRsub[i][u]] * C];
-      const bool all_local = nsub == n_rem && D + sq_all <= budget;
+      const bool all_local = nsub == n_rem && D + sq_all <= budget;  // as the enumeration finds
       const float lam = fminf(1.f, p.skip_slope * I);
       la.skipok[i] = !all_local && I <= p.theta && D + lam <= budget;
     }
