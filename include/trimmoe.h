@@ -73,8 +73,9 @@ extern "C" {
 #define TRIMMOE_MAX_TOPK 8
 /* look-ahead (policy.horizon > 1): H <= 4, top_k <= 4, 1 <= trans_b <= 8,
  * 1 <= la_subs <= 4, and with O = (1 + la_subs)^k + 1 options per token:
- * O * trans_b^k <= 1024 first-level branches per token and
- * O^H * trans_b^(k (H - 1)) <= 2^23 cost evaluations per token */
+ * O * trans_b^k <= 1024 first-level branches per token,
+ * O^H * trans_b^(k (H - 1)) <= 2^23 cost evaluations per token, and the route
+ * block's look-ahead tables within 150 KB of LDS */
 #define TRIMMOE_MAX_HORIZON 4
 #define TRIMMOE_MAX_LOOKAHEAD_TOPK 4
 #define TRIMMOE_MAX_TRANS_B 8
