@@ -553,8 +553,12 @@ __global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
 //     the slice: an LDS-destination DMA of a whole 64 KB slice right after
 //     the barrier asks the texture path for about 128 B/clk per CU against
 //     the ~50 B/clk it sustains, and its stalls land on the MFMA issue;
-//   * two 64 KB stages and one barrier per slice, before the last k-step: it
-//     waits for LDS work only (this slice's reads, the next slice's writes).
+//   * two 64 KB stages and one barrier per slice, in the middle of the last
+//     k-step: it waits for LDS work only (this slice's reads, the next
+//     slice's writes).  The third k-step issues the last 8 writes, one after
+//     each MFMA of its second half, and the last k-step's first 8 MFMAs (which
+//     read no LDS) cover their latency; the next slice's first fragments are
+//     read after the barrier, one after each of the remaining 8 MFMAs.
 // Blocks are persistent and walk their XCD's contiguous tile range as the
 // other core does; each tile runs its own prologue and epilogue.
 namespace big {
@@ -694,7 +698,8 @@ __device__ __forceinline__ void big_put_rt(uint32_t wa, const BigStage& R, int u
 // issued during the previous k-step; newer LDS operations are the NWP writes
 // that followed them there and the min(T, 8) reads of fn issued here), the
 // MFMA, then fn's read T (T < 8), fetch(l0 + ..) after MFMAs 8, 10, 12, 14
-// and put(w0 + ..) after MFMAs 9, 11, 13, 15 (NW of them)
+// and put(w0 + ..) after MFMAs 9, 11, 13, 15 (NW < 8 of them) or after each
+// of MFMAs 8..15 (NW = 8)
 template <int T, bool DUAL, int NWP, int NW, class Fetch, class Put>
 __device__ __forceinline__ void big_slot(Frag8& fc, Frag8& fn, Acc44& acc, uint32_t pa,
                                          uint32_t pb, Fetch& fetch, int l0, Put& put, int w0) {
@@ -716,11 +721,47 @@ __device__ __forceinline__ void big_slot(Frag8& fc, Frag8& fn, Acc44& acc, uint3
     fetch(l0 + (T - 8) / 2);
     sched_fence();
   }
-  if constexpr (T >= 9 && (T & 1) == 1 && (T - 9) / 2 < NW) {
+  if constexpr (NW == 8 && T >= 8) {
+    put(w0 + (T - 8));
+    sched_fence();
+  } else if constexpr (NW < 8 && T >= 9 && (T & 1) == 1 && (T - 9) / 2 < NW) {
     put(w0 + (T - 9) / 2);
     sched_fence();
   }
   if constexpr (T < 15) big_slot<T + 1, DUAL, NWP, NW>(fc, fn, acc, pa, pb, fetch, l0, put, w0);
+}
+
+// Last k-step of a slice: fragments fc were read during the previous k-step,
+// followed by its 8 writes of the next slice.  MFMAs 0..7, then the slice
+// barrier (the writes had those 8 MFMAs to land), then MFMAs 8..15 with the
+// next slice's first fragment reads (from the other stage) after each and
+// fetch(l0 + ..) after 8, 10, 12, 14
+template <int T, bool DUAL, class Fetch>
+__device__ __forceinline__ void big_slot_last(Frag8& fc, Frag8& fn, Acc44& acc, uint32_t pa,
+                                              uint32_t pb, Fetch& fetch, int l0) {
+  if constexpr (T == 0 || T == 1 || T == 4) {
+    constexpr int pair = T == 0 ? 0 : T == 1 ? 1 : 2;
+    lgkm_le<2 * (3 - pair) + 8>();
+    asm volatile("" : "+v"(fc.a[pair]), "+v"(fc.b[pair]));
+    sched_fence();
+  }
+  if constexpr (T == 8) {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    asm volatile("" : "+v"(fc.a[3]), "+v"(fc.b[3]));
+    sched_fence();
+  }
+  constexpr int i = kSqI[T], j = kSqJ[T];
+  acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc.a[i], fc.b[j], acc[i][j], 0, 0, 0);
+  sched_fence();
+  if constexpr (T >= 8) {
+    big_read<DUAL, T - 8>(fn, pa, pb);
+    sched_fence();
+  }
+  if constexpr (T >= 8 && (T & 1) == 0) {
+    fetch(l0 + (T - 8) / 2);
+    sched_fence();
+  }
+  if constexpr (T < 15) big_slot_last<T + 1, DUAL>(fc, fn, acc, pa, pb, fetch, l0);
 }
 
 // One slice from stage H: Rf receives the slice two ahead (rows q, buffers
@@ -735,15 +776,8 @@ __device__ __forceinline__ void big_half(uint32_t s0, const BigRows& q, const Bi
   auto put = [&](int u) { big_put_rt(nxt + w_lane, Rp, u); };
   big_slot<0, DUAL, 0, 4>(f0, f1, acc, cur + a_lane[1], cur + b_lane[1], fetch, 0, put, 0);
   big_slot<0, DUAL, 4, 4>(f1, f0, acc, cur + a_lane[2], cur + b_lane[2], fetch, 4, put, 4);
-  big_slot<0, DUAL, 4, 4>(f0, f1, acc, cur + a_lane[3], cur + b_lane[3], fetch, 8, put, 8);
-  big_put<12>(nxt + w_lane, Rp);
-  big_put<13>(nxt + w_lane, Rp);
-  big_put<14>(nxt + w_lane, Rp);
-  big_put<15>(nxt + w_lane, Rp);
-  // the next slice is in its stage and every wave's reads of this one are done
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  sched_fence();
-  big_slot<0, DUAL, 0, 0>(f1, f0, acc, nxt + a_lane[0], nxt + b_lane[0], fetch, 12, put, 0);
+  big_slot<0, DUAL, 4, 8>(f0, f1, acc, cur + a_lane[3], cur + b_lane[3], fetch, 8, put, 8);
+  big_slot_last<0, DUAL>(f1, f0, acc, nxt + a_lane[0], nxt + b_lane[0], fetch, 12);
 }
 
 // C tile += A rows x B rows over nk slices from the rows' K origin; returns
@@ -757,7 +791,10 @@ __device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Ac
   auto fetch_all = [&](BigStage& R, int kt) {
     const BigSrc src(q, kt, nk);
 #pragma unroll
-    for (int u = 0; u < 16; ++u) big_fetch<DUAL>(R, q, src, u);
+    for (int u = 0; u < 16; ++u) {
+      big_fetch<DUAL>(R, q, src, u);
+      sched_fence();  // issue order = row order, as in the main loop
+    }
   };
   // prologue: slice 0 through R0 into stage 0; slice 1 into R1
   fetch_all(R0, 0);
