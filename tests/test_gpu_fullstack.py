@@ -16,7 +16,9 @@ and each token's confidence xi within the exact shift that the difference
 of the two rounded outputs makes through the exit head (fp32 slack added).
 What holds at any size (Properties 2 and 3, masks, counters) is checked on
 every token.  The Mixtral-shaped weights also serve the first decode steps
-(32 fresh tokens each, p_J = 0.3), every token checked.
+(32 fresh tokens each, p_J = 0.3), every token checked; those four steps form
+one runtime-feedback window (Sec. V-D, V-F) whose GPU sums and host update
+must match the oracle's, and a fifth step runs on the updated policy.
 
 A free-running comparison (each side feeding its own output onward) is not
 used at these depths: bf16 rounding flips of the two sides' hidden states
@@ -83,7 +85,7 @@ def _gpu_stack(mh, policy, h0, N, k, dev):
     tr = abi.TraceBuffers(N, T, k, dev)
     abi.trimmoe_stack_forward(mh.model, policy, st.state, tr.trace, ws)
     torch.cuda.synchronize()
-    return gpu_state_np(st), gpu_trace_np(tr)
+    return gpu_state_np(st), gpu_trace_np(tr), st, tr
 
 
 def _gpu_rows(st, idx):
@@ -114,7 +116,9 @@ class _Run:
         self.label, self.cfg, self.pol, self.idx = label, cfg, pol, idx
         policy = abi.make_policy(**pol)
         log(f"[fullstack] {label}: trimmoe_stack_forward over {h0.shape[0]} tokens")
-        self.ref_state, self.ref_trace = _gpu_stack(mh, policy, h0, N, k, dev)
+        self.ref_state, self.ref_trace, self.dev_state, self.dev_trace = \
+            _gpu_stack(mh, policy, h0, N, k, dev)
+        self.policy = policy
         check_invariants_gpu(cfg, pol, self.ref_state, self.ref_trace)
         _counters_agree(self.ref_trace)
         # the same stack, one layer step at a time, the sampled rows read back
@@ -170,6 +174,47 @@ class _Run:
         self.stats["max_rel_err"] = max(self.stats.get("max_rel_err", 0.0), s["max_rel_err"])
 
 
+# runtime feedback after the decode window (the decode bench's defaults)
+FB_ETA, FB_KAPPA, FB_FLOOR = 0.2, 0.2, 0.1
+KEYS = ("tokens", "exits", "xi_exit", "util", "delay", "delay_ref")
+
+
+def _feedback_window(cfg, inp, mh, runs, dpol):
+    """The window's observations (Sec. V-D, V-F) summed on the GPU over the
+    decode runs against the oracle's sums of the same passes' states and
+    traces, then the library's host update (Eq. (37), Eq. (43)) against the
+    oracle's; returns the updated policy."""
+    N = cfg["n_layers"]
+    stats = torch.zeros(6, dtype=torch.float64, device=runs[0].dev_state.h.device)
+    for r in runs:
+        abi.trimmoe_window_stats(mh.model, r.policy, r.dev_state.state, r.dev_trace.trace, stats)
+    torch.cuda.synchronize()
+    got = stats.cpu().numpy()
+    model = dict(n_layers=N, top_k=cfg["top_k"],
+                 layers={l: dict(local_mask=inp["layers"][l]["local_mask"].cpu().numpy())
+                         for l in range(N)})
+    ref = np.zeros(6)
+    for r in runs:
+        tr = [dict(action=r.ref_trace["action"][l], target=r.ref_trace["target"][l],
+                   kind=r.ref_trace["kind"][l]) for l in range(N)]
+        st = O.window_stats(model, policy32(dpol), r.ref_state, tr)
+        ref += np.array([st[key] for key in KEYS])
+    log(f"[fullstack] feedback window: gpu {got.tolist()} oracle {ref.tolist()}")
+    # counts exactly; the fp64 sums up to their order
+    assert got[0] == ref[0] and got[1] == ref[1]
+    assert np.allclose(got[2:], ref[2:], rtol=1e-12, atol=1e-12)
+    assert got[1] > 0 and got[4] > 0
+    policy = abi.make_policy(**dpol)
+    abi.trimmoe_feedback_update(policy, got.tolist(), FB_ETA, FB_KAPPA, FB_FLOOR)
+    rp, rw = O.feedback_update(policy32(dpol), dict(zip(KEYS, ref.tolist())), FB_ETA, FB_KAPPA,
+                               FB_FLOOR)
+    assert policy.p_exit == pytest.approx(rp, abs=2e-6)
+    assert policy.omega_t == pytest.approx(rw, abs=2e-6)
+    assert (policy.p_exit, policy.omega_t) != (policy32(dpol)["p_exit"],
+                                               policy32(dpol)["omega_t"])
+    return dict(dpol, p_exit=float(policy.p_exit), omega_t=float(policy.omega_t))
+
+
 def _full_stack(name, n_sample, seed, decode_steps=0):
     cfg = workload(name)
     N, T = cfg["n_layers"], cfg["n_tokens"]
@@ -185,6 +230,12 @@ def _full_stack(name, n_sample, seed, decode_steps=0):
         for s in range(decode_steps):
             hd = make_tokens(dcfg, dcfg["token_seed_base"] + s, dev)
             runs.append(_Run(f"decode{s}", dcfg, mh, dpol, hd, np.arange(hd.shape[0]), dev))
+        # the decode steps form one feedback window; the next step runs on
+        # the updated policy
+        dpol = _feedback_window(dcfg, inp, mh, runs[1:], dpol)
+        hd = make_tokens(dcfg, dcfg["token_seed_base"] + decode_steps, dev)
+        runs.append(_Run(f"decode{decode_steps}", dcfg, mh, dpol, hd, np.arange(hd.shape[0]),
+                         dev))
     log(f"[fullstack] {name}: oracle over {N} layers, one layer in fp64 at a time")
     wid = _Widen(inp)
     for l in range(N):
@@ -211,9 +262,10 @@ def test_qwen_full_stack_sampled_tokens():
 def test_mixtral_full_stack_prefill_and_first_decode_steps():
     # 32 layers, 8 experts top-2, Zipf-skewed groups, 8192 tokens (the large-
     # group core, cut down-GEMM tiles); then 4 decode steps of 32 tokens on
-    # the same weights, every token followed
+    # the same weights, every token followed; the 4 steps form one feedback
+    # window, and a fifth step runs on the updated p_J and omega_T
     out, gtr = _full_stack("mixtral_8x7b_prefill", n_sample=24, seed=42, decode_steps=4)
     assert out["prefill"]["compared"] >= 100
     assert gtr["action"][0].min() != O.ACT_INACTIVE
-    for s in range(4):
+    for s in range(5):
         assert out[f"decode{s}"]["compared"] >= 32
