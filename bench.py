@@ -49,6 +49,7 @@ METRIC = "active tokens/s through adaptive-depth MoE stack; grouped-GEMM % MFMA 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_FP32_TFLOPS = 157.3    # MI355X fp32 vector
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+PEAK_CLOCK_MHZ = 2400.0     # engine clock the published MFMA peaks assume
 
 
 def parse():
@@ -464,11 +465,27 @@ def main():
         abi.trimmoe_stack_forward(mh.model, policy, st.state, tr.trace, ws)
         torch.cuda.synchronize()
         work_steps.append(algorithmic_work(cfg, tr.counters.cpu().numpy()))
+    # mean engine clock of each GEMM class: one more pass of the same work
+    # with the library's clock record set (bf16 GEMM kernels only)
+    clock = {}
+    if cfg["dtype"] == "bf16":
+        log("engine-clock pass")
+        rec = torch.zeros(2 * len(classes), dtype=torch.int64, device=dev)
+        st = abi.StateBuffers(batches[0].clone())
+        evict(0)
+        abi.trimmoe_set_clock_record(rec)
+        try:
+            abi.trimmoe_stack_forward(mh.model, policy, st.state, None, ws)
+            torch.cuda.synchronize()
+        finally:
+            abi.trimmoe_set_clock_record(None)
+        clock = abi.clock_mhz(rec)
     # per-step averages, per class and per layer
     flop = {c: sum(w["flop"][c] for ws_ in work_steps for w in ws_) / nb for c in classes}
     byts = {c: sum(w["bytes"][c] for ws_ in work_steps for w in ws_) / nb for c in classes}
 
     peak = PEAK_BF16_TFLOPS if cfg["dtype"] == "bf16" else PEAK_FP32_TFLOPS
+    dev_info = device_info()
     t_class = class_ms.sum(axis=0)  # ms per step per class
     ci = {n: i for i, n in enumerate(classes)}
     launches = {c: N for c in classes}
@@ -527,8 +544,19 @@ def main():
             "avg_launch_ms": t_class[ci[dom]] / launches[dom],
             "algorithmic_flop_per_launch": flop[dom] / launches[dom],
             "algorithmic_bytes_per_launch": byts[dom] / launches[dom],
+            # the same rate against the peak scaled to the engine clock the
+            # kernel ran at (the published peak assumes the peak clock)
+            "clock_mhz": clock.get(dom),
+            "frac_at_clock": (achieved / (pk * clock[dom] / PEAK_CLOCK_MHZ)
+                              if mfma_bound and dom in clock else None),
         },
         "grouped_gemm_mfma_frac": gg_frac,
+        # against the peak at the engine clock the up and down GEMMs ran at
+        # (time-weighted)
+        "grouped_gemm_mfma_frac_at_clock": (
+            gg_frac * PEAK_CLOCK_MHZ * gg_s * 1e3
+            / (t_class[ci["up"]] * clock["up"] + t_class[ci["down"]] * clock["down"])
+            if gg_s and "up" in clock and "down" in clock else None),
         "grouped_gemm_hbm_frac": gg_hbm,
         "class_hbm_frac": {c: (byts[c] / (t_class[ci[c]] * 1e-3) / 1e9 / PEAK_HBM_GBS
                                if t_class[ci[c]] > 0 else 0.0) for c in classes},
@@ -541,7 +569,8 @@ def main():
         "timing": f"median of {K} steps, each between its own HIP events; "
                   + (f"{args.flush_mib} MiB written between steps (outside the events)"
                      if flush is not None else "no cache eviction between steps"),
-        "device": device_info(),
+        "device": dev_info,
+        "sustained_clock_mhz": clock,
         "kernel_ms_per_step": {n: float(t_class[i]) for i, n in enumerate(classes)},
         "per_layer": [{k: w[k] for k in ("n_active", "n_exec", "rows", "distinct")}
                       for w in work_steps[0]],

@@ -47,7 +47,7 @@
 extern "C" {
 #endif
 
-#define TRIMMOE_ABI_VERSION 5
+#define TRIMMOE_ABI_VERSION 6
 
 /* status codes */
 #define TRIMMOE_OK 0
@@ -309,6 +309,22 @@ int trimmoe_stack_forward_timed(const trimmoe_model* m, const trimmoe_policy* p,
                                 void* workspace, size_t workspace_bytes,
                                 void* stream, void* const* events,
                                 int32_t n_events);
+
+/*
+ * Engine-clock record of the GEMM kernels (measurement; no passage of the
+ * method).  While set, each block of a bf16 GEMM launch of class c
+ * (TRIMMOE_CLASS_UP, _DOWN, _SHARED or _EXIT) adds to rec[2 c] the core clock
+ * cycles and to rec[2 c + 1] the ticks of the 100 MHz constant clock that
+ * pass between its start and the end of its last tile (blocks with no tile
+ * add nothing), so 100 MHz * rec[2 c] / rec[2 c + 1] is the mean engine clock
+ * the class ran at.  rec: device memory of 2 * TRIMMOE_TIMED_CLASSES uint64
+ * words on the device of the later launches, zeroed and owned by the caller,
+ * which keeps it allocated while set; NULL stops recording.  The setting is
+ * process-wide and applies to layer steps issued after the call (its
+ * pointer is read when a layer's launches are issued); the work and results
+ * are otherwise identical.  Returns TRIMMOE_OK.
+ */
+int trimmoe_set_clock_record(uint64_t* rec);
 
 
 /*

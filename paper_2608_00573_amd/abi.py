@@ -18,7 +18,7 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libtrimmoe.so")
 
-ABI_VERSION = 5   # TRIMMOE_ABI_VERSION this binding is written for
+ABI_VERSION = 6   # TRIMMOE_ABI_VERSION this binding is written for
 STATIC_SCRATCH_BYTES = 64 << 20  # TRIMMOE_STATIC_SCRATCH_BYTES
 N_COUNTERS = 16   # per-layer trace counters (row stride of trimmoe_trace.counters)
 TRIMMOE_OK = 0
@@ -70,6 +70,7 @@ class Trace(C.Structure):
 EXPORTS = ["trimmoe_abi_version", "trimmoe_status_str", "trimmoe_workspace_size",
            "trimmoe_state_reset", "trimmoe_layer_step", "trimmoe_stack_forward",
            "trimmoe_stack_forward_timed", "trimmoe_stack_forward_static",
+           "trimmoe_set_clock_record",
            "trimmoe_window_stats", "trimmoe_feedback_update",
            "trimmoe_calib_exit_layers", "trimmoe_calib_stats", "trimmoe_calib_transitions",
            "trimmoe_place_replicas", "trimmoe_head_argmax_workspace_size",
@@ -109,6 +110,8 @@ def lib():
                                                   C.POINTER(State), C.POINTER(Trace),
                                                   C.c_void_p, C.c_size_t, C.c_void_p,
                                                   C.POINTER(C.c_void_p), C.c_int32]
+        L.trimmoe_set_clock_record.restype = C.c_int
+        L.trimmoe_set_clock_record.argtypes = [C.c_void_p]
         L.trimmoe_stack_forward_static.restype = C.c_int
         L.trimmoe_stack_forward_static.argtypes = [C.POINTER(Model), C.POINTER(Policy),
                                                    C.POINTER(State), C.POINTER(Trace),
@@ -227,6 +230,22 @@ def trimmoe_stack_forward_timed(model: Model, policy: Policy, state: State, trac
            lib().trimmoe_stack_forward_timed(C.byref(model), C.byref(policy), C.byref(state), tr,
                                              _ptr(workspace), workspace.numel(),
                                              _stream_handle(stream), arr, len(events)))
+
+
+def trimmoe_set_clock_record(rec):
+    """``rec``: an int64 device tensor of 2 * len(TIMED_CLASSES) zeros, or None
+    to stop recording (the caller keeps the tensor alive while it is set)."""
+    if rec is not None:
+        assert rec.is_cuda and rec.dtype == torch.int64 and rec.is_contiguous()
+        assert rec.numel() == 2 * len(TIMED_CLASSES)
+    _check("trimmoe_set_clock_record", lib().trimmoe_set_clock_record(_ptr(rec)))
+
+
+def clock_mhz(rec) -> dict:
+    """Mean engine clock (MHz) per GEMM class from a filled record."""
+    r = rec.cpu().tolist()
+    return {c: 100.0 * r[2 * i] / r[2 * i + 1]
+            for i, c in enumerate(TIMED_CLASSES) if r[2 * i + 1] > 0}
 
 
 def trimmoe_window_stats(model: Model, policy: Policy, state: State, trace,

@@ -13,6 +13,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <mutex>
 
 #include "common.h"
@@ -292,6 +293,11 @@ int check_workspace(const trimmoe_model* m, const trimmoe_state* s, void* ws, si
   return TRIMMOE_OK;
 }
 
+namespace {
+// engine-clock record of later GEMM launches (trimmoe_set_clock_record)
+std::atomic<unsigned long long*> g_clock_rec{nullptr};
+}  // namespace
+
 // ev: NULL, or TRIMMOE_TIMED_CLASSES + 1 events recorded around the classes;
 // fill_layers: trace rows of this many layers from l on get their inactive
 // defaults first (a stack pass fills all of them at layer 0)
@@ -309,6 +315,7 @@ int run_layer(const trimmoe_model* m, int l, const trimmoe_policy* pol, const tr
       ncu <= 0)
     return TRIMMOE_ERR_HIP;
   P.n_cu = ncu;
+  P.clk = g_clock_rec.load(std::memory_order_relaxed);
   const bool bf16 = m->dtype == TRIMMOE_BF16;
   const bool last = l == m->n_layers - 1;
 #define TRIMMOE_TRY(x) \
@@ -427,6 +434,12 @@ int trimmoe_stack_forward(const trimmoe_model* m, const trimmoe_policy* p, trimm
                           trimmoe_trace* trace, void* workspace, size_t workspace_bytes,
                           void* stream) {
   return stack(m, p, s, trace, workspace, workspace_bytes, stream, nullptr, 0);
+}
+
+int trimmoe_set_clock_record(uint64_t* rec) {
+  static_assert(sizeof(uint64_t) == sizeof(unsigned long long), "64-bit record words");
+  g_clock_rec.store(reinterpret_cast<unsigned long long*>(rec), std::memory_order_relaxed);
+  return TRIMMOE_OK;
 }
 
 int trimmoe_stack_forward_timed(const trimmoe_model* m, const trimmoe_policy* p,

@@ -205,6 +205,9 @@ struct LayerParams {
   int n_vtiles;
   int max_tiles;
   int n_cu;            // compute units of the device (persistent grids)
+  // engine-clock record (measurement): [class][2] sums of core cycles and
+  // 100 MHz ticks per GEMM block, or NULL
+  unsigned long long* clk;
 };
 
 // observations of one stack pass for the runtime feedback rules

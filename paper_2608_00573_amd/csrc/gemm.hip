@@ -426,6 +426,21 @@ __device__ __forceinline__ float silu_mul(float g, float u) {
 // the expert-sorted rows, or (dense mode, shared expert) cover the first
 // *dense_rows rows.  A rows are gathered through x_idx (the token whose h
 // row feeds each sorted row) when it is set.
+// Engine-clock record (measurement only): with a record set, a block adds the
+// core clock cycles (s_memtime) and the 100 MHz constant-clock ticks
+// (s_memrealtime) between its start and the end of its work to rec[0] and
+// rec[1]; their ratio is the mean engine clock under the kernel.  The start
+// values are subtracted at once (modulo 2^64) and the end values added at
+// the end, so nothing is held in registers in between.
+__device__ __forceinline__ void clock_mark(unsigned long long* rec, bool start) {
+  if (rec && threadIdx.x == 0) {
+    const unsigned long long t = __builtin_amdgcn_s_memtime();
+    const unsigned long long r = __builtin_amdgcn_s_memrealtime();
+    atomicAdd(rec, start ? 0ull - t : t);
+    atomicAdd(rec + 1, start ? 0ull - r : r);
+  }
+}
+
 struct FfnArgs {
   const bf16_t* X;        // [rows, K], or h [T, K] when x_idx is set
   const int* x_idx;       // row -> source row of X (gather), or NULL
@@ -442,6 +457,7 @@ struct FfnArgs {
   int act;                // up: TRIMMOE_ACT_*
   int* sk_flag;           // large-group down GEMM: per-tile piece words (see SkPlan), or NULL
   float* sk_part;         // ... and the compact partials of pieces 1.. of cut tiles
+  unsigned long long* clk;  // engine-clock record of this class (see clock_mark), or NULL
 };
 
 template <class T, bool UP>
@@ -522,9 +538,11 @@ __global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
   TileSched S;
   int ntiles;
   if (!S.init(n_mt, n_nt, a.n_split, ntiles)) return;
+  clock_mark(a.clk, true);
   const int nk = (a.K / BK) / a.n_split;
   const FfnSrc<T, UP> src{a, S, dense_m1, nk};
   dma_gemm_stream<T>(lds, ntiles, nk, src);
+  clock_mark(a.clk, false);
 }
 
 // ------------------------------------------ large-group expert GEMMs --
@@ -1033,15 +1051,18 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
     TileSched S;
     int ntiles;
     if (!S.init(n_mt, n_nt, a.n_split, ntiles)) return;
+    clock_mark(a.clk, true);
     const int nk = (a.K / BK) / a.n_split;
     for (int jt = 0; jt < ntiles; ++jt) {
       int mt, nt, sp;
       S.decode(jt, mt, nt, sp);
       piece(mt, nt, sp * nk, nk, sp, -1);
     }
+    clock_mark(a.clk, false);
     return;
   }
   const int P = gridDim.x, nk = a.K / BK;
+  clock_mark(a.clk, true);
   const SkPlan plan(n_mt * n_nt, P);
   // whole tiles, in the usual XCD-range order
   TileSched S;
@@ -1069,6 +1090,7 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
     piece(mt, nt, k0, k1 - k0, 0, q == 0 ? -1 : base + q - 1);
     if (q == 0 && tid == 0) a.sk_flag[mt * n_nt + nt] = (base << 4) | plan.s;
   }
+  clock_mark(a.clk, false);
 }
 
 // ----------------------------------------------------------- exit head --
@@ -1084,6 +1106,7 @@ struct ExitArgs {
   const int* n_exec;  // device
   int V, K, n_vtiles;
   float2* partials;   // [n_x, n_vtiles]
+  unsigned long long* clk;  // engine-clock record (see clock_mark), or NULL
 };
 
 using ExitTile = Tile<kExitTileBF16, 128, 1, 4, 2>;
@@ -1254,8 +1277,10 @@ __global__ __launch_bounds__(T::THREADS) void k_exit_mma(ExitArgs a) {
   TileSched S;
   int ntiles;
   if (!S.init(a.n_vtiles, (n_x + T::BN - 1) / T::BN, 1, ntiles)) return;
+  clock_mark(a.clk, true);
   const ExitSrc<T, ARGMAX> src{a, S, n_x, s_part};
   dma_gemm_stream<T>(lds, ntiles, a.K / BK, src);
+  clock_mark(a.clk, false);
 }
 
 // Exit head on the large-group core (large d): 256 vocabulary rows x 256
@@ -1370,6 +1395,7 @@ __global__ __launch_bounds__(big::THREADS) void k_exit_big(ExitArgs a) {
   TileSched S;
   int ntiles;
   if (!S.init(a.n_vtiles, (n_x + big::BN - 1) / big::BN, 1, ntiles)) return;
+  clock_mark(a.clk, true);
   const int nk = a.K / BK;
   const int fr = lane & 31, hi = lane >> 5;
   uint32_t a_lane[4], b_lane[4];
@@ -1395,6 +1421,7 @@ __global__ __launch_bounds__(big::THREADS) void k_exit_big(ExitArgs a) {
     big_tile<false>(lds, q, nk, acc, a_lane, b_lane, w_lane);
     exit_big_epilogue(a, S, n_x, jt, acc, s_part, wm, wn, lane);
   }
+  clock_mark(a.clk, false);
 }
 
 // ------------------------------------------------------------- fp32 path --
@@ -1559,7 +1586,10 @@ static hipError_t ffn_pass(const LayerParams& p, bool bf16, bool up, bool shared
     FfnArgs a{static_cast<const bf16_t*>(X), x_idx, static_cast<const bf16_t*>(w0),
               static_cast<const bf16_t*>(w1), w_stride, K, N, p.tiles, &p.counts[kCntTiles],
               dense, out, p.y_split_stride, n_split, act,
-              (!up && !shared && big) ? p.sk_flag : nullptr, p.sk_part};
+              (!up && !shared && big) ? p.sk_flag : nullptr, p.sk_part,
+              p.clk ? p.clk + 2 * (shared ? TRIMMOE_CLASS_SHARED
+                                          : up ? TRIMMOE_CLASS_UP : TRIMMOE_CLASS_DOWN)
+                    : nullptr};
     if (big) {
       const int big_mt = shared ? cdiv(p.T, kBigBM) : cdiv(p.T * p.k, kBigBM) + p.E;
       if (up && dual)
@@ -1606,7 +1636,8 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st) {
   if (p.T <= 0) return hipSuccess;
   if (bf16) {
     ExitArgs a{static_cast<const bf16_t*>(p.w_exit), static_cast<const bf16_t*>(p.hx), p.b_exit,
-               &p.counts[kCntExec], p.V, p.d, p.n_vtiles, p.partials};
+               &p.counts[kCntExec], p.V, p.d, p.n_vtiles, p.partials,
+               p.clk ? p.clk + 2 * TRIMMOE_CLASS_EXIT : nullptr};
     // persistent: at most one block per CU, none beyond the tile bound
     if (big_exit(true, p.T, p.V, p.d)) {
       const dim3 grid(min(p.n_vtiles * cdiv(p.T, big::BN), p.n_cu));
