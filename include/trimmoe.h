@@ -318,11 +318,13 @@ int trimmoe_stack_forward_timed(const trimmoe_model* m, const trimmoe_policy* p,
  * pass between its start and the end of its last tile (blocks with no tile
  * add nothing), so 100 MHz * rec[2 c] / rec[2 c + 1] is the mean engine clock
  * the class ran at.  rec: device memory of 2 * TRIMMOE_TIMED_CLASSES uint64
- * words on the device of the later launches, zeroed and owned by the caller,
- * which keeps it allocated while set; NULL stops recording.  The setting is
- * process-wide and applies to layer steps issued after the call (its
- * pointer is read when a layer's launches are issued); the work and results
- * are otherwise identical.  Returns TRIMMOE_OK.
+ * words on the current device, zeroed and owned by the caller, which keeps
+ * it allocated while set; NULL stops recording.  The setting is process-wide
+ * and applies to layer steps issued after the call on that device (the
+ * record is read when a layer's launches are issued; launches on other
+ * devices record nothing); the work and results are otherwise identical.
+ * Returns TRIMMOE_OK, or TRIMMOE_ERR_HIP when the current device cannot be
+ * queried.
  */
 int trimmoe_set_clock_record(uint64_t* rec);
 

@@ -13,7 +13,6 @@
 #include <string.h>
 
 #include <algorithm>
-#include <atomic>
 #include <mutex>
 
 #include "common.h"
@@ -294,8 +293,16 @@ int check_workspace(const trimmoe_model* m, const trimmoe_state* s, void* ws, si
 }
 
 namespace {
-// engine-clock record of later GEMM launches (trimmoe_set_clock_record)
-std::atomic<unsigned long long*> g_clock_rec{nullptr};
+// engine-clock record of later GEMM launches (trimmoe_set_clock_record) and
+// the device it lives on: launches on any other device record nothing
+std::mutex g_clock_mu;
+unsigned long long* g_clock_rec = nullptr;
+int g_clock_dev = -1;
+
+unsigned long long* clock_record_for(int dev) {
+  std::lock_guard<std::mutex> lock(g_clock_mu);
+  return dev == g_clock_dev ? g_clock_rec : nullptr;
+}
 }  // namespace
 
 // ev: NULL, or TRIMMOE_TIMED_CLASSES + 1 events recorded around the classes;
@@ -315,7 +322,7 @@ int run_layer(const trimmoe_model* m, int l, const trimmoe_policy* pol, const tr
       ncu <= 0)
     return TRIMMOE_ERR_HIP;
   P.n_cu = ncu;
-  P.clk = g_clock_rec.load(std::memory_order_relaxed);
+  P.clk = clock_record_for(dev);
   const bool bf16 = m->dtype == TRIMMOE_BF16;
   const bool last = l == m->n_layers - 1;
 #define TRIMMOE_TRY(x) \
@@ -438,7 +445,11 @@ int trimmoe_stack_forward(const trimmoe_model* m, const trimmoe_policy* p, trimm
 
 int trimmoe_set_clock_record(uint64_t* rec) {
   static_assert(sizeof(uint64_t) == sizeof(unsigned long long), "64-bit record words");
-  g_clock_rec.store(reinterpret_cast<unsigned long long*>(rec), std::memory_order_relaxed);
+  int dev = -1;
+  if (rec && hipGetDevice(&dev) != hipSuccess) return TRIMMOE_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_clock_mu);
+  g_clock_rec = reinterpret_cast<unsigned long long*>(rec);
+  g_clock_dev = rec ? dev : -1;
   return TRIMMOE_OK;
 }
 
