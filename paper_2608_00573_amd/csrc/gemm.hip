@@ -562,28 +562,35 @@ __global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
 //     in pairs a0 b0 | a1 b1 | a2 b2 | a3 b3 and waits for each pair with a
 //     partial lgkmcnt; the next k-step's 8 reads go out one after each of the
 //     first 8 MFMAs;
-//   * operands are staged through registers two slices ahead: during
-//     slice g each thread's 16 buffer loads (8 A rows, 8 B rows of 16 bytes;
-//     32-bit row offsets, the K position in the scalar offset) fetch slice
-//     g + 2, one after every other MFMA of the second half of each k-step,
-//     and its 16 ds_writes put slice g + 1 (fetched during slice g - 1) into
-//     the other LDS stage.  The global fetch is thereby spread evenly over
-//     the slice: an LDS-destination DMA of a whole 64 KB slice right after
-//     the barrier asks the texture path for about 128 B/clk per CU against
-//     the ~50 B/clk it sustains, and its stalls land on the MFMA issue;
-//   * two 64 KB stages and one barrier per slice, in the middle of the last
-//     k-step: it waits for LDS work only (this slice's reads, the next
-//     slice's writes).  The third k-step issues the last 8 writes, one after
-//     each MFMA of its second half, and the last k-step's first 8 MFMAs (which
-//     read no LDS) cover their latency; the next slice's first fragments are
-//     read after the barrier, one after each of the remaining 8 MFMAs.
+//   * A rows (the gathered activations) are staged through registers two
+//     slices ahead: during slice g each thread's 8 buffer loads (32-bit row
+//     offsets, the K position in the scalar offset) fetch A of slice g + 2,
+//     after MFMAs 8 and 12 of each k-step, and its 8 ds_writes put A of
+//     slice g + 1 (fetched during slice g - 1) into the other of two 32 KB
+//     A stages, after MFMAs 9, 11 and 13 of the first three k-steps;
+//   * B rows (the weights) go straight to LDS: 8 buffer-to-LDS DMAs per
+//     thread (a wavefront's 64 x 16 bytes land at a wave-uniform base)
+//     bring B of slice g + 2 into a ring of three 32 KB B stages, after
+//     MFMAs 10 and 14 of each k-step, so no VGPRs and no ds_write are spent
+//     on them.  Both fetch streams are spread over the slice: an
+//     LDS-destination DMA of a whole 64 KB slice right after the barrier
+//     asks the texture path for about 128 B/clk per CU against the ~50 B/clk
+//     it sustains, and its stalls land on the MFMA issue;
+//   * one barrier per slice, in the middle of the last k-step: it waits for
+//     this slice's reads, the next slice's A writes and its B DMAs (issued a
+//     slice earlier).  The last k-step's first 8 MFMAs read no LDS and cover
+//     the last writes; the next slice's first fragments are read after the
+//     barrier, one after each of the remaining 8 MFMAs.
 // Blocks are persistent and walk their XCD's contiguous tile range as the
 // other core does; each tile runs its own prologue and epilogue.
 namespace big {
 constexpr int BM = 256, BN = 256, THREADS = 256;
 constexpr int RB = 128;                  // bytes of a row segment (64 bf16)
-constexpr int AB = BM * RB;              // A rows of a stage
-constexpr int STAGE = AB + BN * RB;      // 64 KB
+constexpr int AB = BM * RB;              // A rows of a slice (32 KB)
+constexpr int BB = BN * RB;              // B rows of a slice (32 KB)
+constexpr int BS = 3;                    // B stages (DMA ring)
+constexpr int B0 = 2 * AB;               // first B stage, after the two A stages
+constexpr int LDS = 2 * AB + BS * BB;    // 160 KB
 constexpr int RPP = THREADS / 8;         // rows per fetch pass (8 threads per 128-byte row)
 }  // namespace big
 
@@ -646,7 +653,7 @@ constexpr int big_brow(int j) {
 template <bool DUAL, int Q>
 __device__ __forceinline__ void big_read(Frag8& f, uint32_t pa, uint32_t pb) {
   if constexpr (Q & 1)
-    f.b[Q >> 1] = lds_read_at<big::AB + big_brow<DUAL>(Q >> 1) * big::RB>(pb);
+    f.b[Q >> 1] = lds_read_at<big_brow<DUAL>(Q >> 1) * big::RB>(pb);
   else
     f.a[Q >> 1] = lds_read_at<(Q >> 1) * 32 * big::RB>(pa);
 }
@@ -673,22 +680,31 @@ struct BigSrc {
   }
 };
 
-// registers holding one slice of a thread's 16 rows
+// registers holding one slice of a thread's 8 A rows
 struct BigStage {
-  u32x4_t r[16];
+  u32x4_t r[8];
 };
 
-template <bool DUAL>
 __device__ __forceinline__ void big_fetch(BigStage& R, const BigRows& q, const BigSrc& b, int u) {
-  const __amdgpu_buffer_rsrc_t& rs = u < 8 ? b.ra : (DUAL && u >= 12 ? b.rb1 : b.rb0);
-  R.r[u] = buf_load16(rs, q.off[u], b.ko);
+  R.r[u] = buf_load16(b.ra, q.off[u], b.ko);
 }
 
-// row u of the thread into its stage: A rows at u * 32 rows, B rows after
-// the A half (the thread's LDS address wa carries its row r0 and chunk slot)
+// B row group u (0..7) of the wave straight into B stage `bst` (LDS address):
+// lane l lands at bst + (8 w + 32 u) * 128 + 16 l, which is row 8 w + 32 u +
+// l / 8, chunk slot l % 8 (the thread's fetch chunk is the swizzled one)
+template <bool DUAL>
+__device__ __forceinline__ void big_dma(uint32_t bst, int wave, const BigRows& q, const BigSrc& b,
+                                        int u) {
+  const __amdgpu_buffer_rsrc_t& rs = DUAL && u >= 4 ? b.rb1 : b.rb0;
+  const uint32_t dst = bst + (uint32_t)((8 * wave + big::RPP * u) * big::RB);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_char*)(uintptr_t)dst, 16, q.off[8 + u], b.ko, 0,
+                                           0);
+}
+
+// A row u of the thread into A stage `wa` (its row r0 and chunk slot folded in)
 template <int U>
 __device__ __forceinline__ void big_put(uint32_t wa, const BigStage& R) {
-  lds_write_at<(U < 8 ? U * big::RPP * big::RB : big::AB + (U - 8) * big::RPP * big::RB)>(wa, R.r[U]);
+  lds_write_at<U * big::RPP * big::RB>(wa, R.r[U]);
 }
 
 __device__ __forceinline__ void big_put_rt(uint32_t wa, const BigStage& R, int u) {
@@ -700,27 +716,20 @@ __device__ __forceinline__ void big_put_rt(uint32_t wa, const BigStage& R, int u
     case 4: big_put<4>(wa, R); break;
     case 5: big_put<5>(wa, R); break;
     case 6: big_put<6>(wa, R); break;
-    case 7: big_put<7>(wa, R); break;
-    case 8: big_put<8>(wa, R); break;
-    case 9: big_put<9>(wa, R); break;
-    case 10: big_put<10>(wa, R); break;
-    case 11: big_put<11>(wa, R); break;
-    case 12: big_put<12>(wa, R); break;
-    case 13: big_put<13>(wa, R); break;
-    case 14: big_put<14>(wa, R); break;
-    default: big_put<15>(wa, R); break;
+    default: big_put<7>(wa, R); break;
   }
 }
 
 // MFMA slot T of a k-step: the wait for its fragment pair (fc's reads were
 // issued during the previous k-step; newer LDS operations are the NWP writes
 // that followed them there and the min(T, 8) reads of fn issued here), the
-// MFMA, then fn's read T (T < 8), fetch(l0 + ..) after MFMAs 8, 10, 12, 14
-// and put(w0 + ..) after MFMAs 9, 11, 13, 15 (NW < 8 of them) or after each
-// of MFMAs 8..15 (NW = 8)
-template <int T, bool DUAL, int NWP, int NW, class Fetch, class Put>
+// MFMA, then fn's read T (T < 8); A fetch(l0 + ..) after MFMAs 8 and 12, B
+// dma(l0 + ..) after MFMAs 10 and 14, and put(w0 + ..) after MFMAs 9, 11, 13
+// (NW of them)
+template <int T, bool DUAL, int NWP, int NW, class Fetch, class Dma, class Put>
 __device__ __forceinline__ void big_slot(Frag8& fc, Frag8& fn, Acc44& acc, uint32_t pa,
-                                         uint32_t pb, Fetch& fetch, int l0, Put& put, int w0) {
+                                         uint32_t pb, Fetch& fetch, Dma& dma, int l0, Put& put,
+                                         int w0) {
   if constexpr (T == 0 || T == 1 || T == 4 || T == 9) {
     constexpr int pair = T == 0 ? 0 : T == 1 ? 1 : T == 4 ? 2 : 3;
     constexpr int newer = NWP + (T < 8 ? T : 8);
@@ -735,36 +744,39 @@ __device__ __forceinline__ void big_slot(Frag8& fc, Frag8& fn, Acc44& acc, uint3
     big_read<DUAL, T>(fn, pa, pb);
     sched_fence();
   }
-  if constexpr (T >= 8 && (T & 1) == 0) {
-    fetch(l0 + (T - 8) / 2);
+  if constexpr (T == 8 || T == 12) {
+    fetch(l0 + (T - 8) / 4);
     sched_fence();
   }
-  if constexpr (NW == 8 && T >= 8) {
-    put(w0 + (T - 8));
+  if constexpr (T == 10 || T == 14) {
+    dma(l0 + (T - 10) / 4);
     sched_fence();
-  } else if constexpr (NW < 8 && T >= 9 && (T & 1) == 1 && (T - 9) / 2 < NW) {
+  }
+  if constexpr ((T == 9 || T == 11 || T == 13) && (T - 9) / 2 < NW) {
     put(w0 + (T - 9) / 2);
     sched_fence();
   }
-  if constexpr (T < 15) big_slot<T + 1, DUAL, NWP, NW>(fc, fn, acc, pa, pb, fetch, l0, put, w0);
+  if constexpr (T < 15)
+    big_slot<T + 1, DUAL, NWP, NW>(fc, fn, acc, pa, pb, fetch, dma, l0, put, w0);
 }
 
-// Last k-step of a slice: fragments fc were read during the previous k-step,
-// followed by its 8 writes of the next slice.  MFMAs 0..7, then the slice
-// barrier (the writes had those 8 MFMAs to land), then MFMAs 8..15 with the
-// next slice's first fragment reads (from the other stage) after each and
-// fetch(l0 + ..) after 8, 10, 12, 14
-template <int T, bool DUAL, class Fetch>
+// Last k-step of a slice: MFMAs 0..7 on fragments read in the previous
+// k-step (whose 2 writes followed them), then the slice barrier, then MFMAs
+// 8..15 with the next slice's first fragment reads after each and the last
+// fetch / DMA of the slice.  The barrier waits for this wave's DMAs of the
+// next slice: in issue order they are followed by at most VM newer
+// vector-memory operations (this slice's fetches and DMAs so far).
+template <int T, bool DUAL, int VM, class Fetch, class Dma>
 __device__ __forceinline__ void big_slot_last(Frag8& fc, Frag8& fn, Acc44& acc, uint32_t pa,
-                                              uint32_t pb, Fetch& fetch, int l0) {
+                                              uint32_t pb, Fetch& fetch, Dma& dma, int l0) {
   if constexpr (T == 0 || T == 1 || T == 4) {
     constexpr int pair = T == 0 ? 0 : T == 1 ? 1 : 2;
-    lgkm_le<2 * (3 - pair) + 8>();
+    lgkm_le<2 * (3 - pair) + 2>();
     asm volatile("" : "+v"(fc.a[pair]), "+v"(fc.b[pair]));
     sched_fence();
   }
   if constexpr (T == 8) {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(VM) : "memory");
     asm volatile("" : "+v"(fc.a[3]), "+v"(fc.b[3]));
     sched_fence();
   }
@@ -775,27 +787,47 @@ __device__ __forceinline__ void big_slot_last(Frag8& fc, Frag8& fn, Acc44& acc, 
     big_read<DUAL, T - 8>(fn, pa, pb);
     sched_fence();
   }
-  if constexpr (T >= 8 && (T & 1) == 0) {
-    fetch(l0 + (T - 8) / 2);
+  if constexpr (T == 8 || T == 12) {
+    fetch(l0 + (T - 8) / 4);
     sched_fence();
   }
-  if constexpr (T < 15) big_slot_last<T + 1, DUAL>(fc, fn, acc, pa, pb, fetch, l0);
+  if constexpr (T == 10 || T == 14) {
+    dma(l0 + (T - 10) / 4);
+    sched_fence();
+  }
+  if constexpr (T < 15) big_slot_last<T + 1, DUAL, VM>(fc, fn, acc, pa, pb, fetch, dma, l0);
 }
 
-// One slice from stage H: Rf receives the slice two ahead (rows q, buffers
-// and K position src), Rp holds the next slice, which goes to the other stage
+// LDS of the large-group core: A stages at s0 and s0 + AB (slice parity), B
+// stages at s0 + B0 + BB * (slice mod 3)
+struct BigLds {
+  uint32_t s0;
+  __device__ __forceinline__ uint32_t a(int g) const { return s0 + (g & 1) * big::AB; }
+  __device__ __forceinline__ uint32_t b(int g) const { return s0 + big::B0 + (g % 3) * big::BB; }
+};
+
+// One slice g from A stage H = g & 1 and B stage g mod 3: Rf receives A of
+// slice g + 2 (src), B of slice g + 2 is DMAed into B stage (g + 2) mod 3
+// (free: its last reader was slice g - 1, before that slice's barrier), and
+// Rp (A of slice g + 1) goes to the other A stage.  8 fetches, 8 DMAs and 8
+// writes per thread; the writes go out in the first three k-steps (3, 3, 2)
+// and the barrier in the last k-step waits for the DMAs of slice g + 1
+// (issued during slice g - 1, followed by this slice's 12 fetches and DMAs
+// of its first three k-steps).
 template <bool DUAL, int H>
-__device__ __forceinline__ void big_half(uint32_t s0, const BigRows& q, const BigSrc& src,
-                                         Acc44& acc, const uint32_t (&a_lane)[4],
+__device__ __forceinline__ void big_half(const BigLds& L, int g, int wave, const BigRows& q,
+                                         const BigSrc& src, Acc44& acc,
+                                         const uint32_t (&a_lane)[4],
                                          const uint32_t (&b_lane)[4], uint32_t w_lane, Frag8& f0,
                                          Frag8& f1, BigStage& Rf, BigStage& Rp) {
-  const uint32_t cur = s0 + H * big::STAGE, nxt = s0 + (H ^ 1) * big::STAGE;
-  auto fetch = [&](int u) { big_fetch<DUAL>(Rf, q, src, u); };
-  auto put = [&](int u) { big_put_rt(nxt + w_lane, Rp, u); };
-  big_slot<0, DUAL, 0, 4>(f0, f1, acc, cur + a_lane[1], cur + b_lane[1], fetch, 0, put, 0);
-  big_slot<0, DUAL, 4, 4>(f1, f0, acc, cur + a_lane[2], cur + b_lane[2], fetch, 4, put, 4);
-  big_slot<0, DUAL, 4, 8>(f0, f1, acc, cur + a_lane[3], cur + b_lane[3], fetch, 8, put, 8);
-  big_slot_last<0, DUAL>(f1, f0, acc, nxt + a_lane[0], nxt + b_lane[0], fetch, 12);
+  const uint32_t ca = L.a(g), cb = L.b(g), na = L.a(g + 1), nb = L.b(g + 1), db = L.b(g + 2);
+  auto fetch = [&](int u) { big_fetch(Rf, q, src, u); };
+  auto dma = [&](int u) { big_dma<DUAL>(db, wave, q, src, u); };
+  auto put = [&](int u) { big_put_rt(na + w_lane, Rp, u); };
+  big_slot<0, DUAL, 0, 3>(f0, f1, acc, ca + a_lane[1], cb + b_lane[1], fetch, dma, 0, put, 0);
+  big_slot<0, DUAL, 3, 3>(f1, f0, acc, ca + a_lane[2], cb + b_lane[2], fetch, dma, 2, put, 3);
+  big_slot<0, DUAL, 3, 2>(f0, f1, acc, ca + a_lane[3], cb + b_lane[3], fetch, dma, 4, put, 6);
+  big_slot_last<0, DUAL, 12>(f1, f0, acc, na + a_lane[0], nb + b_lane[0], fetch, dma, 6);
 }
 
 // C tile += A rows x B rows over nk slices from the rows' K origin; returns
@@ -804,36 +836,55 @@ template <bool DUAL>
 __device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Acc44& acc,
                                          const uint32_t (&a_lane)[4], const uint32_t (&b_lane)[4],
                                          uint32_t w_lane) {
-  const uint32_t s0 = lds_addr(lds);
+  const BigLds L{lds_addr(lds)};
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   BigStage R0, R1;
-  auto fetch_all = [&](BigStage& R, int kt) {
-    const BigSrc src(q, kt, nk);
+  // prologue: A of slice 0 to R0, B of slice 0 to B stage 0, A of slice 1
+  // to R1, B of slice 1 to B stage 1; R0 into A stage 0
+  {
+    const BigSrc s0(q, 0, nk), s1(q, 1, nk);
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      big_fetch<DUAL>(R, q, src, u);
-      sched_fence();  // issue order = row order, as in the main loop
+    for (int u = 0; u < 8; ++u) {
+      big_fetch(R0, q, s0, u);
+      sched_fence();
     }
-  };
-  // prologue: slice 0 through R0 into stage 0; slice 1 into R1
-  fetch_all(R0, 0);
-  fetch_all(R1, 1);
 #pragma unroll
-  for (int u = 0; u < 16; ++u) big_put_rt(s0 + w_lane, R0, u);
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    for (int u = 0; u < 8; ++u) {
+      big_dma<DUAL>(L.b(0), wave, q, s0, u);
+      sched_fence();
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      big_fetch(R1, q, s1, u);
+      sched_fence();
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      big_dma<DUAL>(L.b(1), wave, q, s1, u);
+      sched_fence();
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < 8; ++u) big_put_rt(L.a(0) + w_lane, R0, u);
+  // B of slice 0 has landed (16 newer operations: A and B of slice 1)
+  asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
   Frag8 f0, f1;
-  big_read<DUAL, 0>(f0, s0 + a_lane[0], s0 + b_lane[0]);
-  big_read<DUAL, 1>(f0, s0 + a_lane[0], s0 + b_lane[0]);
-  big_read<DUAL, 2>(f0, s0 + a_lane[0], s0 + b_lane[0]);
-  big_read<DUAL, 3>(f0, s0 + a_lane[0], s0 + b_lane[0]);
-  big_read<DUAL, 4>(f0, s0 + a_lane[0], s0 + b_lane[0]);
-  big_read<DUAL, 5>(f0, s0 + a_lane[0], s0 + b_lane[0]);
-  big_read<DUAL, 6>(f0, s0 + a_lane[0], s0 + b_lane[0]);
-  big_read<DUAL, 7>(f0, s0 + a_lane[0], s0 + b_lane[0]);
-  // two slices per trip (R0 and R1 swap roles with the stages); for an odd
-  // count the last trip's second slice is the zero slice past the end
+  const uint32_t pa = L.a(0) + a_lane[0], pb = L.b(0) + b_lane[0];
+  big_read<DUAL, 0>(f0, pa, pb);
+  big_read<DUAL, 1>(f0, pa, pb);
+  big_read<DUAL, 2>(f0, pa, pb);
+  big_read<DUAL, 3>(f0, pa, pb);
+  big_read<DUAL, 4>(f0, pa, pb);
+  big_read<DUAL, 5>(f0, pa, pb);
+  big_read<DUAL, 6>(f0, pa, pb);
+  big_read<DUAL, 7>(f0, pa, pb);
+  // two slices per trip (R0 and R1 swap roles); for an odd count the last
+  // trip's second slice is the zero slice past the end
   for (int g = 0; g < nk; g += 2) {
-    big_half<DUAL, 0>(s0, q, BigSrc(q, g + 2, nk), acc, a_lane, b_lane, w_lane, f0, f1, R0, R1);
-    big_half<DUAL, 1>(s0, q, BigSrc(q, g + 3, nk), acc, a_lane, b_lane, w_lane, f0, f1, R1, R0);
+    big_half<DUAL, 0>(L, g, wave, q, BigSrc(q, g + 2, nk), acc, a_lane, b_lane, w_lane, f0, f1,
+                      R0, R1);
+    big_half<DUAL, 1>(L, g + 1, wave, q, BigSrc(q, g + 3, nk), acc, a_lane, b_lane, w_lane, f0,
+                      f1, R1, R0);
   }
   // the zero slices fetched past the end drain before the registers and
   // stages are reused
@@ -858,7 +909,7 @@ __device__ __forceinline__ void big_store_act(char* lds, const FfnArgs& a, Acc44
   constexpr bool DUAL = MODE == 0;
   constexpr int NT = DUAL ? 128 : 256;      // output columns of the tile
   constexpr int RS = NT * 2 + (DUAL ? 16 : 0);  // LDS bytes per row (padded when it fits)
-  static_assert(256 * RS <= 2 * big::STAGE, "activation tile fits the two stages");
+  static_assert(256 * RS <= big::LDS, "activation tile fits the stages");
   const int c = lane & 31, hi = lane >> 5;
   const bool odd = c & 1;
 #pragma unroll
@@ -973,7 +1024,7 @@ template <int MODE>
 __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
   constexpr bool DUAL = MODE == 0;
   constexpr int NT = DUAL ? 128 : 256;  // output columns per tile
-  __shared__ __align__(16) char lds[2 * big::STAGE];
+  __shared__ __align__(16) char lds[big::LDS];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
@@ -1386,8 +1437,11 @@ __device__ __forceinline__ void exit_big_epilogue(const ExitArgs& a, const TileS
 }
 
 __global__ __launch_bounds__(big::THREADS) void k_exit_big(ExitArgs a) {
-  __shared__ __align__(16) char lds[2 * big::STAGE];
-  __shared__ float2 s_part[2][big::BN];  // per row half: (max y, sum) per token column
+  __shared__ __align__(16) char lds[big::LDS];
+  // per row half: (max y, sum) per token column, in the last B stage (free
+  // while the epilogue runs; the next tile writes it only after its first
+  // slice barrier)
+  float2(*s_part)[big::BN] = reinterpret_cast<float2(*)[big::BN]>(lds + big::B0 + 2 * big::BB);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
