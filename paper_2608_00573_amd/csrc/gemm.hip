@@ -23,7 +23,7 @@
 //
 // Large expert groups, the dense shared expert of large batches and the exit
 // head of wide models run on a second bf16 core (4 wavefronts, 256 x 256
-// tiles, operands staged through registers; described with its kernels).
+// tiles in v_mfma_f32_16x16x32_bf16; described with its kernels).
 //
 // fp32 path: plain FMA kernels for fp32 models.
 #include <math.h>
@@ -548,39 +548,39 @@ __global__ __launch_bounds__(T::THREADS) void k_ffn_mma(FfnArgs a) {
 // ------------------------------------------ large-group expert GEMMs --
 // Expert groups of prefill batches (about a thousand rows or more per expert),
 // the dense shared expert of large batches and the exit head of wide models
-// (k_exit_big, below) use a second core with
-// 256 x 256 block tiles and 4 wavefronts, one per SIMD, each owning a
-// 128 x 128 output patch (16 accumulators of 32 x 32, held in AGPRs).  A
-// k-step then reads 8 fragments for 16 MFMAs (half the LDS bytes per MFMA of
-// the 64 x 64 patches) and a 64-wide K slice moves 64 KB for 256 x 256
-// outputs (2/3 of the bytes per MFMA of the 128 x 256 block).  With one
-// wavefront per SIMD no other wavefront fills the MFMA pipe while this one
-// waits, so the instruction stream is laid out explicitly (sched_barrier
-// keeps the compiler from regrouping it):
-//   * a k-step issues its 16 MFMAs in growing-square order (tile (i, j)
-//     after every tile with a smaller max(i, j)), so it needs its fragments
-//     in pairs a0 b0 | a1 b1 | a2 b2 | a3 b3 and waits for each pair with a
-//     partial lgkmcnt; the next k-step's 8 reads go out one after each of the
-//     first 8 MFMAs;
-//   * A rows (the gathered activations) are staged through registers two
-//     slices ahead: during slice g each thread's 8 buffer loads (32-bit row
-//     offsets, the K position in the scalar offset) fetch A of slice g + 2,
-//     after MFMAs 8 and 12 of each k-step, and its 8 ds_writes put A of
-//     slice g + 1 (fetched during slice g - 1) into the other of two 32 KB
-//     A stages, after MFMAs 9, 11 and 13 of the first three k-steps;
-//   * B rows (the weights) go straight to LDS: 8 buffer-to-LDS DMAs per
-//     thread (a wavefront's 64 x 16 bytes land at a wave-uniform base)
-//     bring B of slice g + 2 into a ring of three 32 KB B stages, after
-//     MFMAs 10 and 14 of each k-step, so no VGPRs and no ds_write are spent
-//     on them.  Both fetch streams are spread over the slice: an
-//     LDS-destination DMA of a whole 64 KB slice right after the barrier
-//     asks the texture path for about 128 B/clk per CU against the ~50 B/clk
-//     it sustains, and its stalls land on the MFMA issue;
-//   * one barrier per slice, in the middle of the last k-step: it waits for
-//     this slice's reads, the next slice's A writes and its B DMAs (issued a
-//     slice earlier).  The last k-step's first 8 MFMAs read no LDS and cover
-//     the last writes; the next slice's first fragments are read after the
-//     barrier, one after each of the remaining 8 MFMAs.
+// (k_exit_big, below) use a second core with 256 x 256 block tiles and 4
+// wavefronts, one per SIMD, each owning a 128 x 128 output patch: 8 x 8
+// accumulators of 16 x 16 in AGPRs, multiplied in v_mfma_f32_16x16x32_bf16.
+// A k-step of 32 reads 16 fragments for 64 MFMAs (half the LDS bytes per
+// MFMA of the 64 x 64 patches) and a 64-wide K slice moves 64 KB for
+// 256 x 256 outputs (2/3 of the bytes per MFMA of the 128 x 256 block).  The
+// chip does not hold its peak clock under a dense MFMA load, and the
+// 16 x 16 x 32 form keeps a higher one than 32 x 32 x 16 at nearly the same
+// share of the cycles (a loop of MFMAs alone: about 2.1 GHz against 1.8),
+// which is why this core uses it.  With one wavefront per SIMD no other
+// wavefront fills the MFMA pipe while this one waits, so the instruction
+// stream is laid out explicitly (sched_barrier keeps the compiler from
+// regrouping it; the MFMAs are inline asm on AGPR operands, so the register
+// allocator cannot move accumulators inside the loop):
+//   * a k-step issues its 64 MFMAs row by row (tile (i, j) = (T / 8, T % 8)).
+//     The next k-step's B fragments go to a second register set, read one
+//     after each of the first 8 MFMAs; its a_i replaces this k-step's a_i
+//     right after that fragment's last MFMA (8 i + 7), so A needs one set.
+//     Each MFMA waits for its own fragments with a partial lgkmcnt;
+//   * both operands go straight to LDS through buffer-to-LDS DMAs (a
+//     wavefront's 64 x 16 bytes land at a wave-uniform base; 32-bit row
+//     offsets, the K position in the scalar offset), so no VGPRs and no
+//     ds_write are spent on them.  A (the gathered activations) has two
+//     32 KB stages and B (the weights) a ring of three.  During slice g the
+//     first k-step brings the second half of A of slice g + 1, the last
+//     k-step (after the barrier, into the A stage slice g leaves) the first
+//     half of A of slice g + 2, and both bring B of slice g + 2: 16 DMAs per
+//     thread spread over the slice, since a DMA of a whole 64 KB slice at
+//     once asks the texture path for about 128 B/clk per CU against the
+//     ~50 B/clk it sustains, and its stalls land on the MFMA issue;
+//   * one barrier per slice, before MFMA 32 of the last k-step: it waits for
+//     this slice's reads and every DMA of slice g + 1, and the next slice's
+//     first fragments are read after it, one after each following MFMA.
 // Blocks are persistent and walk their XCD's contiguous tile range as the
 // other core does; each tile runs its own prologue and epilogue.
 namespace big {
@@ -594,10 +594,18 @@ constexpr int LDS = 2 * AB + BS * BB;    // 160 KB
 constexpr int RPP = THREADS / 8;         // rows per fetch pass (8 threads per 128-byte row)
 }  // namespace big
 
-struct Frag8 {
-  bf16x8_t a[4], b[4];
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// a wavefront's fragments of one 32-wide k-step: A rows +16 i, B columns +16 j
+struct FragA {
+  bf16x8_t a[8];
 };
-using Acc44 = f32x16_t[4][4];
+struct FragB {
+  bf16x8_t b[8];
+};
+// its 128 x 128 patch: 8 x 8 accumulators of 16 x 16 (lane: column l % 16,
+// rows 4 (l / 16) .. + 4)
+using AccBig = f32x4_t[8][8];
 
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 
@@ -627,35 +635,41 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc_empty(const void* p) 
 
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
-// 16 bytes per lane from a buffer at voff + soff into registers
-__device__ __forceinline__ u32x4_t buf_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
-}
-
-// 16 bytes per lane to LDS at a + OFF
-template <int OFF>
-__device__ __forceinline__ void lds_write_at(uint32_t a, const u32x4_t& v) {
-  asm volatile("ds_write_b128 %0, %1 offset:%2" ::"v"(a), "v"(v), "n"(OFF));
-}
-
-// k-step MFMA order and the fragment pairs it waits for
-constexpr int kSqI[16] = {0, 0, 1, 1, 0, 1, 2, 2, 2, 0, 1, 2, 3, 3, 3, 3};
-constexpr int kSqJ[16] = {0, 1, 0, 1, 2, 2, 0, 1, 2, 3, 3, 3, 0, 1, 2, 3};
+// A 32-wide k-step issues its 64 MFMAs row by row (tile (i, j) = (T / 8,
+// T % 8)): a_i is last used by MFMA 8 i + 7, so the next k-step's a_i is read
+// into the same registers right after it, while the b fragments alternate
+// between two sets.  Per MFMA slot T: the lgkmcnt wait before it (-1: none;
+// the value counts the LDS reads issued after the ones it needs, capped at
+// the counter's 15, which only waits longer), and the fragment reads after it
+// (q = 2 n for a_n, 2 n + 1 for b_n; -1: none), for the first k-step of a
+// slice (0) and the last (1: its reads, of the next slice, follow the slice
+// barrier before MFMA 32).  The first k-step waits on the last k-step's
+// read order and the last k-step on the first's.
+constexpr int kWait0[64] = {14, 13, 12, 11, 10, 10, 10, 10, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, 15, -1, -1, -1, -1, -1, -1, -1, 15, -1, -1, -1, -1, -1, -1, -1, 15, -1, -1, -1, -1, -1, -1, -1};
+constexpr int kWait1[64] = {7, -1, -1, -1, -1, -1, -1, -1, 6, -1, -1, -1, -1, -1, -1, -1, 5, -1, -1, -1, -1, -1, -1, -1, 4, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1};
+constexpr int kRead0a[64] = {1, 3, 5, 7, 9, 11, 13, 15, -1, -1, -1, -1, -1, -1, -1, 2, -1, -1, -1, -1, -1, -1, -1, 4, -1, -1, -1, -1, -1, -1, -1, 6, -1, -1, -1, -1, -1, -1, -1, 8, -1, -1, -1, -1, -1, -1, -1, 10, -1, -1, -1, -1, -1, -1, -1, 12, -1, -1, -1, -1, -1, -1, -1, 14};
+constexpr int kRead0b[64] = {-1, -1, -1, -1, -1, -1, -1, 0, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1};
+constexpr int kRead1a[64] = {-1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, -1, 11, -1, 13, -1, 15, 10, -1, -1, -1, -1, -1, -1, -1, 12, -1, -1, -1, -1, -1, -1, 14};
+constexpr int kRead1b[64] = {-1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1};
 
 // B fragment j of a wavefront: LDS row offset from its first B row.  DUAL:
-// columns j = 0, 1 of the up operand (rows 0..127 of the stage's B half),
-// j = 2, 3 the same columns of the gate operand (rows 128..255).
+// columns j = 0..3 of the up operand (rows 0..127 of the B stage), j = 4..7
+// the same columns of the gate operand (rows 128..255).
 template <bool DUAL>
 constexpr int big_brow(int j) {
-  return DUAL ? (j < 2 ? 32 * j : 128 + 32 * (j - 2)) : 32 * j;
+  return DUAL ? (j < 4 ? 16 * j : 128 + 16 * (j - 4)) : 16 * j;
 }
 
+// fragment read Q of a k-step: a_{Q/2} for even Q, b_{Q/2} for odd Q
 template <bool DUAL, int Q>
-__device__ __forceinline__ void big_read(Frag8& f, uint32_t pa, uint32_t pb) {
-  if constexpr (Q & 1)
-    f.b[Q >> 1] = lds_read_at<big_brow<DUAL>(Q >> 1) * big::RB>(pb);
-  else
-    f.a[Q >> 1] = lds_read_at<(Q >> 1) * 32 * big::RB>(pa);
+__device__ __forceinline__ void big_read(FragA& fa, FragB& fb, uint32_t pa, uint32_t pb) {
+  if constexpr (Q >= 0) {
+    if constexpr (Q & 1)
+      fb.b[Q >> 1] = lds_read_at<big_brow<DUAL>(Q >> 1) * big::RB>(pb);
+    else
+      fa.a[Q >> 1] = lds_read_at<(Q >> 1) * 16 * big::RB>(pa);
+    sched_fence();
+  }
 }
 
 // Per-thread operand rows of one tile: row u < 8 is A row r0 + 32 u (gathered,
@@ -680,15 +694,6 @@ struct BigSrc {
   }
 };
 
-// registers holding one slice of a thread's 8 A rows
-struct BigStage {
-  u32x4_t r[8];
-};
-
-__device__ __forceinline__ void big_fetch(BigStage& R, const BigRows& q, const BigSrc& b, int u) {
-  R.r[u] = buf_load16(b.ra, q.off[u], b.ko);
-}
-
 // B row group u (0..7) of the wave straight into B stage `bst` (LDS address):
 // lane l lands at bst + (8 w + 32 u) * 128 + 16 l, which is row 8 w + 32 u +
 // l / 8, chunk slot l % 8 (the thread's fetch chunk is the swizzled one)
@@ -701,101 +706,59 @@ __device__ __forceinline__ void big_dma(uint32_t bst, int wave, const BigRows& q
                                            0);
 }
 
-// A row u of the thread into A stage `wa` (its row r0 and chunk slot folded in)
-template <int U>
-__device__ __forceinline__ void big_put(uint32_t wa, const BigStage& R) {
-  lds_write_at<U * big::RPP * big::RB>(wa, R.r[U]);
+// A row group u (0..7) of the wave straight into A stage `ast`
+__device__ __forceinline__ void big_dma_a(uint32_t ast, int wave, const BigRows& q, const BigSrc& b,
+                                          int u) {
+  const uint32_t dst = ast + (uint32_t)((8 * wave + big::RPP * u) * big::RB);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(b.ra, (lds_char*)(uintptr_t)dst, 16, q.off[u], b.ko, 0, 0);
 }
 
-__device__ __forceinline__ void big_put_rt(uint32_t wa, const BigStage& R, int u) {
-  switch (u) {
-    case 0: big_put<0>(wa, R); break;
-    case 1: big_put<1>(wa, R); break;
-    case 2: big_put<2>(wa, R); break;
-    case 3: big_put<3>(wa, R); break;
-    case 4: big_put<4>(wa, R); break;
-    case 5: big_put<5>(wa, R); break;
-    case 6: big_put<6>(wa, R); break;
-    default: big_put<7>(wa, R); break;
-  }
-}
-
-// MFMA slot T of a k-step: the wait for its fragment pair (fc's reads were
-// issued during the previous k-step; newer LDS operations are the NWP writes
-// that followed them there and the min(T, 8) reads of fn issued here), the
-// MFMA, then fn's read T (T < 8); A fetch(l0 + ..) after MFMAs 8 and 12, B
-// dma(l0 + ..) after MFMAs 10 and 14, and put(w0 + ..) after MFMAs 9, 11, 13
-// (NW of them)
-template <int T, bool DUAL, int NWP, int NW, class Fetch, class Dma, class Put>
-__device__ __forceinline__ void big_slot(Frag8& fc, Frag8& fn, Acc44& acc, uint32_t pa,
-                                         uint32_t pb, Fetch& fetch, Dma& dma, int l0, Put& put,
-                                         int w0) {
-  if constexpr (T == 0 || T == 1 || T == 4 || T == 9) {
-    constexpr int pair = T == 0 ? 0 : T == 1 ? 1 : T == 4 ? 2 : 3;
-    constexpr int newer = NWP + (T < 8 ? T : 8);
-    lgkm_le<2 * (3 - pair) + newer>();
-    asm volatile("" : "+v"(fc.a[pair]), "+v"(fc.b[pair]));
+// MFMA slot T of a k-step (LAST: the second of the slice) from fragments fa,
+// fb, with the next k-step's reads into fa (rotating) and fn: the wait, the
+// MFMA, the reads; in the first k-step the A DMAs of the next slice (rows
+// 4..7 of each thread) after MFMAs 16, 20, 24, 28; in the last the slice
+// barrier before MFMA 32 and the A DMAs of the slice after next (rows 0..3,
+// into the A stage this slice leaves) after MFMAs 32, 36, 40, 44; in both
+// the B DMAs of the slice after next after MFMAs 18, 26, 50, 58 (rows 0..3
+// in the first, 4..7 in the last).  The barrier waits for the next slice's
+// A DMAs (the last issued at MFMA 28 of the first k-step, followed by 4 B
+// DMAs) and its B DMAs (issued a slice earlier).
+template <int T, bool LAST, bool DUAL, class DmaA, class DmaB>
+__device__ __forceinline__ void big_slot(FragA& fa, FragB& fb, FragB& fn, AccBig& acc,
+                                         uint32_t pa, uint32_t pb, DmaA& dma_a, DmaB& dma_b) {
+  constexpr int i = T / 8, j = T % 8;
+  constexpr int w = LAST ? kWait1[T] : kWait0[T];
+  if constexpr (w >= 0) {
+    lgkm_le<w>();
+    asm volatile("" : "+v"(fa.a[i]), "+v"(fb.b[j]));
     sched_fence();
   }
-  constexpr int i = kSqI[T], j = kSqJ[T];
-  acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc.a[i], fc.b[j], acc[i][j], 0, 0, 0);
+  if constexpr (LAST && T == 32) {
+    asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    asm volatile("" : "+v"(fa.a[i]), "+v"(fb.b[j]));
+    sched_fence();
+  }
+  // the accumulators stay in AGPRs (with the builtin the allocator moved some
+  // through VGPRs inside the loop)
+  asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+               : "+a"(acc[i][j])
+               : "v"(fa.a[i]), "v"(fb.b[j]));
   sched_fence();
-  if constexpr (T < 8) {
-    big_read<DUAL, T>(fn, pa, pb);
+  big_read<DUAL, LAST ? kRead1a[T] : kRead0a[T]>(fa, fn, pa, pb);
+  big_read<DUAL, LAST ? kRead1b[T] : kRead0b[T]>(fa, fn, pa, pb);
+  if constexpr (!LAST && (T == 16 || T == 20 || T == 24 || T == 28)) {
+    dma_a(4 + (T - 16) / 4);
     sched_fence();
   }
-  if constexpr (T == 8 || T == 12) {
-    fetch(l0 + (T - 8) / 4);
+  if constexpr (LAST && (T == 32 || T == 36 || T == 40 || T == 44)) {
+    dma_a((T - 32) / 4);
     sched_fence();
   }
-  if constexpr (T == 10 || T == 14) {
-    dma(l0 + (T - 10) / 4);
+  if constexpr (T == 18 || T == 26 || T == 50 || T == 58) {
+    dma_b((LAST ? 4 : 0) + (T == 18 ? 0 : T == 26 ? 1 : T == 50 ? 2 : 3));
     sched_fence();
   }
-  if constexpr ((T == 9 || T == 11 || T == 13) && (T - 9) / 2 < NW) {
-    put(w0 + (T - 9) / 2);
-    sched_fence();
-  }
-  if constexpr (T < 15)
-    big_slot<T + 1, DUAL, NWP, NW>(fc, fn, acc, pa, pb, fetch, dma, l0, put, w0);
-}
-
-// Last k-step of a slice: MFMAs 0..7 on fragments read in the previous
-// k-step (whose 2 writes followed them), then the slice barrier, then MFMAs
-// 8..15 with the next slice's first fragment reads after each and the last
-// fetch / DMA of the slice.  The barrier waits for this wave's DMAs of the
-// next slice: in issue order they are followed by at most VM newer
-// vector-memory operations (this slice's fetches and DMAs so far).
-template <int T, bool DUAL, int VM, class Fetch, class Dma>
-__device__ __forceinline__ void big_slot_last(Frag8& fc, Frag8& fn, Acc44& acc, uint32_t pa,
-                                              uint32_t pb, Fetch& fetch, Dma& dma, int l0) {
-  if constexpr (T == 0 || T == 1 || T == 4) {
-    constexpr int pair = T == 0 ? 0 : T == 1 ? 1 : 2;
-    lgkm_le<2 * (3 - pair) + 2>();
-    asm volatile("" : "+v"(fc.a[pair]), "+v"(fc.b[pair]));
-    sched_fence();
-  }
-  if constexpr (T == 8) {
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(VM) : "memory");
-    asm volatile("" : "+v"(fc.a[3]), "+v"(fc.b[3]));
-    sched_fence();
-  }
-  constexpr int i = kSqI[T], j = kSqJ[T];
-  acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc.a[i], fc.b[j], acc[i][j], 0, 0, 0);
-  sched_fence();
-  if constexpr (T >= 8) {
-    big_read<DUAL, T - 8>(fn, pa, pb);
-    sched_fence();
-  }
-  if constexpr (T == 8 || T == 12) {
-    fetch(l0 + (T - 8) / 4);
-    sched_fence();
-  }
-  if constexpr (T == 10 || T == 14) {
-    dma(l0 + (T - 10) / 4);
-    sched_fence();
-  }
-  if constexpr (T < 15) big_slot_last<T + 1, DUAL, VM>(fc, fn, acc, pa, pb, fetch, dma, l0);
+  if constexpr (T < 63) big_slot<T + 1, LAST, DUAL>(fa, fb, fn, acc, pa, pb, dma_a, dma_b);
 }
 
 // LDS of the large-group core: A stages at s0 and s0 + AB (slice parity), B
@@ -806,46 +769,35 @@ struct BigLds {
   __device__ __forceinline__ uint32_t b(int g) const { return s0 + big::B0 + (g % 3) * big::BB; }
 };
 
-// One slice g from A stage H = g & 1 and B stage g mod 3: Rf receives A of
-// slice g + 2 (src), B of slice g + 2 is DMAed into B stage (g + 2) mod 3
-// (free: its last reader was slice g - 1, before that slice's barrier), and
-// Rp (A of slice g + 1) goes to the other A stage.  8 fetches, 8 DMAs and 8
-// writes per thread; the writes go out in the first three k-steps (3, 3, 2)
-// and the barrier in the last k-step waits for the DMAs of slice g + 1
-// (issued during slice g - 1, followed by this slice's 12 fetches and DMAs
-// of its first three k-steps).
-template <bool DUAL, int H>
+// One 64-wide slice g: two k-steps of 32 from A stage g & 1 and B stage
+// g mod 3
+template <bool DUAL>
 __device__ __forceinline__ void big_half(const BigLds& L, int g, int wave, const BigRows& q,
-                                         const BigSrc& src, Acc44& acc,
-                                         const uint32_t (&a_lane)[4],
-                                         const uint32_t (&b_lane)[4], uint32_t w_lane, Frag8& f0,
-                                         Frag8& f1, BigStage& Rf, BigStage& Rp) {
+                                         int nk, AccBig& acc, const uint32_t (&a_lane)[2],
+                                         const uint32_t (&b_lane)[2], FragA& fa, FragB& fb0,
+                                         FragB& fb1) {
   const uint32_t ca = L.a(g), cb = L.b(g), na = L.a(g + 1), nb = L.b(g + 1), db = L.b(g + 2);
-  auto fetch = [&](int u) { big_fetch(Rf, q, src, u); };
-  auto dma = [&](int u) { big_dma<DUAL>(db, wave, q, src, u); };
-  auto put = [&](int u) { big_put_rt(na + w_lane, Rp, u); };
-  big_slot<0, DUAL, 0, 3>(f0, f1, acc, ca + a_lane[1], cb + b_lane[1], fetch, dma, 0, put, 0);
-  big_slot<0, DUAL, 3, 3>(f1, f0, acc, ca + a_lane[2], cb + b_lane[2], fetch, dma, 2, put, 3);
-  big_slot<0, DUAL, 3, 2>(f0, f1, acc, ca + a_lane[3], cb + b_lane[3], fetch, dma, 4, put, 6);
-  big_slot_last<0, DUAL, 12>(f1, f0, acc, na + a_lane[0], nb + b_lane[0], fetch, dma, 6);
+  const BigSrc sa(q, g + 1, nk), sb(q, g + 2, nk);
+  auto dma_a = [&](int u) { big_dma_a(na, wave, q, sa, u); };
+  auto dma_a2 = [&](int u) { big_dma_a(ca, wave, q, sb, u); };
+  auto dma_b = [&](int u) { big_dma<DUAL>(db, wave, q, sb, u); };
+  big_slot<0, false, DUAL>(fa, fb0, fb1, acc, ca + a_lane[1], cb + b_lane[1], dma_a, dma_b);
+  big_slot<0, true, DUAL>(fa, fb1, fb0, acc, na + a_lane[0], nb + b_lane[0], dma_a2, dma_b);
 }
 
 // C tile += A rows x B rows over nk slices from the rows' K origin; returns
 // with every load landed and every wave past its last LDS access
 template <bool DUAL>
-__device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Acc44& acc,
-                                         const uint32_t (&a_lane)[4], const uint32_t (&b_lane)[4],
-                                         uint32_t w_lane) {
+__device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, AccBig& acc,
+                                         const uint32_t (&a_lane)[2],
+                                         const uint32_t (&b_lane)[2]) {
   const BigLds L{lds_addr(lds)};
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  BigStage R0, R1;
-  // prologue: A of slice 0 to R0, B of slice 0 to B stage 0, A of slice 1
-  // to R1, B of slice 1 to B stage 1; R0 into A stage 0
   {
     const BigSrc s0(q, 0, nk), s1(q, 1, nk);
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      big_fetch(R0, q, s0, u);
+      big_dma_a(L.a(0), wave, q, s0, u);
       sched_fence();
     }
 #pragma unroll
@@ -855,47 +807,51 @@ __device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Ac
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      big_fetch(R1, q, s1, u);
-      sched_fence();
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
       big_dma<DUAL>(L.b(1), wave, q, s1, u);
       sched_fence();
     }
-  }
 #pragma unroll
-  for (int u = 0; u < 8; ++u) big_put_rt(L.a(0) + w_lane, R0, u);
-  // B of slice 0 has landed (16 newer operations: A and B of slice 1)
-  asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
-  Frag8 f0, f1;
-  const uint32_t pa = L.a(0) + a_lane[0], pb = L.b(0) + b_lane[0];
-  big_read<DUAL, 0>(f0, pa, pb);
-  big_read<DUAL, 1>(f0, pa, pb);
-  big_read<DUAL, 2>(f0, pa, pb);
-  big_read<DUAL, 3>(f0, pa, pb);
-  big_read<DUAL, 4>(f0, pa, pb);
-  big_read<DUAL, 5>(f0, pa, pb);
-  big_read<DUAL, 6>(f0, pa, pb);
-  big_read<DUAL, 7>(f0, pa, pb);
-  // two slices per trip (R0 and R1 swap roles); for an odd count the last
-  // trip's second slice is the zero slice past the end
-  for (int g = 0; g < nk; g += 2) {
-    big_half<DUAL, 0>(L, g, wave, q, BigSrc(q, g + 2, nk), acc, a_lane, b_lane, w_lane, f0, f1,
-                      R0, R1);
-    big_half<DUAL, 1>(L, g + 1, wave, q, BigSrc(q, g + 3, nk), acc, a_lane, b_lane, w_lane, f0,
-                      f1, R1, R0);
+    for (int u = 0; u < 4; ++u) {
+      big_dma_a(L.a(1), wave, q, s1, u);
+      sched_fence();
+    }
   }
-  // the zero slices fetched past the end drain before the registers and
-  // stages are reused
-  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  // A and B of slice 0 have landed (12 newer operations: B of slice 1 and
+  // the first half of its A)
+  asm volatile("s_waitcnt vmcnt(12)\n\ts_barrier" ::: "memory");
+  // the first k-step's fragments, in the order the last k-step of a slice
+  // reads them (the first k-step's waits count on it)
+  FragA fa;
+  FragB fb0, fb1;
+  const uint32_t pa = L.a(0) + a_lane[0], pb = L.b(0) + b_lane[0];
+  big_read<DUAL, 0>(fa, fb0, pa, pb);
+  big_read<DUAL, 1>(fa, fb0, pa, pb);
+  big_read<DUAL, 2>(fa, fb0, pa, pb);
+  big_read<DUAL, 3>(fa, fb0, pa, pb);
+  big_read<DUAL, 4>(fa, fb0, pa, pb);
+  big_read<DUAL, 5>(fa, fb0, pa, pb);
+  big_read<DUAL, 6>(fa, fb0, pa, pb);
+  big_read<DUAL, 7>(fa, fb0, pa, pb);
+  big_read<DUAL, 8>(fa, fb0, pa, pb);
+  big_read<DUAL, 9>(fa, fb0, pa, pb);
+  big_read<DUAL, 11>(fa, fb0, pa, pb);
+  big_read<DUAL, 13>(fa, fb0, pa, pb);
+  big_read<DUAL, 15>(fa, fb0, pa, pb);
+  big_read<DUAL, 10>(fa, fb0, pa, pb);
+  big_read<DUAL, 12>(fa, fb0, pa, pb);
+  big_read<DUAL, 14>(fa, fb0, pa, pb);
+  for (int g = 0; g < nk; ++g)
+    big_half<DUAL>(L, g, wave, q, nk, acc, a_lane, b_lane, fa, fb0, fb1);
+  // the last MFMAs' results are in their AGPRs before anything reads them
+  // (the compiler does not see the inline MFMAs' write latency)
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier\n\ts_nop 7\n\ts_nop 7" ::: "memory");
 }
 
 // ---------------------------------------------- large-group epilogues --
-// Activation tile (MODE 0 SwiGLU: silu(g) u with g, u from accumulators j + 2
+// Activation tile (MODE 0 SwiGLU: silu(g) u with g, u from accumulators j + 4
 // and j; MODE 1 ReLU) as bf16 through LDS, so that it leaves as 16-byte row
 // chunks instead of one 2-byte store per element.  A lane holds one column
-// of 16 rows per accumulator; lanes c and c ^ 1 swap one value of each row
+// of 4 rows per accumulator; lanes c and c ^ 1 swap one value of each row
 // pair (rows r, r + 1) so that each holds two adjacent columns of one row,
 // which v_cvt_pk_bf16_f32 packs (round to nearest even) into one dword of
 // the LDS image [256 rows][NT columns].  Every wave's LDS accesses of the
@@ -903,34 +859,33 @@ __device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Ac
 // barrier), and it ends on a barrier before the next tile's operands go to
 // LDS.
 template <int MODE>
-__device__ __forceinline__ void big_store_act(char* lds, const FfnArgs& a, Acc44& acc, int m0,
+__device__ __forceinline__ void big_store_act(char* lds, const FfnArgs& a, AccBig& acc, int m0,
                                               int n0, int a_valid, int b_valid, int wm, int wn,
                                               int lane) {
   constexpr bool DUAL = MODE == 0;
   constexpr int NT = DUAL ? 128 : 256;      // output columns of the tile
   constexpr int RS = NT * 2 + (DUAL ? 16 : 0);  // LDS bytes per row (padded when it fits)
   static_assert(256 * RS <= big::LDS, "activation tile fits the stages");
-  const int c = lane & 31, hi = lane >> 5;
+  const int c = lane & 15, h = lane >> 4;
   const bool odd = c & 1;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < (DUAL ? 2 : 4); ++j) {
-      const int col = (DUAL ? wn * 64 : wn * 128) + 32 * j + (c & ~1);
+    for (int j = 0; j < (DUAL ? 4 : 8); ++j) {
+      const int col = (DUAL ? wn * 64 : wn * 128) + 16 * j + (c & ~1);
 #pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const int r = 2 * s;
+      for (int r = 0; r < 4; r += 2) {
         float v0, v1;
         if constexpr (DUAL) {
-          v0 = silu_mul(acc[i][j + 2][r], acc[i][j][r]);
-          v1 = silu_mul(acc[i][j + 2][r + 1], acc[i][j][r + 1]);
+          v0 = silu_mul(acc[i][j + 4][r], acc[i][j][r]);
+          v1 = silu_mul(acc[i][j + 4][r + 1], acc[i][j][r + 1]);
         } else {
           v0 = fmaxf(acc[i][j][r], 0.f);
           v1 = fmaxf(acc[i][j][r + 1], 0.f);
         }
         const float got = swap_pair(odd ? v0 : v1);
         const uint32_t w = odd ? pack_bf16x2(got, v1) : pack_bf16x2(v0, got);
-        const int row = wm * 128 + 32 * i + 8 * (r >> 2) + 4 * hi + (r & 3) + (odd ? 1 : 0);
+        const int row = wm * 128 + 16 * i + 4 * h + r + (odd ? 1 : 0);
         *reinterpret_cast<uint32_t*>(lds + row * RS + col * 2) = w;
       }
     }
@@ -952,40 +907,40 @@ __device__ __forceinline__ void big_store_act(char* lds, const FfnArgs& a, Acc44
   __syncthreads();
 }
 
-// fp32 down partials straight from the accumulators: per store, 32 lanes
-// write 128 contiguous bytes of one row.  Addresses are a per-lane 32-bit
-// offset from the tile's first element plus a wave-uniform one per
+// fp32 down partials straight from the accumulators: per store, 16 lanes
+// write 64 contiguous bytes of each of 4 rows.  Addresses are a per-lane
+// 32-bit offset from the tile's first element plus a wave-uniform one per
 // accumulator row (an SGPR), so nothing per element is kept across tiles;
 // full tiles skip the per-element bounds tests.
 template <bool CHECK>
-__device__ __forceinline__ void big_store_partial_rows(Acc44& acc, __amdgpu_buffer_rsrc_t ro,
+__device__ __forceinline__ void big_store_partial_rows(AccBig& acc, __amdgpu_buffer_rsrc_t ro,
                                                        uint32_t voff, int N, int rl, int cl,
                                                        int a_valid, int b_valid) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 8; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (CHECK && cl + 32 * j >= b_valid) continue;
+    for (int j = 0; j < 8; ++j) {
+      if (CHECK && cl + 16 * j >= b_valid) continue;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int dr = 32 * i + 8 * (r >> 2) + (r & 3);
+      for (int r = 0; r < 4; ++r) {
+        const int dr = 16 * i + r;
         if (CHECK && rl + dr >= a_valid) continue;
         // through a VGPR: stored straight from the accumulator registers, every
-        // element of a 32 x 32 block came out as its first one
+        // element of a block came out as its first one
         float v = acc[i][j][r];
         asm volatile("" : "+v"(v));
         __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), ro, voff,
-                                              (uint32_t)((dr * N + 32 * j) * 4), 0);
+                                              (uint32_t)((dr * N + 16 * j) * 4), 0);
       }
     }
 }
 
 // tile partials to `out` (the tile's first element; rows ld floats apart)
-__device__ __forceinline__ void big_store_partial(float* out, int ld, Acc44& acc, int a_valid,
+__device__ __forceinline__ void big_store_partial(float* out, int ld, AccBig& acc, int a_valid,
                                                   int b_valid, int wm, int wn, int lane) {
   asm volatile("" : "+s"(ld));  // per-tile value: keeps the offsets below inside the tile loop
-  const int c = lane & 31, hi = lane >> 5;
-  const int rl = wm * 128 + 4 * hi, cl = wn * 128 + c;  // the lane's first row and column
+  const int c = lane & 15, h = lane >> 4;
+  const int rl = wm * 128 + 4 * h, cl = wn * 128 + c;  // the lane's first row and column
   const __amdgpu_buffer_rsrc_t ro = buf_rsrc(out);
   const uint32_t voff = (uint32_t)((rl * ld + cl) * 4);
   if (a_valid == big::BM && b_valid == big::BN)
@@ -1032,12 +987,13 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
   const int dense_m1 = a.dense_rows ? *a.dense_rows : 0;
   const int n_mt = a.dense_rows ? (dense_m1 + big::BM - 1) / big::BM : *a.n_tiles;
   const bool sk = MODE == 2 && a.sk_flag != nullptr;
-  // per-lane LDS offsets of the fragments, per k-step (16-byte chunk swizzle)
-  const int fr = lane & 31, hi = lane >> 5;
-  uint32_t a_lane[4], b_lane[4];
+  // per-lane LDS offsets of the fragments, per 32-wide k-step (row l % 16,
+  // 16-byte chunk 4 ks + l / 16 of the slice, swizzled)
+  const int fr = lane & 15, hk = lane >> 4;
+  uint32_t a_lane[2], b_lane[2];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const uint32_t ch = ((2 * ks + hi) ^ swz(fr)) << 4;
+  for (int ks = 0; ks < 2; ++ks) {
+    const uint32_t ch = ((4 * ks + hk) ^ swz(fr)) << 4;
     a_lane[ks] = (wm * 128 + fr) * big::RB + ch;
     b_lane[ks] = ((DUAL ? wn * 64 : wn * 128) + fr) * big::RB + ch;
   }
@@ -1046,9 +1002,8 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
   // so the stage holds the swizzled layout the fragment reads expect
   const int r0 = tid >> 3;
   const int cc = 8 * ((tid & 7) ^ swz(r0));
-  const uint32_t w_lane = r0 * big::RB + (tid & 7) * 16;
   const __amdgpu_buffer_rsrc_t ra = buf_rsrc(a.X);
-  Acc44 acc;
+  AccBig acc;
   // output tile (mt, nt) over K slices [ka, ka + nkp) into partial slot sp
   // of its rows, or (cslot >= 0, down GEMM) compact partial cslot
   auto piece = [&](int mt, int nt, int ka, int nkp, int sp, int cslot) {
@@ -1083,10 +1038,10 @@ __global__ __launch_bounds__(big::THREADS) void k_ffn_big(FfnArgs a) {
       q.off[8 + u] = (uint32_t)(((size_t)min(col, b_valid - 1) * a.K + k0 + cc) * 2);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
-    big_tile<DUAL>(lds, q, nkp, acc, a_lane, b_lane, w_lane);
+      for (int j = 0; j < 8; ++j) acc[i][j] = f32x4_t{};
+    big_tile<DUAL>(lds, q, nkp, acc, a_lane, b_lane);
     if constexpr (MODE == 2) {
       if (cslot >= 0)
         big_store_partial(a.sk_part + (size_t)cslot * big::BM * big::BN, big::BN, acc, a_valid,
@@ -1360,67 +1315,71 @@ __device__ __forceinline__ void exit_big_rows(BigRows& q, const ExitArgs& a, con
 // and the sum of 2^(y - max y) over the tile's vocabulary rows.  Two passes
 // over the accumulators (the logit z is recomputed, nothing written back):
 // the largest z, then sum 2^(z log2 e - max y), one FMA and one v_exp_f32
-// per logit.  Partial tiles (last vocabulary tile, or a bias) take the bias
-// and row mask in both passes.  The tile's loads have all landed by now (the
-// next tile fetches its first slices after this), so the LDS exchange waits
-// for LDS work only.
+// per logit.  A lane holds 4 rows of one token column per accumulator; the
+// four row groups of a column (lanes l, l ^ 16, l ^ 32, l ^ 48) combine by
+// lane exchange, the two row halves of the tile in LDS.  Partial tiles (last
+// vocabulary tile, or a bias) take the bias and row mask in both passes.
+// The tile's loads have all landed by now, so the LDS exchange waits for LDS
+// work only.
 __device__ __forceinline__ void exit_big_epilogue(const ExitArgs& a, const TileSched& S, int n_x,
-                                                  int jt, const Acc44& acc,
+                                                  int jt, const AccBig& acc,
                                                   float2 (*s_part)[big::BN], int wm, int wn,
                                                   int lane) {
   int vt, tt, sp;
   S.decode(jt, vt, tt, sp);
   const int v0 = vt * big::BM, c0 = tt * big::BN;
   const int a_valid = min(big::BM, a.V - v0), b_valid = min(big::BN, n_x - c0);
-  const int hi = lane >> 5;
+  const int h = lane >> 4;
   const float ninf = -__builtin_inff();
   const float kLog2e = 1.4426950408889634f;
   const bool full = a_valid == big::BM && !a.bias;
-  // this lane's rows are wm * 128 + 4 hi + o, o = 32 i + 8 (r / 4) + r % 4;
-  // row o is valid for o < lim, and bias row min(o, lim - 1) stays in range
-  const int lim = a_valid - (wm * 128 + 4 * hi);
-  const float* bias = a.bias ? a.bias + v0 + wm * 128 + 4 * hi : nullptr;
+  // this lane's rows are wm * 128 + 4 h + o, o = 16 i + r; row o is valid for
+  // o < lim, and bias row min(o, lim - 1) stays in range
+  const int lim = a_valid - (wm * 128 + 4 * h);
+  const float* bias = a.bias ? a.bias + v0 + wm * 128 + 4 * h : nullptr;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < 8; ++j) {
     float mz = ninf;
     if (full) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) mz = fmaxf(mz, acc[i][j][r]);
+        for (int r = 0; r < 4; ++r) mz = fmaxf(mz, acc[i][j][r]);
     } else {
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < 8; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int o = 32 * i + 8 * (r >> 2) + (r & 3);
+        for (int r = 0; r < 4; ++r) {
+          const int o = 16 * i + r;
           const float b = bias ? bias[min(o, lim - 1)] : 0.f;
           mz = fmaxf(mz, o < lim ? acc[i][j][r] + b : ninf);
         }
     }
+    mz = fmaxf(mz, __shfl_xor(mz, 16));
     mz = fmaxf(mz, __shfl_xor(mz, 32));
     const float m = mz * kLog2e;
     float sum = 0.f;
     if (mz != ninf) {
       if (full) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 8; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -m));
+          for (int r = 0; r < 4; ++r) sum += __builtin_amdgcn_exp2f(fmaf(acc[i][j][r], kLog2e, -m));
       } else {
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < 8; ++i)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int o = 32 * i + 8 * (r >> 2) + (r & 3);
+          for (int r = 0; r < 4; ++r) {
+            const int o = 16 * i + r;
             const float b = bias ? bias[min(o, lim - 1)] : 0.f;
             const float e = __builtin_amdgcn_exp2f(fmaf(acc[i][j][r] + b, kLog2e, -m));
             sum += o < lim ? e : 0.f;
           }
       }
     }
+    sum += __shfl_xor(sum, 16);
     sum += __shfl_xor(sum, 32);
-    if (lane < 32) s_part[wm][wn * 128 + 32 * j + lane] = make_float2(m, sum);
+    if (lane < 16) s_part[wm][wn * 128 + 16 * j + lane] = make_float2(m, sum);
   }
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   const int c = threadIdx.x;
@@ -1451,28 +1410,27 @@ __global__ __launch_bounds__(big::THREADS) void k_exit_big(ExitArgs a) {
   if (!S.init(a.n_vtiles, (n_x + big::BN - 1) / big::BN, 1, ntiles)) return;
   clock_mark(a.clk, true);
   const int nk = a.K / BK;
-  const int fr = lane & 31, hi = lane >> 5;
-  uint32_t a_lane[4], b_lane[4];
+  const int fr = lane & 15, hk = lane >> 4;
+  uint32_t a_lane[2], b_lane[2];
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const uint32_t ch = ((2 * ks + hi) ^ swz(fr)) << 4;
+  for (int ks = 0; ks < 2; ++ks) {
+    const uint32_t ch = ((4 * ks + hk) ^ swz(fr)) << 4;
     a_lane[ks] = (wm * 128 + fr) * big::RB + ch;
     b_lane[ks] = (wn * 128 + fr) * big::RB + ch;
   }
   const int r0 = tid >> 3;
   const int cc = 8 * ((tid & 7) ^ swz(r0));
-  const uint32_t w_lane = r0 * big::RB + (tid & 7) * 16;
   BigRows q;
   q.ra = buf_rsrc(a.W);
   q.none = buf_rsrc_empty(a.W);
-  Acc44 acc;
+  AccBig acc;
   for (int jt = 0; jt < ntiles; ++jt) {
     exit_big_rows(q, a, S, n_x, jt, r0, cc);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 8; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = f32x16_t{};
-    big_tile<false>(lds, q, nk, acc, a_lane, b_lane, w_lane);
+      for (int j = 0; j < 8; ++j) acc[i][j] = f32x4_t{};
+    big_tile<false>(lds, q, nk, acc, a_lane, b_lane);
     exit_big_epilogue(a, S, n_x, jt, acc, s_part, wm, wn, lane);
   }
   clock_mark(a.clk, false);
