@@ -74,8 +74,8 @@ __device__ __forceinline__ int acc_col(int wn, int j, int lane) {
 // ------------------------------------------------ direct-to-LDS pipeline --
 // gfx950's global_load_lds_dwordx4 moves a wavefront's 64 x 16 bytes from
 // global memory straight into LDS at a wave-uniform base (lane l at base +
-// 16 l): no staging VGPRs and no ds_write, which is what the register-staged
-// core above spends most of its non-MFMA issue time on.  Three LDS stages
+// 16 l): no staging VGPRs and no ds_write (the two things a register-staged
+// operand path spends most of its non-MFMA issue time on).  Three LDS stages
 // form a ring: slice g+2 is in flight while slice g is computed and slice
 // g+1 has landed.  Lane l of the DMA that covers tile rows r..r+7 loads row
 // r + l/8, chunk (l % 8) ^ swz(row), so the LDS image is the same swizzled
