@@ -640,17 +640,52 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 // into the same registers right after it, while the b fragments alternate
 // between two sets.  Per MFMA slot T: the lgkmcnt wait before it (-1: none;
 // the value counts the LDS reads issued after the ones it needs, capped at
-// the counter's 15, which only waits longer), and the fragment reads after it
-// (q = 2 n for a_n, 2 n + 1 for b_n; -1: none), for the first k-step of a
-// slice (0) and the last (1: its reads, of the next slice, follow the slice
-// barrier before MFMA 32).  The first k-step waits on the last k-step's
-// read order and the last k-step on the first's.
-constexpr int kWait0[64] = {14, 13, 12, 11, 10, 10, 10, 10, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, 15, -1, -1, -1, -1, -1, -1, -1, 15, -1, -1, -1, -1, -1, -1, -1, 15, -1, -1, -1, -1, -1, -1, -1};
-constexpr int kWait1[64] = {7, -1, -1, -1, -1, -1, -1, -1, 6, -1, -1, -1, -1, -1, -1, -1, 5, -1, -1, -1, -1, -1, -1, -1, 4, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1};
-constexpr int kRead0a[64] = {1, 3, 5, 7, 9, 11, 13, 15, -1, -1, -1, -1, -1, -1, -1, 2, -1, -1, -1, -1, -1, -1, -1, 4, -1, -1, -1, -1, -1, -1, -1, 6, -1, -1, -1, -1, -1, -1, -1, 8, -1, -1, -1, -1, -1, -1, -1, 10, -1, -1, -1, -1, -1, -1, -1, 12, -1, -1, -1, -1, -1, -1, -1, 14};
-constexpr int kRead0b[64] = {-1, -1, -1, -1, -1, -1, -1, 0, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1};
-constexpr int kRead1a[64] = {-1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, 0, 1, 2, 3, 4, 5, 6, 7, 8, 9, -1, 11, -1, 13, -1, 15, 10, -1, -1, -1, -1, -1, -1, -1, 12, -1, -1, -1, -1, -1, -1, 14};
-constexpr int kRead1b[64] = {-1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1, -1};
+// the counter's 15, which only waits longer), and the fragment read after it
+// (q = 2 n for a_n, 2 n + 1 for b_n; -1: none; the first k-step also reads
+// the next a_0 after MFMA 7), for the first k-step of a slice (0) and the
+// last (1: its reads, of the next slice, follow the slice barrier before
+// MFMA 32).  The first k-step waits on the last k-step's read order and the
+// last k-step on the first's.
+constexpr int kWait0[64] = {
+    14, 13, 12, 11, 10, 10, 10, 10,  // MFMAs 0..7
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 8..15
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 16..23
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 24..31
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 32..39
+    15, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 40..47
+    15, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 48..55
+    15, -1, -1, -1, -1, -1, -1, -1   // MFMAs 56..63
+};
+constexpr int kWait1[64] = {
+     7, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 0..7
+     6, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 8..15
+     5, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 16..23
+     4, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 24..31
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 32..39
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 40..47
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 48..55
+    -1, -1, -1, -1, -1, -1, -1, -1   // MFMAs 56..63
+};
+constexpr int kRead0[64] = {
+     1,  3,  5,  7,  9, 11, 13, 15,  // MFMAs 0..7
+    -1, -1, -1, -1, -1, -1, -1,  2,  // MFMAs 8..15
+    -1, -1, -1, -1, -1, -1, -1,  4,  // MFMAs 16..23
+    -1, -1, -1, -1, -1, -1, -1,  6,  // MFMAs 24..31
+    -1, -1, -1, -1, -1, -1, -1,  8,  // MFMAs 32..39
+    -1, -1, -1, -1, -1, -1, -1, 10,  // MFMAs 40..47
+    -1, -1, -1, -1, -1, -1, -1, 12,  // MFMAs 48..55
+    -1, -1, -1, -1, -1, -1, -1, 14   // MFMAs 56..63
+};
+constexpr int kRead1[64] = {
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 0..7
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 8..15
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 16..23
+    -1, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 24..31
+     0,  1,  2,  3,  4,  5,  6,  7,  // MFMAs 32..39
+     8,  9, -1, 11, -1, 13, -1, 15,  // MFMAs 40..47
+    10, -1, -1, -1, -1, -1, -1, -1,  // MFMAs 48..55
+    12, -1, -1, -1, -1, -1, -1, 14   // MFMAs 56..63
+};
 
 // B fragment j of a wavefront: LDS row offset from its first B row.  DUAL:
 // columns j = 0..3 of the up operand (rows 0..127 of the B stage), j = 4..7
@@ -744,8 +779,9 @@ __device__ __forceinline__ void big_slot(FragA& fa, FragB& fb, FragB& fn, AccBig
                : "+a"(acc[i][j])
                : "v"(fa.a[i]), "v"(fb.b[j]));
   sched_fence();
-  big_read<DUAL, LAST ? kRead1a[T] : kRead0a[T]>(fa, fn, pa, pb);
-  big_read<DUAL, LAST ? kRead1b[T] : kRead0b[T]>(fa, fn, pa, pb);
+  big_read<DUAL, LAST ? kRead1[T] : kRead0[T]>(fa, fn, pa, pb);
+  // the first k-step's a_0 for the next k-step, after its last use
+  if constexpr (!LAST && T == 7) big_read<DUAL, 0>(fa, fn, pa, pb);
   if constexpr (!LAST && (T == 16 || T == 20 || T == 24 || T == 28)) {
     dma_a(4 + (T - 16) / 4);
     sched_fence();
