@@ -1,0 +1,163 @@
+"""Generated-code checks of the large-group GEMM core (CPU: hipcc cross-compiles).
+
+The core issues its MFMAs as inline asm (so that its accumulators stay in
+AGPRs), which hides their write latency from the compiler: the code must not
+read, copy or overwrite an accumulator register before the MFMA that writes
+it has finished, and the hand-ordered slice loop must not spill.  Both are
+properties of the code the compiler emits, so this test compiles gemm.hip for
+gfx950 with the library's flags and checks the assembly of the large-group
+kernels:
+
+* no scratch access inside the slice loops (the innermost loops that issue
+  MFMAs);
+* along every control-flow path from an MFMA, no instruction other than
+  another MFMA touches its destination AGPRs within 19 wait states (the
+  most a 16-pass XDL MFMA asks of a following VALU access; `s_nop N`
+  counts N + 1, every other instruction 1).
+"""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2608_00573_amd", "csrc")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+KERNELS = {
+    "k_ffn_big<0>": "_ZN7trimmoe9k_ffn_bigILi0EEEvNS_7FfnArgsE",
+    "k_ffn_big<1>": "_ZN7trimmoe9k_ffn_bigILi1EEEvNS_7FfnArgsE",
+    "k_ffn_big<2>": "_ZN7trimmoe9k_ffn_bigILi2EEEvNS_7FfnArgsE",
+    "k_exit_big": "_ZN7trimmoe10k_exit_bigENS_8ExitArgsE",
+}
+WAIT_STATES = 19
+
+pytestmark = pytest.mark.skipif(not shutil.which(HIPCC) and not os.path.exists(HIPCC),
+                                reason="hipcc not available")
+
+
+@pytest.fixture(scope="module")
+def asm(tmp_path_factory):
+    out = tmp_path_factory.mktemp("gemm_asm") / "gemm.s"
+    cmd = [HIPCC, "--offload-arch=gfx950", "-O3", "-std=c++17", "-Xclang", "-target-feature",
+           "-Xclang", "-packed-fp32-ops", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           "--cuda-device-only", "-S", os.path.join(CSRC, "gemm.hip"), "-o", str(out)]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-2000:]
+    return out.read_text()
+
+
+def _function(text, name):
+    start = text.index(f"\n{name}:") + 1
+    end = text.index(".Lfunc_end", start)
+    body = []
+    for line in text[start:end].splitlines()[1:]:
+        line = line.split(";")[0].strip()
+        if line and not line.startswith("."):
+            body.append(line)
+        elif re.match(r"^\.LBB\d+_\d+:", line):
+            body.append(line)
+    return body
+
+
+def _agprs(ins):
+    regs = set()
+    for lo, hi in re.findall(r"\ba\[(\d+):(\d+)\]", ins):
+        regs.update(range(int(lo), int(hi) + 1))
+    for r in re.findall(r"\ba(\d+)\b", ins):
+        regs.add(int(r))
+    return regs
+
+
+def _cfg(body):
+    labels = {l[:-1]: i for i, l in enumerate(body) if l.endswith(":")}
+
+    def succ(i):
+        ins = body[i]
+        op = ins.split()[0] if not ins.endswith(":") else ""
+        out = []
+        if op.startswith("s_branch") or op.startswith("s_cbranch"):
+            out.append(labels[ins.split()[-1]])
+        if not (op.startswith("s_branch") or op.startswith("s_endpgm") or
+                op.startswith("s_setpc")):
+            if i + 1 < len(body):
+                out.append(i + 1)
+        return out
+    return succ
+
+
+def _hazards(body):
+    succ = _cfg(body)
+    found = []
+    for i, ins in enumerate(body):
+        if not ins.startswith("v_mfma"):
+            continue
+        dst = _agprs(ins.split(",")[0])
+        # bounded search over paths: (position, wait states left)
+        stack = [(j, WAIT_STATES) for j in succ(i)]
+        seen = set()
+        while stack:
+            j, left = stack.pop()
+            if left <= 0 or (j, left) in seen:
+                continue
+            seen.add((j, left))
+            cur = body[j]
+            cost = 0
+            if not cur.endswith(":"):
+                if not cur.startswith("v_mfma") and _agprs(cur) & dst:
+                    found.append((i, ins, j, cur))
+                    continue
+                m = re.match(r"s_nop\s+(\d+)", cur)
+                cost = int(m.group(1)) + 1 if m else 1
+            for k in succ(j):
+                stack.append((k, left - cost))
+    return found
+
+
+def _loops_with_mfma(body):
+    """(start, end) index ranges of the innermost loops (a backward branch)
+    that issue MFMAs: the slice loops, not the tile loops around them, whose
+    per-tile code may spill"""
+    labels = {l[:-1]: i for i, l in enumerate(body) if l.endswith(":")}
+    loops = []
+    for i, ins in enumerate(body):
+        if ins.startswith("s_cbranch") or ins.startswith("s_branch"):
+            t = labels.get(ins.split()[-1])
+            if t is not None and t < i and any(b.startswith("v_mfma") for b in body[t:i]):
+                loops.append((t, i))
+    return [(s, e) for s, e in loops
+            if not any((s2, e2) != (s, e) and s <= s2 and e2 <= e for s2, e2 in loops)]
+
+
+@pytest.mark.parametrize("kernel", list(KERNELS))
+def test_no_spill_in_mfma_loops(asm, kernel):
+    body = _function(asm, KERNELS[kernel])
+    loops = _loops_with_mfma(body)
+    assert loops, "no MFMA loop found"
+    for s, e in loops:
+        spills = [b for b in body[s:e] if b.startswith("scratch_") or "Spill" in b]
+        assert not spills, (kernel, spills[:4])
+
+
+@pytest.mark.parametrize("kernel", list(KERNELS))
+def test_no_early_accumulator_access(asm, kernel):
+    body = _function(asm, KERNELS[kernel])
+    assert any(b.startswith("v_mfma") for b in body)
+    bad = _hazards(body)
+    assert not bad, [(kernel, m, a) for _, m, _, a in bad[:4]]
+
+
+def test_checker_finds_a_planted_hazard():
+    # a read of an MFMA result right after it, and the same read after wait states
+    body = ["v_mfma_f32_16x16x32_bf16 a[0:3], v[0:3], v[4:7], a[0:3]",
+            "v_accvgpr_read_b32 v8, a2", "s_endpgm"]
+    assert _hazards(body)
+    body = ["v_mfma_f32_16x16x32_bf16 a[0:3], v[0:3], v[4:7], a[0:3]",
+            "s_nop 7", "s_nop 7", "s_nop 7", "v_accvgpr_read_b32 v8, a2", "s_endpgm"]
+    assert not _hazards(body)
+    # through a branch to a block that copies the accumulator
+    body = ["v_mfma_f32_16x16x32_bf16 a[4:7], v[0:3], v[4:7], a[4:7]",
+            "s_branch .LBB0_2", ".LBB0_1:", "s_endpgm", ".LBB0_2:",
+            "v_accvgpr_mov_b32 a9, a5", "s_branch .LBB0_1"]
+    assert _hazards(body)
