@@ -878,11 +878,13 @@ __device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Ac
   big_read<DUAL, 14>(fa, fb0, pa, pb);
   for (int g = 0; g < nk; ++g)
     big_half<DUAL>(L, g, wave, q, nk, acc, a_lane, b_lane, fa, fb0, fb1);
-  // the last MFMAs' results are in their AGPRs before anything reads them:
-  // the compiler does not see the inline MFMAs' write latency, so the wait
-  // states follow the last k-step's final row of MFMAs as an asm statement
-  // that takes those accumulators (no read of them moves above it; the
-  // other rows were written at least 8 MFMAs earlier)
+  // the last MFMAs' results must be in their AGPRs before anything reads
+  // them, and the compiler does not see the inline MFMAs' write latency: the
+  // wait states follow the loop in an asm statement that takes the last row
+  // of accumulators (the other rows were written at least 8 MFMAs earlier).
+  // The compiler may still place its own accumulator copies between the
+  // loop and this statement, so the emitted code is checked for any access
+  // to an MFMA's destination within 19 wait states of it.
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier\n\ts_nop 7\n\ts_nop 7"
                : "+a"(acc[7][0]), "+a"(acc[7][1]), "+a"(acc[7][2]), "+a"(acc[7][3]),
                  "+a"(acc[7][4]), "+a"(acc[7][5]), "+a"(acc[7][6]), "+a"(acc[7][7])
