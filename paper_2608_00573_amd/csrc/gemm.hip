@@ -878,14 +878,25 @@ __device__ __forceinline__ void big_tile(char* lds, const BigRows& q, int nk, Ac
   big_read<DUAL, 14>(fa, fb0, pa, pb);
   for (int g = 0; g < nk; ++g)
     big_half<DUAL>(L, g, wave, q, nk, acc, a_lane, b_lane, fa, fb0, fb1);
+  // The last k-step read the first fragments of the slice past the end
+  // (never used).  Those reads land whenever the LDS returns them, which the
+  // compiler cannot see: the wait for them takes their registers as inputs,
+  // so no other value is put there before they have landed.
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)"
+               :
+               : "v"(fa.a[0]), "v"(fa.a[1]), "v"(fa.a[2]), "v"(fa.a[3]), "v"(fa.a[4]),
+                 "v"(fa.a[5]), "v"(fa.a[6]), "v"(fa.a[7])
+               : "memory");
+  asm volatile("" ::"v"(fb0.b[0]), "v"(fb0.b[1]), "v"(fb0.b[2]), "v"(fb0.b[3]), "v"(fb0.b[4]),
+               "v"(fb0.b[5]), "v"(fb0.b[6]), "v"(fb0.b[7]));
   // the last MFMAs' results must be in their AGPRs before anything reads
   // them, and the compiler does not see the inline MFMAs' write latency: the
-  // wait states follow the loop in an asm statement that takes the last row
-  // of accumulators (the other rows were written at least 8 MFMAs earlier).
+  // wait states follow in an asm statement that takes the last row of
+  // accumulators (the other rows were written at least 8 MFMAs earlier).
   // The compiler may still place its own accumulator copies between the
   // loop and this statement, so the emitted code is checked for any access
   // to an MFMA's destination within 19 wait states of it.
-  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier\n\ts_nop 7\n\ts_nop 7"
+  asm volatile("s_barrier\n\ts_nop 7\n\ts_nop 7"
                : "+a"(acc[7][0]), "+a"(acc[7][1]), "+a"(acc[7][2]), "+a"(acc[7][3]),
                  "+a"(acc[7][4]), "+a"(acc[7][5]), "+a"(acc[7][6]), "+a"(acc[7][7])
                :

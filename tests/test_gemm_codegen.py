@@ -13,7 +13,10 @@ kernels:
 * along every control-flow path from an MFMA, no instruction other than
   another MFMA touches its destination AGPRs within 19 wait states (the
   most a 16-pass XDL MFMA asks of a following VALU access; `s_nop N`
-  counts N + 1, every other instruction 1).
+  counts N + 1, every other instruction 1);
+* along every path from an LDS read, its destination registers are neither
+  read nor written before an lgkmcnt wait shows it landed (the explicit
+  waits of the hand-ordered loop are checked this way too).
 """
 import os
 import re
@@ -115,6 +118,60 @@ def _hazards(body):
     return found
 
 
+def _vgprs(ins):
+    regs = set()
+    for lo, hi in re.findall(r"\bv\[(\d+):(\d+)\]", ins):
+        regs.update(range(int(lo), int(hi) + 1))
+    for r in re.findall(r"\bv(\d+)\b", ins):
+        regs.add(int(r))
+    return regs
+
+
+_SMEM = ("s_load", "s_buffer_load", "s_memtime", "s_memrealtime", "s_scratch_load", "s_dcache")
+
+
+def _lds_races(body, limit=4000):
+    """Accesses to the destination VGPRs of an LDS read before the read is
+    known to have landed.  Along every path from a ds_read the read is known
+    to have landed at an `s_waitcnt lgkmcnt(N)` once N or more LDS operations
+    were issued after it (LDS operations return in order), or at
+    lgkmcnt(0) once a scalar memory operation (which may return out of order)
+    was issued; before that, any instruction that reads or writes one of its
+    destination registers is a race (the compiler cannot see the inline-asm
+    reads' latency, so nothing else orders them)."""
+    succ = _cfg(body)
+    found = []
+    for p, ins in enumerate(body):
+        if not ins.startswith("ds_read"):
+            continue
+        dst = _vgprs(ins.split(",")[0])
+        stack = [(j, 0, False, 0) for j in succ(p)]
+        seen = set()
+        while stack:
+            j, after, smem, depth = stack.pop()
+            key = (j, min(after, 64), smem)
+            if key in seen or depth > limit:
+                continue
+            seen.add(key)
+            cur = body[j]
+            if not cur.endswith(":"):
+                m = re.search(r"lgkmcnt\((\d+)\)", cur)
+                if cur.startswith("s_waitcnt") and m:
+                    n = int(m.group(1))
+                    if n == 0 or (not smem and after >= n):
+                        continue
+                if _vgprs(cur) & dst:
+                    found.append((p, ins, j, cur))
+                    continue
+                if cur.startswith("ds_"):
+                    after += 1
+                elif cur.startswith(_SMEM):
+                    smem = True
+            for k in succ(j):
+                stack.append((k, after, smem, depth + 1))
+    return found
+
+
 def _loops_with_mfma(body):
     """(start, end) index ranges of the innermost loops (a backward branch)
     that issue MFMAs: the slice loops, not the tile loops around them, whose
@@ -146,6 +203,33 @@ def test_no_early_accumulator_access(asm, kernel):
     assert any(b.startswith("v_mfma") for b in body)
     bad = _hazards(body)
     assert not bad, [(kernel, m, a) for _, m, _, a in bad[:4]]
+
+
+@pytest.mark.parametrize("kernel", list(KERNELS))
+def test_lds_reads_land_before_their_registers_are_used(asm, kernel):
+    body = _function(asm, KERNELS[kernel])
+    bad = _lds_races(body)
+    assert not bad, [(kernel, r, a) for _, r, _, a in bad[:4]]
+
+
+def test_race_checker_finds_planted_races():
+    ok = ["ds_read_b128 v[0:3], v9", "ds_read_b128 v[4:7], v9 offset:16",
+          "s_waitcnt lgkmcnt(1)", "v_mov_b32 v10, v1", "s_endpgm"]
+    assert not _lds_races(ok)
+    # the wait is one read too weak for the first read
+    weak = ["ds_read_b128 v[0:3], v9", "ds_read_b128 v[4:7], v9 offset:16",
+            "s_waitcnt lgkmcnt(2)", "v_mov_b32 v10, v1", "s_endpgm"]
+    assert _lds_races(weak)
+    # a register of a read still in flight written on the way out of a loop
+    loop = ["ds_read_b128 v[0:3], v9", ".LBB0_1:", "s_waitcnt lgkmcnt(0)",
+            "ds_read_b128 v[0:3], v9", "s_cbranch_scc1 .LBB0_1", "v_sub_u32 v2, s4, 1",
+            "s_waitcnt lgkmcnt(0)", "s_endpgm"]
+    assert _lds_races(loop)
+    # a scalar load in between: only lgkmcnt(0) orders the read
+    smem = ["ds_read_b128 v[0:3], v9", "ds_read_b128 v[4:7], v9 offset:16",
+            "s_load_dword s0, s[2:3], 0x0", "s_waitcnt lgkmcnt(1)", "v_mov_b32 v10, v1",
+            "s_endpgm"]
+    assert _lds_races(smem)
 
 
 def test_checker_finds_a_planted_hazard():
