@@ -6,7 +6,8 @@ read, copy or overwrite an accumulator register before the MFMA that writes
 it has finished, and the hand-ordered slice loop must not spill.  Both are
 properties of the code the compiler emits, so this test compiles gemm.hip for
 gfx950 with the library's flags and checks the assembly of the large-group
-kernels:
+kernels (and, for the LDS reads and spills, the first core's kernels, whose
+fragment reads are inline asm with explicit waits as well):
 
 * no scratch access inside the slice loops (the innermost loops that issue
   MFMAs);
@@ -210,6 +211,31 @@ def test_lds_reads_land_before_their_registers_are_used(asm, kernel):
     body = _function(asm, KERNELS[kernel])
     bad = _lds_races(body)
     assert not bad, [(kernel, r, a) for _, r, _, a in bad[:4]]
+
+
+def _first_core(asm):
+    # every instance of the first core's kernels (inline-asm fragment reads
+    # with explicit waits, MFMAs by builtin)
+    names = re.findall(r"^(_ZN7trimmoe\w*k_(?:ffn|exit)_mma\w*):", asm, re.M)
+    assert names
+    return names
+
+
+def test_first_core_lds_reads_land_before_use(asm):
+    for name in _first_core(asm):
+        bad = _lds_races(_function(asm, name))
+        assert not bad, [(name, r, a) for _, r, _, a in bad[:4]]
+
+
+def test_first_core_hot_loops_do_not_spill(asm):
+    # the offline argmax variant of the exit tile (Lb1E) is not on the hot path
+    for name in _first_core(asm):
+        if "k_exit_mma" in name and name.endswith("Lb1EEEvNS_8ExitArgsE"):
+            continue
+        body = _function(asm, name)
+        for s, e in _loops_with_mfma(body):
+            spills = [b for b in body[s:e] if b.startswith("scratch_")]
+            assert not spills, (name, spills[:4])
 
 
 def test_race_checker_finds_planted_races():
