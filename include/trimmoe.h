@@ -75,7 +75,7 @@ extern "C" {
  * 1 <= la_subs <= 4, and with O = (1 + la_subs)^k + 1 options per token:
  * O * trans_b^k <= 1024 first-level branches per token,
  * O^H * trans_b^(k (H - 1)) <= 2^23 cost evaluations per token, and the route
- * block's look-ahead tables within 150 KB of LDS */
+ * block's look-ahead tables within 148 KB of LDS */
 #define TRIMMOE_MAX_HORIZON 4
 #define TRIMMOE_MAX_LOOKAHEAD_TOPK 4
 #define TRIMMOE_MAX_TRANS_B 8

@@ -260,8 +260,8 @@ hipError_t launch_exit_head(const LayerParams& p, bool bf16, hipStream_t st);
 int down_splits(int max_tiles, int N, int K);
 // dynamic LDS of a route block (logits, and the look-ahead tables at H > 1)
 size_t route_lds_bytes(bool bf16, int E, int d, int horizon, int trans_b, int k, int la_subs);
-// dynamic LDS a route block may take next to its static arrays (gfx950: 160 KB
-// per workgroup)
-constexpr size_t kRouteLdsMax = 150 * 1024;
+// dynamic LDS a route block may take next to its static arrays (about 10 KB;
+// gfx950: 160 KB per workgroup)
+constexpr size_t kRouteLdsMax = 148 * 1024;
 
 }  // namespace trimmoe

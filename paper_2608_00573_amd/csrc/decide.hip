@@ -395,6 +395,22 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   const int E = p.E, d = p.d, k = p.k;
   for (int e = threadIdx.x; e < E; e += blockDim.x) s_cnt[e] = 0;
   if (threadIdx.x == 0) s_xcnt = 0;
+  // the decision's per-expert and per-token inputs, loaded here so that
+  // their latency overlaps the substitute table and the router logits
+  // instead of adding round trips after them
+  __shared__ uint8_t s_local[TRIMMOE_MAX_EXPERTS];
+  __shared__ float s_bias[TRIMMOE_MAX_EXPERTS];
+  for (int e = threadIdx.x; e < E; e += blockDim.x) {
+    s_local[e] = p.local_mask[e] ? 1 : 0;
+    s_bias[e] = p.b_router ? p.b_router[e] : 0.f;
+  }
+  int t_pre = 0;
+  float d_pre = 0.f, budget_pre = 0.f;
+  if ((int)threadIdx.x < nt) {
+    t_pre = p.active_idx[base + threadIdx.x];
+    d_pre = p.d_acc[t_pre];
+    budget_pre = p.budget_tok ? p.budget_tok[t_pre] : p.budget;
+  }
 
   // Eq. (3): the layer's substitute table, one wavefront per expert
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -562,7 +578,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
       float* z = zs + ti * E;
       const float ninf = -__builtin_inff();
       for (int e = g; e < E; e += G) {
-        const float v = z[e] + (p.b_router ? p.b_router[e] : 0.f);
+        const float v = z[e] + s_bias[e];
         z[e] = (v == v) ? v : ninf;
       }
       float vprev = 0.f, vtop[KMAX];
@@ -630,16 +646,16 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
   const float* candq = LA ? la.candq0 : s_subq;
   if (i < nt) {
     pos = base + i;
-    t = p.active_idx[pos];
+    t = t_pre;
     I = sI[i];
 
-    budget = p.budget_tok ? p.budget_tok[t] : p.budget;
-    D = p.d_acc[t];
+    budget = budget_pre;
+    D = d_pre;
     // resolve slots: local exact, or remote with or without candidates that
     // fit the budget
     for (int r = 0; r < k; ++r) {
       const int e = sS[i][r];
-      if (p.local_mask[e]) {
+      if (s_local[e]) {
         ++n_loc;
       } else {
         ++n_rem;
@@ -765,7 +781,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
     int nrows = 0, nsubst = 0, nremote = 0, nroute_remote = 0;
     for (int r = 0; r < k; ++r) {
       const int e = sS[i][r];
-      nroute_remote += !p.local_mask[e];
+      nroute_remote += !s_local[e];
       int x = -1, kind = TRIMMOE_KIND_NONE;
       if (!skip) {
         if ((bmask >> r) & 1) {
@@ -774,7 +790,7 @@ __global__ __launch_bounds__(64 * kRouteWaves) void k_route(LayerParams p) {
           ++nsubst;
         } else {
           x = e;
-          kind = p.local_mask[e] ? TRIMMOE_KIND_LOCAL : TRIMMOE_KIND_REMOTE;
+          kind = s_local[e] ? TRIMMOE_KIND_LOCAL : TRIMMOE_KIND_REMOTE;
           if (kind == TRIMMOE_KIND_REMOTE) ++nremote;
         }
         int j = 0;
