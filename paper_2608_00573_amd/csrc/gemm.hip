@@ -410,6 +410,29 @@ __device__ __forceinline__ float swap_pair(float v) {
                                                              0xf, false));
 }
 
+// The values of lanes l and l ^ 16 (lanes_xor16) or l and l ^ 32
+// (lanes_xor32) in every lane, by gfx950's permlane swaps instead of an LDS
+// exchange: (a, b) is (own, other) in lanes 0..15 (xor16: every even row of
+// 16 lanes) or 0..31 (xor32) and (other, own) in the rest, so a commutative
+// reduction of a and b gives every lane the pair's result.  The two results
+// are copied out of the returned pair before the bit casts: a bit cast of
+// the subscripted second element read the first one.
+struct LanePair {
+  float a, b;
+};
+__device__ __forceinline__ LanePair lanes_xor16(float x) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto r = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const unsigned r0 = r[0], r1 = r[1];
+  return {__builtin_bit_cast(float, r0), __builtin_bit_cast(float, r1)};
+}
+__device__ __forceinline__ LanePair lanes_xor32(float x) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const unsigned r0 = r[0], r1 = r[1];
+  return {__builtin_bit_cast(float, r0), __builtin_bit_cast(float, r1)};
+}
+
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   const bf16x2_t v = {(__bf16)lo, (__bf16)hi};
   return __builtin_bit_cast(uint32_t, v);
@@ -1242,12 +1265,13 @@ struct ExitSrc {
             mi = row;
           }
         }
-      const float m2 = __shfl_xor(m, 32);
-      const int mi2 = __shfl_xor(mi, 32);
-      if (m2 > m || (m2 == m && mi2 < mi)) {
-        m = m2;
-        mi = mi2;
-      }
+      // the better of the two row halves (ties to the lower row); lanes 0..31,
+      // the ones that store it, hold their own candidate in a
+      const LanePair pm = lanes_xor32(m), pi = lanes_xor32(__int_as_float(mi));
+      const int ia = __float_as_int(pi.a), ib = __float_as_int(pi.b);
+      const bool take_b = pm.b > pm.a || (pm.b == pm.a && ib < ia);
+      m = take_b ? pm.b : pm.a;
+      mi = take_b ? ib : ia;
       if (lane < 32) s_part[wm][acc_col<T>(wn, jj, lane)] = make_float2(m, __int_as_float(mi));
     }
     lds_barrier();
@@ -1303,7 +1327,10 @@ struct ExitSrc {
             m = fmaxf(m, y);
           }
       }
-      m = fmaxf(m, __shfl_xor(m, 32));
+      {
+        const LanePair pm = lanes_xor32(m);
+        m = fmaxf(pm.a, pm.b);
+      }
       float sum = 0.f;
       if (m != ninf) {
 #pragma unroll
@@ -1311,7 +1338,10 @@ struct ExitSrc {
 #pragma unroll
           for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(acc[i][jj][r] - m);
       }
-      sum += __shfl_xor(sum, 32);
+      {
+        const LanePair ps = lanes_xor32(sum);
+        sum = ps.a + ps.b;
+      }
       if (lane < 32) s_part[wm][acc_col<T>(wn, jj, lane)] = make_float2(m, sum);
     }
     lds_barrier();
@@ -1411,8 +1441,12 @@ __device__ __forceinline__ void exit_big_epilogue(const ExitArgs& a, const TileS
           mz = fmaxf(mz, o < lim ? acc[i][j][r] + b : ninf);
         }
     }
-    mz = fmaxf(mz, __shfl_xor(mz, 16));
-    mz = fmaxf(mz, __shfl_xor(mz, 32));
+    {
+      const LanePair p16 = lanes_xor16(mz);
+      mz = fmaxf(p16.a, p16.b);
+      const LanePair p32 = lanes_xor32(mz);
+      mz = fmaxf(p32.a, p32.b);
+    }
     const float m = mz * kLog2e;
     float sum = 0.f;
     if (mz != ninf) {
@@ -1433,8 +1467,12 @@ __device__ __forceinline__ void exit_big_epilogue(const ExitArgs& a, const TileS
           }
       }
     }
-    sum += __shfl_xor(sum, 16);
-    sum += __shfl_xor(sum, 32);
+    {
+      const LanePair p16 = lanes_xor16(sum);
+      sum = p16.a + p16.b;
+      const LanePair p32 = lanes_xor32(sum);
+      sum = p32.a + p32.b;
+    }
     if (lane < 16) s_part[wm][wn * 128 + 16 * j + lane] = make_float2(m, sum);
   }
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
