@@ -73,6 +73,24 @@ def test_large_expert_groups_skewed_ragged():
     _run_and_compare(cfg)
 
 
+def test_decode_sized_swiglu_split_down_ragged():
+    # a decode-sized batch (29 tokens, a few rows per expert) at bf16:
+    # d_model 576 leaves a partial 256-column down tile, d_ff 1152 gives the
+    # down GEMM two K splits, and the exit head takes its decode tile
+    # (vocabulary 1000: a partial 128-row tile)
+    cfg = workload("mixtral_8x7b_decode", n_tokens=29, n_layers=3, d_model=576, d_ff=1152,
+                   vocab_exit=1000)
+    _run_and_compare(cfg)
+
+
+def test_decode_sized_relu_top1_ragged_up():
+    # ReLU up tiles (256 columns) over d_ff 704 leave a partial tile; 32
+    # tokens over 8 experts
+    cfg = workload("switch_base_8e", n_tokens=32, n_layers=3, d_model=512, d_ff=704,
+                   vocab_exit=1000)
+    _run_and_compare(cfg)
+
+
 def test_wide_model_exit_head_ragged():
     # d_model 2048 at 1100 tokens: the exit head takes 256 x 256 tiles with
     # 4 wavefronts; 1100 tokens and 1000 vocabulary rows leave partial token
