@@ -307,3 +307,34 @@ def test_static_entry_validates_before_any_device_call():
     st.xi = None
     assert L.trimmoe_stack_forward_static(C.byref(mh.model), C.byref(pol), C.byref(st), None,
                                           None) == -1
+
+
+def test_empty_batch_is_a_no_op_without_device_calls():
+    # a batch of no tokens: every entry point that runs the path validates
+    # its arguments and returns TRIMMOE_OK before any device call, writing
+    # nothing (so this runs without a GPU)
+    mh = _handle()
+    L = abi.lib()
+    pol = abi.make_policy(**POL)
+    st, keep = _state_stub(T=0)
+    need = abi.trimmoe_workspace_size(mh.model, 0)
+    assert need > 0
+    big = torch.zeros(need + 512, dtype=torch.uint8)
+    off = (-big.data_ptr()) % 256
+    ws = big[off:off + need]
+    assert L.trimmoe_state_reset(C.byref(mh.model), C.byref(st), None) == 0
+    assert L.trimmoe_stack_forward(C.byref(mh.model), C.byref(pol), C.byref(st), None,
+                                   C.c_void_p(ws.data_ptr()), need, None) == 0
+    for layer in range(DIMS["n_layers"]):
+        assert L.trimmoe_layer_step(C.byref(mh.model), layer, C.byref(pol), C.byref(st), None,
+                                    C.c_void_p(ws.data_ptr()), need, None) == 0
+    assert L.trimmoe_stack_forward_static(C.byref(mh.model), C.byref(pol), C.byref(st), None,
+                                          None) == 0
+    # arguments are still checked first: a bad policy or a missing workspace
+    bad = abi.make_policy(**dict(POL, budget=-1.0))
+    assert L.trimmoe_stack_forward(C.byref(mh.model), C.byref(bad), C.byref(st), None,
+                                   C.c_void_p(ws.data_ptr()), need, None) == -4
+    assert L.trimmoe_stack_forward(C.byref(mh.model), C.byref(pol), C.byref(st), None, None,
+                                   need, None) == -6
+    assert torch.count_nonzero(keep) == 0
+    assert torch.count_nonzero(ws) == 0

@@ -122,6 +122,18 @@ def test_many_experts_bf16_top4_substitution():
     assert (gtr["action"] == O.ACT_SKIP).any()
 
 
+def test_max_experts_and_top_k_bf16():
+    # the library's maxima together: 256 SwiGLU experts, top-8, 128 of them
+    # local, bf16 (a whole wavefront per token in top-k and softmax, every
+    # token's Eq. (34) enumeration over 8 slots, up to 256 groups of a few
+    # rows in the expert GEMMs), 300 tokens (a ragged route block)
+    cfg = workload("qwen_moe_a2_7b", n_tokens=300, n_layers=2, d_model=128, d_ff=128,
+                   d_ff_shared=128, n_experts=256, n_local=128, top_k=8, vocab_exit=512)
+    _, _, gtr, _, _, _ = _run_and_compare(cfg)
+    assert (gtr["kind"] == O.KIND_SUB).any()
+    assert (gtr["action"] == O.ACT_SKIP).any()
+
+
 @pytest.mark.parametrize("E,k", [(8, 2), (60, 4)])
 def test_tied_router_logits_rank_lower_id_first(E, k):
     # router rows duplicated in pairs: experts 2j and 2j + 1 get bitwise equal
