@@ -46,6 +46,16 @@ def test_tiny_bf16_swiglu_top2_shared():
     _run_and_compare(cfg)
 
 
+@pytest.mark.parametrize("dtype,act", [("f32", "relu"), ("f32", "swiglu"), ("bf16", "relu")])
+def test_shared_expert_with_every_routed_activation(dtype, act):
+    # the shared expert (SwiGLU) beside ReLU or SwiGLU routed experts, on the
+    # fp32 path and beside ReLU on the bf16 path (the bf16 SwiGLU case is
+    # above); 200 tokens leave ragged route, row and token tiles
+    cfg = workload("tiny_fp32", dtype=dtype, act=act, top_k=2, normalize_topk=1,
+                   d_ff_shared=192, n_tokens=200, n_layers=3)
+    _run_and_compare(cfg)
+
+
 def test_large_batch_swiglu_top2_shared():
     # 6144 tokens: the 256-token exit-head tile; top-2 over 4 experts gives
     # long, ragged expert groups
